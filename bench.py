@@ -1,0 +1,185 @@
+#!/usr/bin/env python3
+"""Replayed anchor tokens/s of SuffixReplay state reconstruction on one MI355X.
+
+A step is one sr_replay_state call over the whole batch: projection GEMM,
+conv/gates, conv tail and the chunked scan for every segment and layer of the
+workload, inputs already resident in HBM.  Default workload: "varlen16", 16
+requests with suffixes of 64*U{8..64} anchor rows, D=2560, H_k=16, H_v=32,
+d_k=d_v=128, bf16 (the Qwen3.5-4B linear-layer shape), seeded synthetic data.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload varlen16]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+METRIC = "replayed anchor tokens/sec (state reconstruction) + % MFMA/HBM roofline"
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_work(wl, with_q=True):
+    """Per-launch algorithmic work of each kernel (flops for the MFMA GEMM,
+    HBM bytes for the streaming kernels), from the shapes alone."""
+    sh = wl.shape
+    T = wl.t_total
+    D, hk, hv, d, w = sh.d_model, sh.n_k_heads, sh.n_v_heads, sh.d_k, sh.conv_width
+    c_kv = (hk + hv) * d
+    N = c_kv + 2 * hv
+    es = 4 if sh.anchor_dtype == "f32" else 2             # k/v operand bytes
+    wb = {"f32": 4, "bf16": 2, "fp8_e4m3": 1}[sh.weight_dtype]
+    tb = 4 if sh.tail_dtype == "f32" else 2
+    live = [b for b, s in enumerate(wl.slot_ids) if s >= 0]
+    n_layers = len(wl.layers)
+    c_q = hk * d if with_q else 0
+    return {
+        # one launch per layer
+        "proj_gemm": ("mfma", 2.0 * T * D * N),
+        "conv_gate": ("hbm", T * N * 4 + T * c_kv * es + 2 * T * hv * 4),
+        "tail": ("hbm", c_q * D * wb + len(live) * (w - 1) * ((c_q + c_kv) * tb + D * es)),
+        # one launch covers all layers (up to 32)
+        "gdn_scan": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * d * d * 4)),
+    }
+
+
+def cpu_baseline(wl, budget_s=15.0):
+    """The fp64 oracle on a bounded sample of the same workload: whole
+    segments, in order, until ~budget_s of CPU work."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    cu = wl.cu_seqlens
+    lay = wl.layers[0]
+    rows = 0
+    segs = []
+    t0 = time.perf_counter()
+    for b in np.argsort(wl.seg_lens):          # shortest first keeps the sample bounded
+        if time.perf_counter() - t0 > budget_s:
+            break
+        oracle.replay_segment(wl.shape, lay, lay.anchors[cu[b]:cu[b + 1]])
+        rows += wl.seg_lens[b]
+        segs.append(int(b))
+    el = time.perf_counter() - t0
+    return {"value": rows / el, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{len(segs)} of {len(wl.seg_lens)} segments of layer 0 ({rows} anchor rows, "
+                      f"segments {segs}), fp64 numpy, {el:.1f} s; projection on {cores} BLAS threads, "
+                      f"recurrence single-threaded"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="varlen16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one MI355X: the replay path here runs on a single GPU "
+              f"(--gpus {args.gpus}, WORLD_SIZE {world} requested). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    from workloads.device import upload
+    import paper_2609_33477_amd as sr
+
+    log(f"generating workload {args.workload}")
+    wl = W.make_config(args.workload)
+    dev = upload(wl)
+    ws_bytes = sr.replay_workspace_size(wl.shape, len(wl.layers), wl.t_total)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    layers = [sr.LayerTensors(**vars(ns)) for ns in dev.layers]
+    n_seg = len(wl.seg_lens)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        sr.replay_state(wl.shape, layers, n_seg, wl.t_total, dev.cu_seqlens, dev.slot_ids, ws, ws_bytes, stream)
+
+    log(f"T={wl.t_total} rows x {len(wl.layers)} layers, workspace {ws_bytes / 2**20:.1f} MiB; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    sr.kernel_timing_enable(True)
+    sr.kernel_timing_read()                       # drop anything recorded before
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    ms_total = start.elapsed_time(stop)
+    kt = sr.kernel_timing_read()
+    sr.kernel_timing_enable(False)
+    ms_per_step = ms_total / args.steps
+    tokens = wl.replayed_tokens
+    value = tokens / (ms_per_step / 1e3)
+    log(f"{ms_per_step:.3f} ms/step (wall {wall_ms / args.steps:.3f}), {value / 1e6:.2f} M tokens/s")
+
+    work = algorithmic_work(wl, with_q=dev.with_q)
+    kernels = {}
+    for k, (tot, n) in kt.items():
+        if n == 0:
+            continue
+        bound, amount = work[k]
+        avg_ms = tot / n
+        if bound == "mfma":
+            dt = "f32" if wl.shape.anchor_dtype == "f32" else "bf16"
+            ach, peak, unit = amount / (avg_ms * 1e-3) / 1e12, PEAK_TFLOPS[dt], "TFLOP/s"
+        else:
+            ach, peak, unit = amount / (avg_ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
+        kernels[k] = {"avg_ms": round(avg_ms, 5), "launches_per_step": n / args.steps,
+                      "share": round(tot / max(sum(v[0] for v in kt.values()), 1e-12), 4),
+                      "bound": bound, "achieved": round(ach, 2), "peak": peak, "unit": unit,
+                      "frac": round(ach / peak, 4)}
+    dom = max(kernels, key=lambda k: kernels[k]["share"])
+    d = kernels[dom]
+    roofline = {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
+                "frac": d["frac"], "traffic": None, "kernel": dom}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on a bounded sample")
+        cpu = cpu_baseline(wl, args.cpu_budget_s)
+
+    sh = wl.shape
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32" if sh.anchor_dtype == "f32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "requests": n_seg, "layers": len(wl.layers), "t_total": wl.t_total,
+                   "replayed_tokens_per_step": tokens, "d_model": sh.d_model, "n_k_heads": sh.n_k_heads,
+                   "n_v_heads": sh.n_v_heads, "d_k": sh.d_k, "d_v": sh.d_v, "conv_width": sh.conv_width,
+                   "anchor_dtype": sh.anchor_dtype, "weight_dtype": sh.weight_dtype, "state_dtype": "f32"},
+        "latency_ms": round(ms_per_step, 4),
+        "roofline": roofline,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,184 @@
+"""ctypes binding of libsr_replay.so (argument marshalling only).
+
+Names mirror the C ABI in include/sr_replay.h: ``state_bytes``,
+``conv_tail_bytes``, ``replay_workspace_size``, ``replay_state``.  Tensors are
+PyTorch tensors on the current HIP device; only their ``data_ptr()`` values
+cross the boundary, and every step of the replay runs in the library's
+kernels.  If the library has not been built the import fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsr_replay.so")
+
+SR_F32, SR_BF16, SR_FP8_E4M3 = 0, 1, 2
+_DTYPE_CODES = {"f32": SR_F32, "bf16": SR_BF16, "fp8_e4m3": SR_FP8_E4M3,
+                SR_F32: SR_F32, SR_BF16: SR_BF16, SR_FP8_E4M3: SR_FP8_E4M3}
+
+STATUS_NAMES = {0: "SR_OK", 1: "SR_ERR_NULL_ARG", 2: "SR_ERR_BAD_SHAPE", 3: "SR_ERR_UNSUPPORTED_DTYPE",
+                4: "SR_ERR_WORKSPACE_TOO_SMALL", 5: "SR_ERR_MISALIGNED", 6: "SR_ERR_HIP"}
+
+
+class SrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class SrShape(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("n_k_heads", ctypes.c_int32), ("n_v_heads", ctypes.c_int32),
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("conv_width", ctypes.c_int32),
+                ("l2_eps", ctypes.c_float), ("anchor_dtype", ctypes.c_int32), ("weight_dtype", ctypes.c_int32),
+                ("conv_dtype", ctypes.c_int32), ("tail_dtype", ctypes.c_int32)]
+
+
+_LAYER_FIELDS = ("anchors", "w_k", "w_v", "w_a", "w_b", "w_q", "s_k", "s_v", "s_a", "s_b", "s_q",
+                 "conv_w", "a_log", "dt_bias", "state_in", "state_out", "tail_out")
+
+
+class SrLayer(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in _LAYER_FIELDS]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_33477_amd.build` "
+                          "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    lib.sr_state_bytes.argtypes = [P(SrShape)]
+    lib.sr_state_bytes.restype = ctypes.c_size_t
+    lib.sr_conv_tail_bytes.argtypes = [P(SrShape), ctypes.c_int32]
+    lib.sr_conv_tail_bytes.restype = ctypes.c_size_t
+    lib.sr_replay_workspace_size.argtypes = [P(SrShape), ctypes.c_int32, ctypes.c_int64, P(ctypes.c_size_t)]
+    lib.sr_replay_workspace_size.restype = ctypes.c_int
+    lib.sr_replay_state.argtypes = [P(SrShape), ctypes.c_int32, P(SrLayer), ctypes.c_int32, ctypes.c_int64,
+                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                    ctypes.c_void_p]
+    lib.sr_replay_state.restype = ctypes.c_int
+    lib.sr_kernel_timing_enable.argtypes = [ctypes.c_int32]
+    lib.sr_kernel_timing_enable.restype = ctypes.c_int
+    lib.sr_kernel_timing_read.argtypes = [P(ctypes.c_double), P(ctypes.c_int64)]
+    lib.sr_kernel_timing_read.restype = ctypes.c_int
+    lib.sr_status_str.argtypes = [ctypes.c_int]
+    lib.sr_status_str.restype = ctypes.c_char_p
+    return lib
+
+
+LIB = _load()
+
+EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
+                    "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_status_str")
+
+KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan")
+
+
+def make_shape(shape) -> SrShape:
+    """SrShape from any object with the sr_shape field names (dtype fields may
+    be the strings 'f32' / 'bf16' / 'fp8_e4m3' or the integer codes)."""
+    return SrShape(int(shape.d_model), int(shape.n_k_heads), int(shape.n_v_heads), int(shape.d_k),
+                   int(shape.d_v), int(shape.conv_width), float(shape.l2_eps),
+                   _DTYPE_CODES[shape.anchor_dtype], _DTYPE_CODES[shape.weight_dtype],
+                   _DTYPE_CODES[shape.conv_dtype], _DTYPE_CODES[shape.tail_dtype])
+
+
+def status_str(status: int) -> str:
+    return LIB.sr_status_str(int(status)).decode()
+
+
+def _check(status: int):
+    if status != 0:
+        raise SrError(status, status_str(status))
+
+
+def state_bytes(shape) -> int:
+    return int(LIB.sr_state_bytes(ctypes.byref(make_shape(shape))))
+
+
+def conv_tail_bytes(shape, with_q: bool = True) -> int:
+    return int(LIB.sr_conv_tail_bytes(ctypes.byref(make_shape(shape)), int(bool(with_q))))
+
+
+def replay_workspace_size(shape, n_layers: int, t_total: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(LIB.sr_replay_workspace_size(ctypes.byref(make_shape(shape)), int(n_layers), int(t_total),
+                                        ctypes.byref(out)))
+    return int(out.value)
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+@dataclass
+class LayerTensors:
+    """Device tensors of one layer; field names and layouts as sr_layer."""
+    anchors: object
+    w_k: object
+    w_v: object
+    w_a: object
+    w_b: object
+    conv_w: object
+    a_log: object
+    dt_bias: object
+    state_out: object
+    w_q: object = None
+    s_k: object = None
+    s_v: object = None
+    s_a: object = None
+    s_b: object = None
+    s_q: object = None
+    state_in: object = None
+    tail_out: object = None
+
+
+def make_layer_array(layers: Sequence[LayerTensors]):
+    arr = (SrLayer * len(layers))()
+    for i, L in enumerate(layers):
+        for name in _LAYER_FIELDS:
+            setattr(arr[i], name, _ptr(getattr(L, name)))
+    return arr
+
+
+def kernel_timing_enable(enable: bool = True):
+    _check(LIB.sr_kernel_timing_enable(int(bool(enable))))
+
+
+def kernel_timing_read():
+    """{kind: (total_ms, launches)} of the launches recorded since the last
+    read (waits for their events)."""
+    ms = (ctypes.c_double * len(KERNEL_KINDS))()
+    n = (ctypes.c_int64 * len(KERNEL_KINDS))()
+    _check(LIB.sr_kernel_timing_read(ms, n))
+    return {k: (ms[i], int(n[i])) for i, k in enumerate(KERNEL_KINDS)}
+
+
+def replay_state(shape, layers: Sequence[LayerTensors], n_segments: int, t_total: int, cu_seqlens,
+                 slot_ids=None, workspace=None, workspace_bytes: Optional[int] = None, stream=None):
+    """Enqueue sr_replay_state on `stream` (a torch.cuda.Stream, a raw
+    hipStream_t int, or None for torch's current stream).  Raises SrError on
+    a non-OK status."""
+    import torch  # plumbing: device memory and streams
+
+    if stream is None:
+        stream_ptr = torch.cuda.current_stream().cuda_stream
+    elif isinstance(stream, int):
+        stream_ptr = stream
+    else:
+        stream_ptr = stream.cuda_stream
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    sh = make_shape(shape)
+    arr = make_layer_array(layers)
+    status = LIB.sr_replay_state(ctypes.byref(sh), len(layers), arr, int(n_segments), int(t_total),
+                                 _ptr(cu_seqlens), _ptr(slot_ids), _ptr(workspace), int(workspace_bytes),
+                                 stream_ptr)
+    _check(status)

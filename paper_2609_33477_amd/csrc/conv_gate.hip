@@ -1,0 +1,300 @@
+// Fused short causal depthwise conv + SiLU + key L2 norm + decay/erase gates,
+// and the conv tail (Appendix A: the conv state is the last w-1 inputs of the
+// q, k, v channels).
+//
+// conv_gate_kernel: one wave per (row block, head); each lane owns d/64 (or one)
+// channels of the head and walks the block's rows, keeping the previous w-1
+// raw projection values in registers, so every projection element is read
+// from HBM once (plus a (w-1)-row halo per block).  History is masked at
+// segment starts: replay has no inputs before its first row.  Key heads are
+// L2-normalised with a wave reduction.  The last y-block of the grid computes
+// the per-(row, value head) gates:
+//   g = log alpha = -exp(A_log) * softplus(a + dt_bias),  beta = sigmoid(b).
+// Outputs are head-major ([H][T][d], [H][T]) so the scan reads each 64-row
+// chunk of a head as one contiguous block.
+//
+// tail_kernel: per (segment, 64 tail channels): q channels are projected from
+// the anchors of the segment's last w-1 rows (W_q is used nowhere else);
+// positions before the segment's first row are zero-filled for every channel.
+// The k | v channels of existing rows are written by conv_gate_kernel.
+#include "sr_device.hpp"
+
+#include <type_traits>
+
+namespace sr {
+namespace {
+
+constexpr int kRowsPerBlock = 64;
+constexpr int kConvThreads = 256;
+
+__device__ __forceinline__ int segment_of_row(const int32_t* cu, int n_seg, int64_t t) {
+  // Largest b with cu[b] <= t (skips empty segments): cu[b] <= t < cu[b+1].
+  int lo = 0, hi = n_seg;  // answer in [0, n_seg)
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (cu[mid] <= t) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ float silu(float y) { return y / (1.f + expf(-y)); }
+__device__ __forceinline__ float softplus(float x) { return fmaxf(x, 0.f) + log1pf(expf(-fabsf(x))); }
+__device__ __forceinline__ float sigmoid(float x) { return 1.f / (1.f + expf(-x)); }
+
+template <typename OUT, typename CW, typename TT, int DH>
+__global__ __launch_bounds__(kConvThreads) void conv_gate_kernel(ConvGateArgs a) {
+  constexpr int CPL = DH >= 64 ? DH / 64 : 1;   // channels per lane
+  constexpr int LPH = DH / CPL;                   // lanes per head
+  constexpr int HPW = 64 / LPH;                   // heads per wave
+  constexpr int WMAX = 4;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
+  const int64_t r1 = min(a.T, r0 + kRowsPerBlock);
+  const int n_heads = a.H_k + a.H_v;
+  const int C_kv = n_heads * DH;
+
+  if ((int)blockIdx.y == (int)gridDim.y - 1) {
+    // ---- gates: thread -> (head, row) with rows fastest for coalesced stores
+    const int rows = (int)(r1 - r0);
+    for (int idx = tid; idx < rows * a.H_v; idx += kConvThreads) {
+      const int h = idx / rows;
+      const int64_t t = r0 + idx % rows;
+      const float av = a.P[t * a.ldp + C_kv + h];
+      const float bv = a.P[t * a.ldp + C_kv + a.H_v + h];
+      a.Gbuf[(int64_t)h * a.T + t] = -expf(a.a_log[h]) * softplus(av + a.dt_bias[h]);
+      a.Bbuf[(int64_t)h * a.T + t] = sigmoid(bv);
+    }
+    return;
+  }
+
+  const int head = (blockIdx.y * (kConvThreads / 64) + wid) * HPW + lane / LPH;
+  const bool active = head < n_heads;
+  const bool is_k = head < a.H_k;
+  const int sub = lane % LPH;
+  const int c0 = (active ? head : 0) * DH + sub * CPL;   // channel of the first value
+  const int w = a.w;
+
+  float taps[CPL][WMAX];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q)
+#pragma unroll
+    for (int i = 0; i < WMAX; ++i) taps[q][i] = (i < w) ? Elem<CW>::load(a.conv_w, (int64_t)(c0 + q) * w + i) : 0.f;
+
+  // prev[j][q] = raw value at row t-1-j
+  float prev[WMAX - 1][CPL];
+#pragma unroll
+  for (int j = 0; j < WMAX - 1; ++j)
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      const int64_t t = r0 - 1 - j;
+      prev[j][q] = (j < w - 1 && t >= 0) ? a.P[t * a.ldp + c0 + q] : 0.f;
+    }
+
+  int b = segment_of_row(a.cu, a.n_seg, r0);
+  int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
+  int slot = a.slot_ids ? a.slot_ids[b] : b;
+
+  void* dst = is_k ? a.Kbuf : a.Vbuf;
+  const int hh = is_k ? head : head - a.H_k;
+
+  for (int64_t t = r0; t < r1; ++t) {
+    while (t >= s1) {
+      ++b;
+      s0 = a.cu[b];
+      s1 = a.cu[b + 1];
+      slot = a.slot_ids ? a.slot_ids[b] : b;
+    }
+    float raw[CPL], act[CPL];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) raw[q] = a.P[t * a.ldp + c0 + q];
+    float ss = 0.f;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      float y = taps[q][w - 1] * raw[q];
+#pragma unroll
+      for (int j = 0; j < WMAX - 1; ++j)
+        if (j < w - 1 && t - 1 - j >= s0) y = fmaf(taps[q][w - 2 - j], prev[j][q], y);
+      act[q] = silu(y);
+      ss = fmaf(act[q], act[q], ss);
+    }
+    if (is_k) {
+#pragma unroll
+      for (int off = LPH / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+      const float inv = 1.f / sqrtf(ss + a.eps);
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) act[q] *= inv;
+    }
+    if (active) {
+      const int64_t base = ((int64_t)hh * a.T + t) * DH + sub * CPL;
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) Elem<OUT>::store(dst, base + q, act[q]);
+      if (a.tail && slot >= 0 && t >= s1 - (w - 1)) {
+        const int pos = (int)(t - (s1 - (w - 1)));
+#pragma unroll
+        for (int q = 0; q < CPL; ++q)
+          Elem<TT>::store(a.tail, ((int64_t)slot * a.c_tail + a.tail_kv_off + c0 + q) * (w - 1) + pos, raw[q]);
+      }
+    }
+#pragma unroll
+    for (int j = WMAX - 2; j > 0; --j)
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) prev[j][q] = prev[j - 1][q];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) prev[0][q] = raw[q];
+  }
+}
+
+template <typename OUT, typename CW, typename TT, int DH>
+hipError_t run_conv(const ConvGateArgs& a, hipStream_t s) {
+  if (a.T == 0) return hipSuccess;
+  constexpr int CPL = DH >= 64 ? DH / 64 : 1;
+  constexpr int HPW = 64 / (DH / CPL);
+  const int heads_per_block = (kConvThreads / 64) * HPW;
+  const int n_heads = a.H_k + a.H_v;
+  dim3 grid((unsigned)((a.T + kRowsPerBlock - 1) / kRowsPerBlock),
+            (n_heads + heads_per_block - 1) / heads_per_block + 1);
+  hipLaunchKernelGGL((conv_gate_kernel<OUT, CW, TT, DH>), grid, dim3(kConvThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename OUT, typename CW, typename TT>
+hipError_t conv_by_head(int d, const ConvGateArgs& a, hipStream_t s) {
+  switch (d) {
+    case 32: return run_conv<OUT, CW, TT, 32>(a, s);
+    case 64: return run_conv<OUT, CW, TT, 64>(a, s);
+    case 128: return run_conv<OUT, CW, TT, 128>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename OUT, typename CW>
+hipError_t conv_by_tail(int tail_dtype, int d, const ConvGateArgs& a, hipStream_t s) {
+  if (tail_dtype == SR_F32) return conv_by_head<OUT, CW, float>(d, a, s);
+  if (tail_dtype == SR_BF16) return conv_by_head<OUT, CW, bf16_t>(d, a, s);
+  return hipErrorInvalidValue;
+}
+
+// ------------------------------------------------------------------ tail
+constexpr int kTailThreads = 256;
+constexpr int kTailChannels = 64;
+
+// 8 consecutive elements starting at element i, as fp32.
+template <typename T>
+__device__ __forceinline__ void load8(const void* p, int64_t i, float* out);
+template <>
+__device__ __forceinline__ void load8<bf16_t>(const void* p, int64_t i, float* out) {
+  const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i);
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    out[2 * j] = bf16_bits_to_f32(w[j] & 0xffffu);
+    out[2 * j + 1] = bf16_bits_to_f32(w[j] >> 16);
+  }
+}
+template <>
+__device__ __forceinline__ void load8<float>(const void* p, int64_t i, float* out) {
+  const float4* q = reinterpret_cast<const float4*>(static_cast<const float*>(p) + i);
+  const float4 x = q[0], y = q[1];
+  out[0] = x.x; out[1] = x.y; out[2] = x.z; out[3] = x.w;
+  out[4] = y.x; out[5] = y.y; out[6] = y.z; out[7] = y.w;
+}
+template <>
+__device__ __forceinline__ void load8<fp8_t>(const void* p, int64_t i, float* out) {
+  const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p) + i);
+  const uint32_t w[2] = {v.x, v.y};
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) out[4 * j + q] = e4m3_to_f32((w[j] >> (8 * q)) & 0xffu);
+}
+
+template <typename TA, typename TW, typename TT>
+__global__ __launch_bounds__(kTailThreads) void tail_kernel(TailArgs a) {
+  constexpr int WMAX = 4;
+  const int b = blockIdx.x;
+  const int slot = a.slot_ids ? a.slot_ids[b] : b;
+  if (slot < 0) return;
+  const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
+  const int w1 = a.w - 1;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int cb = blockIdx.y * kTailChannels;
+  const int ce = min(a.c_tail, cb + kTailChannels);
+
+  // zero-fill positions that precede the segment's first row
+  for (int idx = tid; idx < (ce - cb) * w1; idx += kTailThreads) {
+    const int c = cb + idx / w1, pos = idx % w1;
+    if (s1 - w1 + pos < s0) Elem<TT>::store(a.tail, ((int64_t)slot * a.c_tail + c) * w1 + pos, 0.f);
+  }
+  if (cb >= a.c_q) return;
+
+  // q channels: dot products of W_q rows with the last w-1 anchor rows
+  const int per_wave = kTailChannels / (kTailThreads / 64);
+  for (int ci = 0; ci < per_wave; ++ci) {
+    const int c = cb + wid * per_wave + ci;
+    if (c >= min(ce, a.c_q)) break;
+    float acc[WMAX - 1] = {0.f, 0.f, 0.f};
+    for (int k = lane * 8; k < a.D; k += 64 * 8) {
+      float wv[8];
+      load8<TW>(a.w_q, (int64_t)c * a.D + k, wv);
+#pragma unroll
+      for (int pos = 0; pos < WMAX - 1; ++pos) {
+        const int64_t t = s1 - w1 + pos;
+        if (pos < w1 && t >= s0) {
+          float xv[8];
+          load8<TA>(a.anchors, t * a.D + k, xv);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[pos] = fmaf(xv[j], wv[j], acc[pos]);
+        }
+      }
+    }
+#pragma unroll
+    for (int pos = 0; pos < WMAX - 1; ++pos)
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) acc[pos] += __shfl_xor(acc[pos], off);
+    if (lane == 0) {
+      const float scale = std::is_same<TW, fp8_t>::value ? Elem<bf16_t>::load(a.s_q, c) : 1.f;
+      for (int pos = 0; pos < w1; ++pos)
+        if (s1 - w1 + pos >= s0)
+          Elem<TT>::store(a.tail, ((int64_t)slot * a.c_tail + c) * w1 + pos, acc[pos] * scale);
+    }
+  }
+}
+
+template <typename TA, typename TW, typename TT>
+hipError_t run_tail(const TailArgs& a, hipStream_t s) {
+  if (a.n_seg == 0 || a.w < 2 || a.c_tail == 0) return hipSuccess;
+  dim3 grid(a.n_seg, (a.c_tail + kTailChannels - 1) / kTailChannels);
+  hipLaunchKernelGGL((tail_kernel<TA, TW, TT>), grid, dim3(kTailThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename TT>
+hipError_t tail_by_input(int ad, int wd, const TailArgs& a, hipStream_t s) {
+  if (ad == SR_F32 && wd == SR_F32) return run_tail<float, float, TT>(a, s);
+  if (ad == SR_BF16 && wd == SR_BF16) return run_tail<bf16_t, bf16_t, TT>(a, s);
+  if (ad == SR_BF16 && wd == SR_FP8_E4M3) return run_tail<bf16_t, fp8_t, TT>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_conv_gate(int op_dtype, int conv_dtype, int tail_dtype, int d_head,
+                            const ConvGateArgs& a, hipStream_t s) {
+  if (op_dtype == SR_F32) {
+    if (conv_dtype == SR_F32) return conv_by_tail<float, float>(tail_dtype, d_head, a, s);
+    if (conv_dtype == SR_BF16) return conv_by_tail<float, bf16_t>(tail_dtype, d_head, a, s);
+  } else if (op_dtype == SR_BF16) {
+    if (conv_dtype == SR_F32) return conv_by_tail<bf16_t, float>(tail_dtype, d_head, a, s);
+    if (conv_dtype == SR_BF16) return conv_by_tail<bf16_t, bf16_t>(tail_dtype, d_head, a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_tail(int anchor_dtype, int weight_dtype, int tail_dtype, const TailArgs& a,
+                       hipStream_t s) {
+  if (tail_dtype == SR_F32) return tail_by_input<float>(anchor_dtype, weight_dtype, a, s);
+  if (tail_dtype == SR_BF16) return tail_by_input<bf16_t>(anchor_dtype, weight_dtype, a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace sr

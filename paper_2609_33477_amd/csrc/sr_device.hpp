@@ -1,0 +1,114 @@
+// Device-side helpers shared by the replay kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sr_internal.hpp"
+
+namespace sr {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Storage tags: bf16 and fp8 tensors are handled as raw bits.
+struct bf16_t { uint16_t bits; };
+struct fp8_t { uint8_t bits; };
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) {
+  return __uint_as_float(h << 16);
+}
+
+// Round-to-nearest-even fp32 -> bf16 bits (NaN stays NaN); branch-free.
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t r = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t q = (u >> 16) | 0x40u;
+  return (uint16_t)(((u & 0x7fffffffu) > 0x7f800000u) ? q : r);
+}
+
+// OCP FP8 E4M3 -> bf16 bits, exact.  Normal: 2^(e-7) (1 + m/8); subnormal:
+// m 2^-9; e = 15, m = 7 is NaN.
+__device__ __forceinline__ uint32_t e4m3_to_bf16_bits(uint32_t b) {
+  const uint32_t s = (b & 0x80u) << 8;
+  const uint32_t e = (b >> 3) & 0xfu;
+  const uint32_t m = b & 0x7u;
+  if (e == 0) {
+    if (m == 0) return s;
+    // m * 2^-9 with m in 1..7: normalise the leading bit.
+    const uint32_t lead = 31u - __builtin_clz(m);           // 0..2
+    const uint32_t exp = 127u - 9u + lead;                    // biased bf16 exponent
+    const uint32_t mant = (m << (7u - lead)) & 0x7fu;
+    return s | (exp << 7) | mant;
+  }
+  if (e == 15 && m == 7) return s | 0x7fc0u;
+  return s | ((e + 120u) << 7) | (m << 4);
+}
+
+__device__ __forceinline__ float e4m3_to_f32(uint32_t b) {
+  return bf16_bits_to_f32(e4m3_to_bf16_bits(b));
+}
+
+// Generic scalar load/store of a storage element as fp32.
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static constexpr int bytes = 4;
+  __device__ static float load(const void* p, int64_t i) { return static_cast<const float*>(p)[i]; }
+  __device__ static void store(void* p, int64_t i, float v) { static_cast<float*>(p)[i] = v; }
+};
+template <> struct Elem<bf16_t> {
+  static constexpr int bytes = 2;
+  __device__ static float load(const void* p, int64_t i) {
+    return bf16_bits_to_f32(static_cast<const uint16_t*>(p)[i]);
+  }
+  __device__ static void store(void* p, int64_t i, float v) {
+    static_cast<uint16_t*>(p)[i] = f32_to_bf16_bits(v);
+  }
+};
+template <> struct Elem<fp8_t> {
+  static constexpr int bytes = 1;
+  __device__ static float load(const void* p, int64_t i) {
+    return e4m3_to_f32(static_cast<const uint8_t*>(p)[i]);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// MFMA 32x32 tiles.  Accumulator layout (both variants): lane l, register r
+// holds C[8*(r/4) + 4*(l/32) + (r%4)][l%32].  Operand layout: lane l supplies
+// A[l%32][k-slots] and B[k-slots][l%32]; the 32x32x16 bf16 form takes 8
+// consecutive k per lane (lanes 0-31: k 0-7, lanes 32-63: k 8-15), the
+// 32x32x2 f32 form one k per lane (lanes 0-31: k 0, lanes 32-63: k 1).
+// ---------------------------------------------------------------------------
+template <typename OP> struct Mfma;
+
+template <> struct Mfma<bf16_t> {
+  static constexpr int K = 16;      // k per instruction
+  static constexpr int HALF = 8;    // k per lane
+  typedef bf16x8 frag;
+  __device__ static void mma(f32x16& c, const frag& a, const frag& b) {
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <> struct Mfma<float> {
+  static constexpr int K = 2;
+  static constexpr int HALF = 1;
+  typedef float frag;
+  __device__ static void mma(f32x16& c, const frag& a, const frag& b) {
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+__device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+
+}  // namespace sr

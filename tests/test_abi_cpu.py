@@ -1,0 +1,124 @@
+"""CPU-side checks of the C-ABI library: it loads without a GPU, exports every
+function include/sr_replay.h declares, reproduces the paper's state and
+conv-state sizes (Appendix A), and rejects bad arguments on the host before
+any launch (no device work is started by these calls)."""
+import ctypes
+import json
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sr_replay.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden", "storage_table6.json")
+
+sr = pytest.importorskip("paper_2609_33477_amd.binding",
+                         reason="libsr_replay.so not built (run __graft_entry__.build())")
+from workloads import Shape, F32, BF16, FP8  # noqa: E402
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    # declarations: "<return type> sr_name(" at the start of a line
+    return sorted(set(re.findall(r"^(?:size_t|sr_status|const char\s*\*)\s*(sr_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_and_library_exports_every_function():
+    names = declared_functions()
+    assert set(names) == {"sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
+                          "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read",
+                          "sr_status_str"}
+    lib = ctypes.CDLL(sr.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(sr.EXPORTED_SYMBOLS)
+
+
+def test_size_helpers_match_paper_table():
+    tab = json.load(open(GOLDEN))
+    for name, m in tab["models"].items():
+        shape = Shape(m["d"], m["H_k"], m["H_v"], m["d_k"], m["d_v"], conv_width=tab["conv_width"])
+        assert sr.state_bytes(shape) == m["B_rec"], name
+        assert sr.conv_tail_bytes(shape, with_q=True) == m["B_conv"], name
+
+
+def test_status_strings():
+    for code in range(7):
+        assert isinstance(sr.status_str(code), str) and sr.status_str(code)
+    assert sr.status_str(99) == "unknown status"
+
+
+def test_workspace_size_plan():
+    shape = Shape(2560, 16, 32, 128, 128)
+    t = 36672
+    ws = sr.replay_workspace_size(shape, 1, t)
+    n = 16 * 128 + 32 * 128 + 64
+    # fp32 projection rows + bf16 k|v + fp32 log-alpha/beta, each 256-byte aligned
+    expect = t * n * 4 + t * (16 + 32) * 128 * 2 + 2 * t * 32 * 4
+    assert expect <= ws <= expect + 5 * 256
+    assert sr.replay_workspace_size(shape, 12, t) > 11 * (ws - t * n * 4)
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(d_model=100), 2), (dict(d_model=0), 2), (dict(n_k_heads=0), 2), (dict(n_v_heads=24, n_k_heads=16), 2),
+    (dict(d_k=96, d_v=96), 2), (dict(d_k=128, d_v=64), 2), (dict(conv_width=5), 2), (dict(l2_eps=0.0), 2),
+    (dict(anchor_dtype=F32, weight_dtype=BF16), 3), (dict(anchor_dtype=FP8), 3), (dict(tail_dtype=FP8), 3),
+])
+def test_workspace_size_rejects_bad_shapes(bad, code):
+    kw = dict(d_model=256, n_k_heads=2, n_v_heads=4, d_k=128, d_v=128)
+    kw.update({k: v for k, v in bad.items() if k in kw})
+    shape = Shape(**kw)
+    for k, v in bad.items():
+        setattr(shape, k, v)
+    with pytest.raises(sr.SrError) as e:
+        sr.replay_workspace_size(shape, 1, 128)
+    assert e.value.status == code
+
+
+def _fake_layer(**over):
+    # distinct 256-aligned fake addresses; validation never dereferences them
+    base = dict(anchors=0x10000, w_k=0x20000, w_v=0x30000, w_a=0x40000, w_b=0x50000, conv_w=0x60000,
+                a_log=0x70000, dt_bias=0x80000, state_out=0x90000)
+    base.update(over)
+    return sr.LayerTensors(**base)
+
+
+def _call(layers, shape=None, n_seg=1, t=64, cu=0xA0000, ws=0xB0000, ws_bytes=None, n_layers=None):
+    shape = shape or Shape(256, 2, 4, 128, 128)
+    if ws_bytes is None:
+        ws_bytes = sr.replay_workspace_size(shape, len(layers), t)
+    sh = sr.make_shape(shape)
+    arr = sr.make_layer_array(layers)
+    return sr.LIB.sr_replay_state(ctypes.byref(sh), len(layers) if n_layers is None else n_layers, arr,
+                                  n_seg, t, cu, None, ws, ws_bytes, None)
+
+
+def test_replay_state_host_validation():
+    assert _call([_fake_layer(w_v=None)]) == 1
+    assert _call([_fake_layer(state_out=None)]) == 1
+    assert _call([_fake_layer()], cu=None) == 1
+    assert _call([_fake_layer(anchors=0x10004)]) == 5
+    assert _call([_fake_layer()], ws=0xB0010) == 5
+    assert _call([_fake_layer()], ws_bytes=1024) == 4
+    assert _call([_fake_layer()], n_seg=-1) == 2
+    assert _call([_fake_layer()], n_seg=0, t=64) == 2
+    assert _call([_fake_layer()], t=-5, ws_bytes=1 << 30) == 2
+    assert _call([_fake_layer()], n_layers=0) == 2
+    fp8 = Shape(256, 2, 4, 128, 128, weight_dtype=FP8)
+    assert _call([_fake_layer()], shape=fp8) == 1            # fp8 needs scales
+    assert _call([_fake_layer(s_k=1 << 20, s_v=1 << 21, s_a=1 << 22, s_b=1 << 23, w_q=1 << 24)], shape=fp8) == 1
+    assert sr.LIB.sr_replay_state(None, 1, None, 0, 0, None, None, None, 0, None) == 1
+
+
+def test_replay_state_empty_batch_is_noop():
+    # zero segments and zero rows: valid, nothing to launch
+    assert _call([_fake_layer(anchors=None)], n_seg=0, t=0, cu=None, ws=None, ws_bytes=0) == 0
+
+
+def test_kernel_timing_read_without_launches():
+    sr.kernel_timing_enable(True)
+    out = sr.kernel_timing_read()
+    sr.kernel_timing_enable(False)
+    assert set(out) == set(sr.KERNEL_KINDS)
+    assert all(v == (0.0, 0) for v in out.values())
