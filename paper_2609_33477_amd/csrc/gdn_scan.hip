@@ -1,4 +1,5 @@
-// Chunked Gated DeltaNet state accumulation for suffix replay.
+// Chunked Gated DeltaNet state accumulation for suffix replay: the fp32
+// operand path (v_mfma_f32_32x32x2f32); bf16 operands use gdn_scan_bf16.hip.
 //
 // Evaluates, for each (layer, segment, value head), the final state of the
 // recurrence S_t = alpha_t S_{t-1}(I - beta_t k_t k_t^T) + beta_t v_t k_t^T
@@ -39,6 +40,7 @@ namespace {
 constexpr int kC = 64;       // chunk rows
 constexpr int kFP = 68;      // fp32 pitch of A and T
 constexpr int kSortMax = 256;
+constexpr float kLog2e = 1.4426950408889634f;
 
 template <typename OP, int D>
 struct ScanCfg {
@@ -130,6 +132,21 @@ __device__ __forceinline__ void store_op<bf16_t>(char* base, int idx, float v) {
 template <>
 __device__ __forceinline__ void store_op<float>(char* base, int idx, float v) {
   reinterpret_cast<float*>(base)[idx] = v;
+}
+
+// Four consecutive operand values (8- or 16-byte aligned destination).
+template <typename OP>
+__device__ __forceinline__ void store4_op(char* base, int idx, const float* v);
+template <>
+__device__ __forceinline__ void store4_op<bf16_t>(char* base, int idx, const float* v) {
+  uint2 u;
+  u.x = f32_to_bf16_bits(v[0]) | ((uint32_t)f32_to_bf16_bits(v[1]) << 16);
+  u.y = f32_to_bf16_bits(v[2]) | ((uint32_t)f32_to_bf16_bits(v[3]) << 16);
+  *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(base) + idx) = u;
+}
+template <>
+__device__ __forceinline__ void store4_op<float>(char* base, int idx, const float* v) {
+  *reinterpret_cast<float4*>(reinterpret_cast<float*>(base) + idx) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
 // Scatter a 16-byte piece (VPP elements of one row) into a transposed matrix.
@@ -278,10 +295,10 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
       store_transposed<OP>(Vt, CP, cc * CF::VPP, row, pv[i]);
     }
     if (tid < kC) {
-      gs[tid] = pg;
+      gs[tid] = pg * kLog2e;   // log2 alpha: every decay factor below is an exp2
       bs[tid] = pb;
     }
-    __syncthreads();
+    lds_barrier();
     if (c0 + kC < s1) prefetch(c0 + kC);
 
     // ---- 2. in-chunk prefix of log alpha (wave 0); Gram tiles K K^T
@@ -294,56 +311,59 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
       }
       const float gC = __shfl(x, 63);
       Gc[lane] = x;
-      eG[lane] = expf(x);
-      eD[lane] = expf(gC - x);
+      eG[lane] = exp2f(x);
+      eD[lane] = exp2f(gC - x);
     }
-    // lower tiles (0,0), (1,0), (1,1); tile q handled by wave q % NW
-    f32x16 gam[3];
+    // lower 32x32 tiles q = 0, 1, 2 -> (0,0), (1,0), (1,1); wave w owns q = w + n NW
+    constexpr int GT = (3 + NW - 1) / NW;
+    f32x16 gam[GT];
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      gam[q] = zero16();
-      if (q % NW != wid) continue;
+    for (int n = 0; n < GT; ++n) {
+      gam[n] = zero16();
+      const int q = wid + n * NW;
+      if (q >= 3) continue;
       const int ti = (q + 1) >> 1, tj = q >> 1;
 #pragma unroll
       for (int s = 0; s < D / MF::K; ++s) {
         const auto fa = frag_std<OP>(R1, KP, 32 * ti + fr, s * MF::K + fk);
         const auto fb = frag_std<OP>(R1, KP, 32 * tj + fr, s * MF::K + fk);
-        MF::mma(gam[q], fa, fb);
+        MF::mma(gam[n], fa, fb);
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- 3. A_ij = beta_i e^{G_i - G_j} Gamma_ij for i > j (fp32, into R1)
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      if (q % NW != wid) continue;
+    for (int n = 0; n < GT; ++n) {
+      const int q = wid + n * NW;
+      if (q >= 3) continue;
       const int ti = (q + 1) >> 1, tj = q >> 1;
       const int j = 32 * tj + fr;
       const float gj = Gc[j];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int i = 32 * ti + acc_row(r, lane);
-        Am[i * kFP + j] = (i > j) ? bs[i] * expf(Gc[i] - gj) * gam[q][r] : 0.f;
+        Am[i * kFP + j] = (i > j) ? bs[i] * exp2f(fminf(Gc[i] - gj, 0.f)) * gam[n][r] : 0.f;
       }
     }
-    __syncthreads();
+    lds_barrier();
 
-    // ---- 4. diagonal 16x16 blocks of T = (I + A)^{-1}: lane = (block, column)
+    // ---- 4. diagonal 16x16 blocks of T = (I + A)^{-1}: lane = (block, column),
+    //         column-sweep forward substitution (16-step dependency chain)
     if (wid == 0) {
       const int bb = lane >> 4, c = lane & 15;
       const float* Ab = Am + (16 * bb) * kFP + 16 * bb;
       float x[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float sacc = (i == c) ? 1.f : 0.f;
+      for (int i = 0; i < 16; ++i) x[i] = (i == c) ? 1.f : 0.f;
 #pragma unroll
-        for (int m = 0; m < i; ++m) sacc = fmaf(-Ab[i * kFP + m], x[m], sacc);
-        x[i] = sacc;
-      }
+      for (int m = 0; m < 15; ++m)
+#pragma unroll
+        for (int i = m + 1; i < 16; ++i) x[i] = fmaf(-Ab[i * kFP + m], x[m], x[i]);
 #pragma unroll
       for (int i = 0; i < 16; ++i) Tm[(16 * bb + i) * kFP + 16 * bb + c] = x[i];
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- 5. block rows 1..3: T_bc = -T_bb sum_{m=c}^{b-1} A_bm T_mc (fp32 MFMA)
     {
@@ -369,18 +389,22 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) Tm[(16 * lv + 4 * k4 + r) * kFP + 16 * c + i16] = -Z[r];
         }
-        __syncthreads();
+        lds_barrier();
       }
     }
 
     // ---- 6. Tu = T diag(beta), Tw = T diag(beta e^G), rounded once (into R1)
-    for (int e = tid; e < kC * kC; e += CF::THREADS) {
+    for (int e = 4 * tid; e < kC * kC; e += 4 * CF::THREADS) {
       const int i = e >> 6, j = e & 63;
-      const float t = Tm[i * kFP + j] * bs[j];
-      store_op<OP>(Tu, i * CP + j, t);
-      store_op<OP>(Tw, i * CP + j, t * eG[j]);
+      const float4 t = *reinterpret_cast<const float4*>(Tm + i * kFP + j);
+      const float4 b4 = *reinterpret_cast<const float4*>(bs + j);
+      const float4 g4 = *reinterpret_cast<const float4*>(eG + j);
+      const float u[4] = {t.x * b4.x, t.y * b4.y, t.z * b4.z, t.w * b4.w};
+      const float v[4] = {u[0] * g4.x, u[1] * g4.y, u[2] * g4.z, u[3] * g4.w};
+      store4_op<OP>(Tu, i * CP + j, u);
+      store4_op<OP>(Tw, i * CP + j, v);
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- 7. U = Tu V (this wave's columns), W = Tw K (tiles q = wid mod NW)
     f32x16 Uacc[2], Wacc[2];
@@ -406,7 +430,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
         MF::mma(Wacc[n], fa, fb);
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- 8. W to R1, row-major, rounded once
 #pragma unroll
@@ -416,7 +440,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) store_op<OP>(Wr, (32 * ti + acc_row(r, lane)) * KP + 32 * td + fr, Wacc[n][r]);
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- 9. Delta = U - W M0 (state from registers), Delta' = e^{G_C - G} Delta
     typename MF::frag dfrag[2][32 / MF::K];
@@ -452,7 +476,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
           MF::mma(M[td], fa, dfrag[ti][s]);
         }
     }
-    __syncthreads();
+    lds_barrier();
   }
 
   float* out = st_out + state_base;
@@ -473,13 +497,8 @@ hipError_t run_scan(const ScanArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_scan(int op_dtype, int d_head, const ScanArgs& a, hipStream_t s) {
-  if (op_dtype == SR_BF16) {
-    switch (d_head) {
-      case 32: return run_scan<bf16_t, 32>(a, s);
-      case 64: return run_scan<bf16_t, 64>(a, s);
-      case 128: return run_scan<bf16_t, 128>(a, s);
-    }
-  } else if (op_dtype == SR_F32) {
+  if (op_dtype == SR_BF16) return launch_scan_bf16(d_head, a, s);
+  if (op_dtype == SR_F32) {
     switch (d_head) {
       case 32: return run_scan<float, 32>(a, s);
       case 64: return run_scan<float, 64>(a, s);

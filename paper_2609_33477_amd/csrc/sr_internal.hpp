@@ -94,5 +94,6 @@ struct ScanArgs {
 };
 
 hipError_t launch_scan(int op_dtype, int d_head, const ScanArgs& a, hipStream_t s);
+hipError_t launch_scan_bf16(int d_head, const ScanArgs& a, hipStream_t s);
 
 }  // namespace sr
