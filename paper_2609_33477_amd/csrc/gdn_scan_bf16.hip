@@ -1,26 +1,31 @@
 // Chunked Gated DeltaNet state accumulation, bf16 operands (gfx950).
 //
-// Same chunked form as the fp32 kernel (gdn_scan.hip), for C = 64 rows that
-// start from state M0, G = in-chunk prefix of log alpha:
-//   A_ij  = beta_i e^{G_i - G_j} k_i.k_j  (i > j)        T = (I + A)^{-1}
-//   U     = T diag(beta) V                              W = T diag(beta e^G) K
+// Same recurrence as the fp32 kernel (gdn_scan.hip).  Rows are staged 64 at a
+// time and processed as four 16-row sub-chunks b; within a sub-chunk that
+// starts from state M0 (= S^T), with G the sub-chunk prefix of log alpha:
+//   A_ij  = beta_i e^{G_i - G_j} k_i.k_j  (i > j)        T = (I + A)^{-1}  (16x16)
+//   U     = T diag(beta) V,    W = T diag(beta e^G) K
 //   Delta = U - W M0
-//   M_C   = e^{G_C} M0 + K^T diag(e^{G_C - G}) Delta
+//   M_16  = e^{G_15} M0 + K^T diag(e^{G_15 - G}) Delta
+// Everything except the last two lines is independent of the state, so for
+// all four sub-chunks it runs in parallel across the workgroup; the four
+// state steps then run back to back in registers with no barrier.  16-row
+// sub-chunks need only the 16x16 triangular inverses (no block merges) and
+// cut the state-independent work per row by 4x against 64-row chunks.
 //
 // Layout for MI355X: d/16 waves per unit; wave w owns state columns
-// [16w, 16w+16) as d/16 16x16 fp32 accumulator tiles (32 registers at d=128),
-// all products are v_mfma_f32_16x16x32_bf16.  K and V stay row-major in LDS
-// (plain 16-byte staging stores); every operand whose reduction index runs
-// down the rows of a row-major LDS matrix (V and K for U and W, K^T for the
-// state update, W for W M0) is read with ds_read_b64_tr_b16, which hands lane
-// i of each 16-lane group the 4 consecutive rows kbase..kbase+3 of column
-// n0 + i when lane j of the group addresses row kbase + j/4, columns
-// n0 + 4 (j%4) .. +3.  The two state products take the state / Delta operand
+// [16w, 16w+16) as d/16 16x16 fp32 accumulator tiles (32 registers at d=128).
+// Products use v_mfma_f32_16x16x32_bf16 (reduction over d) and
+// v_mfma_f32_16x16x16_bf16 (reduction over a sub-chunk's 16 rows).  K and V
+// stay row-major in LDS; operands whose reduction index runs down the rows of
+// an LDS matrix are read with ds_read_b64_tr_b16, which hands lane i of each
+// 16-lane group rows kbase..kbase+3 of column n0 + i when lane j of the group
+// addresses row kbase + j/4, columns n0 + 4 (j%4) .. +3.  W M0 takes the state
 // straight from accumulator registers, with the MFMA k slots permuted to the
-// accumulator row order and the other operand read in the same order.
+// accumulator row order and W read in the same order.
 //
-// LDS (d = 128): K, V, A (fp32), T (fp32), Tu | Tw, W^T, each ~18 KB, plus
-// four 64-float vectors: 108 KB; one unit (8 waves) per CU.
+// LDS (d = 128): K, V, W^T (~18 KB each), A (fp32) 5 KB, Tu | Tw 5 KB,
+// vectors 1 KB: 66 KB.
 #include "sr_device.hpp"
 
 #include <cstddef>
@@ -28,20 +33,19 @@
 namespace sr {
 namespace {
 
-constexpr int kC = 64;       // chunk rows
-constexpr int kFP = 68;      // fp32 pitch of A
-constexpr int kTP = 72;      // fp32 pitch of T
+constexpr int kC = 64;       // rows staged per step
+constexpr int kS = 16;       // sub-chunk rows
+constexpr int kAP = 20;      // fp32 pitch of the 16x16 A blocks
+constexpr int kTP = 20;      // bf16 pitch of the 16x16 Tu / Tw blocks
 constexpr int kSortMax = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 // LDS is addressed through address-space-3 pointers with 32-bit offsets so
-// that the per-read constants fold into the instructions' offset field
-// instead of occupying one address register per read.
+// that per-read constants fold into the instructions' offset field.
 #define SR_LDS __attribute__((address_space(3)))
 typedef SR_LDS char lchar;
-
 typedef unsigned int nu32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int nu32x2 __attribute__((ext_vector_type(2)));
 typedef float nf32x4 __attribute__((ext_vector_type(4)));
@@ -49,12 +53,12 @@ typedef float nf32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 lds_ld16(const lchar* p) {
   return __builtin_bit_cast(uint4, *reinterpret_cast<const SR_LDS nu32x4*>(p));
 }
+__device__ __forceinline__ uint2 lds_ld8(const lchar* p) {
+  return __builtin_bit_cast(uint2, *reinterpret_cast<const SR_LDS nu32x2*>(p));
+}
 __device__ __forceinline__ float4 lds_ldf4(const lchar* p) {
   const nf32x4 v = *reinterpret_cast<const SR_LDS nf32x4*>(p);
   return make_float4(v[0], v[1], v[2], v[3]);
-}
-__device__ __forceinline__ uint2 lds_ld8(const lchar* p) {
-  return __builtin_bit_cast(uint2, *reinterpret_cast<const SR_LDS nu32x2*>(p));
 }
 __device__ __forceinline__ void lds_st16(lchar* p, const uint4& v) {
   *reinterpret_cast<SR_LDS nu32x4*>(p) = __builtin_bit_cast(nu32x4, v);
@@ -63,40 +67,8 @@ __device__ __forceinline__ void lds_st8(lchar* p, const uint2& v) {
   *reinterpret_cast<SR_LDS nu32x2*>(p) = __builtin_bit_cast(nu32x2, v);
 }
 
-template <int D>
-struct Cfg {
-  static constexpr int NW = D / 16;
-  static constexpr int THREADS = 64 * NW;
-  static constexpr int NT = D / 16;               // 16-row tiles along d
-  static constexpr int KP = D + 16;               // K / V row pitch (bf16): 4 rows hit 32 distinct banks
-  static constexpr int WP = kC + 8;               // W^T, Tu, Tw row pitch (bf16)
-  static constexpr int SZ_KV = kC * KP * 2;
-  static constexpr int SZ_A = kC * kFP * 4;           // A, fp32
-  static constexpr int SZ_T = kC * kTP * 4;           // T, fp32
-  static constexpr int SZ_TUW = 2 * kC * WP * 2;      // Tu | Tw, bf16
-  static constexpr int SZ_W = D * WP * 2;             // W^T, bf16
-  static constexpr int OFF_K = 0, OFF_V = SZ_KV, OFF_A = 2 * SZ_KV, OFF_T = OFF_A + SZ_A;
-  static constexpr int OFF_TUW = OFF_T + SZ_T, OFF_W = OFF_TUW + SZ_TUW;
-  static constexpr int OFF_VEC = OFF_W + SZ_W;
-  static constexpr int LDS = OFF_VEC + 4 * kC * 4;
-  static constexpr int PPR = D / 8;                   // 16-byte pieces per row
-  static constexpr int PER_T = kC * PPR / THREADS;    // pieces per thread (= 2)
-  static constexpr int EPT = kC * kC / (4 * THREADS); // float4 of T per thread
-  static_assert(kC * PPR % THREADS == 0, "staging split");
-};
-
-__device__ __forceinline__ f32x4 mma16(const f32x4& c, const bf16x8& a, const bf16x8& b) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
-
-__device__ __forceinline__ bf16x8 ld16(const lchar* p) { return as_bf16x8(lds_ld16(p)); }
-
-// Transposed read: with lane j of each 16-lane group pointing at row
-// kbase + j/4, columns n0 + 4 (j%4) .. +3 of a row-major bf16 matrix, lane i
-// receives rows kbase..kbase+3 of column n0 + i.  `p` already includes the
-// lane part ((j/4) * pitch + 4 (j%4)) * 2.
+// Transposed read (see the file comment); `p` includes the lane part of the
+// address.
 __device__ __forceinline__ uint2 tr4(const lchar* p) {
   const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SR_LDS v4i16*)p);
   return __builtin_bit_cast(uint2, v);
@@ -108,12 +80,40 @@ __device__ __forceinline__ bf16x8 join(uint2 lo, uint2 hi, bool negate) {
   return as_bf16x8(u);
 }
 
-__device__ __forceinline__ uint32_t pack2(float a, float b) { return pack_bf16x2(a, b); }
+__device__ __forceinline__ v4i16 as_v4(uint2 u) { return __builtin_bit_cast(v4i16, u); }
 
 // Two 16x16 accumulator tiles (rows 4g..4g+3 of each) as one 16x16x32 operand.
 __device__ __forceinline__ bf16x8 acc_pair(const f32x4& x, const f32x4& y) {
-  return as_bf16x8(make_uint4(pack2(x[0], x[1]), pack2(x[2], x[3]), pack2(y[0], y[1]), pack2(y[2], y[3])));
+  return as_bf16x8(make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(y[0], y[1]),
+                              pack_bf16x2(y[2], y[3])));
 }
+
+__device__ __forceinline__ f32x4 mma_k32(const f32x4& c, const bf16x8& a, const bf16x8& b) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma_k16(const f32x4& c, const v4i16& a, const v4i16& b) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+template <int D>
+struct Cfg {
+  static constexpr int NW = D / 16;                   // waves; wave w owns state columns [16w, 16w+16)
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int NT = D / 16;                   // 16-row tiles along d
+  static constexpr int KP = D + 16;                   // K / V row pitch (bf16)
+  static constexpr int WP = kC + 8;                   // W^T row pitch (bf16)
+  static constexpr int SZ_KV = kC * KP * 2;
+  static constexpr int SZ_W = D * WP * 2;
+  static constexpr int SZ_A = kC * kAP * 4;           // four 16x16 fp32 blocks
+  static constexpr int SZ_T = 2 * kC * kTP * 2;       // Tu | Tw, four 16x16 bf16 blocks each
+  static constexpr int OFF_K = 0, OFF_V = SZ_KV, OFF_W = 2 * SZ_KV, OFF_A = OFF_W + SZ_W;
+  static constexpr int OFF_T = OFF_A + SZ_A, OFF_VEC = OFF_T + SZ_T;
+  static constexpr int LDS = OFF_VEC + 4 * kC * 4;
+  static constexpr int PPR = D / 8;                   // 16-byte pieces per row
+  static constexpr int PER_T = kC * PPR / THREADS;    // pieces per thread
+  static_assert(kC * PPR % THREADS == 0, "staging split");
+};
 
 __device__ int rank_to_segment(const ScanArgs& a, int rank, int* shared_sel) {
   if (a.n_seg > kSortMax) return rank;
@@ -142,26 +142,24 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
   __shared__ int sel;
 
   lchar* L = (lchar*)smem;
-  lchar* Kr = L + CF::OFF_K;                               // [64][KP] bf16
-  lchar* Vr = L + CF::OFF_V;                               // [64][KP] bf16
-  SR_LDS float* Am = (SR_LDS float*)(L + CF::OFF_A);       // [64][kFP] fp32
-  lchar* Wt = L + CF::OFF_W;                               // [D][WP] bf16
-  SR_LDS float* Tm = (SR_LDS float*)(L + CF::OFF_T);       // [64][kTP] fp32
-  lchar* Tu = L + CF::OFF_TUW;                             // [64][WP] bf16
-  lchar* Tw = Tu + kC * WP * 2;
-  SR_LDS float* gs = (SR_LDS float*)(L + CF::OFF_VEC);     // log2 alpha
-  SR_LDS float* bs = gs + kC;                              // beta
-  SR_LDS float* eG = bs + kC;                              // 2^{G_i}
-  SR_LDS float* eD = eG + kC;                              // 2^{G_C - G_i}
+  lchar* Kr = L + CF::OFF_K;                              // [64][KP] bf16
+  lchar* Vr = L + CF::OFF_V;                              // [64][KP] bf16
+  lchar* Wt = L + CF::OFF_W;                              // [D][WP] bf16, W^T of the four sub-chunks
+  SR_LDS float* Am = (SR_LDS float*)(L + CF::OFF_A);      // [64][kAP] fp32: block b = rows 16b..16b+15
+  lchar* Tu = L + CF::OFF_T;                              // [64][kTP] bf16
+  lchar* Tw = Tu + kC * kTP * 2;
+  SR_LDS float* gs = (SR_LDS float*)(L + CF::OFF_VEC);    // log2 alpha
+  SR_LDS float* bs = gs + kC;                             // beta
+  SR_LDS float* eG = bs + kC;                             // 2^{G_i}      (G: sub-chunk prefix, log2)
+  SR_LDS float* eD = eG + kC;                             // 2^{G_15 - G_i}
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int g = lane >> 4, li = lane & 15;
   // per-lane byte offsets; everything else is a compile-time immediate
-  const int kv_row = (li * KP + 8 * g) * 2;                          // 16-byte row reads of K
-  const int t_row4 = (li * WP + 4 * g) * 2;                          // 8-byte row reads of Tu / Tw
-  const int tr_kv = ((li >> 2) * KP + 4 * (li & 3)) * 2;             // transposed reads of K / V
-  const int tr_kv4 = tr_kv + 4 * g * KP * 2;                         //   rows 4g + ...
-  const int tr_w4 = ((li >> 2) * WP + 4 * (li & 3) + 4 * g * WP) * 2; // transposed reads of W^T, rows 4g + ...
+  const int kv_row = (li * KP + 8 * g) * 2;                           // 16-byte row reads of K
+  const int t_row = (li * kTP + 4 * g) * 2;                           // 8-byte row reads of Tu / Tw
+  const int tr_kv = ((li >> 2) * KP + 4 * (li & 3) + 4 * g * KP) * 2; // transposed reads of K / V, rows 4g + ..
+  const int tr_w = ((li >> 2) * WP + 4 * (li & 3) + 4 * g * WP) * 2;  // transposed reads of W^T, rows 4g + ..
 
   const int u = blockIdx.x;
   const int head = u % a.H_v;
@@ -195,9 +193,6 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
     }
   }
 
-  // T's strictly upper 16x16 blocks stay zero for the whole segment.
-  for (int i = tid; i < kC * kTP; i += CF::THREADS) Tm[i] = 0.f;
-
   uint4 pk[CF::PER_T], pv[CF::PER_T];
   float pg = 0.f, pb = 0.f;
   auto prefetch = [&](int64_t c0) {
@@ -223,7 +218,8 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
   if (s0 < s1) prefetch(s0);
 
   for (int64_t c0 = s0; c0 < s1; c0 += kC) {
-    // ---- 1. stage the chunk (row-major K, V; padding rows are zero)
+    // ---- 1. stage 64 rows (row-major K, V; padding rows are zero with
+    //         log alpha = 0 and beta = 0, which makes them inert)
 #pragma unroll
     for (int i = 0; i < CF::PER_T; ++i) {
       const int p = tid + i * CF::THREADS;
@@ -238,183 +234,105 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
     lds_barrier();
     if (c0 + kC < s1) prefetch(c0 + kC);
 
-    // ---- 2. in-chunk prefix G of log2 alpha (every wave, in registers);
-    //         lower 16x16 tiles of K K^T;  A_ij = beta_i 2^{G_i - G_j} Gamma_ij
+    // ---- 2. sub-chunk prefix G (registers: lane = row, scan within 16 lanes);
+    //         Gram blocks K_b K_b^T -> A_b = beta_i 2^{G_i - G_j} Gamma (i > j)
     float Gx = gs[lane];
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const float y = __shfl_up(Gx, off);
-      if (lane >= off) Gx += y;
+    for (int off = 1; off < kS; off <<= 1) {
+      const float y = __shfl_up(Gx, off, kS);
+      if (li >= off) Gx += y;
     }
     if (wid == 0) {
       eG[lane] = exp2f(Gx);
-      eD[lane] = exp2f(__shfl(Gx, 63) - Gx);
+      eD[lane] = exp2f(__shfl(Gx, 16 * g + 15) - Gx);
     }
-    constexpr int GT = (10 + NW - 1) / NW;
 #pragma unroll
-    for (int n = 0; n < GT; ++n) {
-      const int q = wid + n * NW;
-      if (q >= 10) continue;
-      const int ti = q < 1 ? 0 : q < 3 ? 1 : q < 6 ? 2 : 3;
-      const int tj = q - ti * (ti + 1) / 2;
+    for (int n = 0; n < (4 + NW - 1) / NW; ++n) {
+      const int sb = wid + n * NW;   // sub-chunk
+      if (sb >= 4) continue;
       f32x4 gam = zero4();
 #pragma unroll
-      for (int s = 0; s < D / 32; ++s) {
-        const bf16x8 fa = ld16(Kr + kv_row + (16 * ti * KP + 32 * s) * 2);
-        const bf16x8 fb = ld16(Kr + kv_row + (16 * tj * KP + 32 * s) * 2);
-        gam = mma16(gam, fa, fb);
-      }
-      const int j = 16 * tj + li;
-      const float gj = __shfl(Gx, j);
+      for (int s = 0; s < D / 32; ++s)
+        gam = mma_k32(gam, as_bf16x8(lds_ld16(Kr + kv_row + (16 * sb * KP + 32 * s) * 2)),
+                      as_bf16x8(lds_ld16(Kr + kv_row + (16 * sb * KP + 32 * s) * 2)));
+      const float gj = __shfl(Gx, 16 * sb + li);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int i = 16 * ti + 4 * g + r;
-        const float gi = __shfl(Gx, i);
-        Am[i * kFP + j] = (i > j) ? bs[i] * exp2f(fminf(gi - gj, 0.f)) * gam[r] : 0.f;
+        const int i = 4 * g + r;
+        const float gi = __shfl(Gx, 16 * sb + i);
+        Am[(16 * sb + i) * kAP + li] = (i > li) ? bs[16 * sb + i] * exp2f(fminf(gi - gj, 0.f)) * gam[r] : 0.f;
       }
     }
     lds_barrier();
 
-    // ---- 4. diagonal 16x16 blocks of T (wave 0, column-sweep substitution);
-    //         the other waves clear T's strictly upper blocks
+    // ---- 3. T_b = (I + A_b)^{-1} by column-sweep substitution (wave 0, lane =
+    //         (sub-chunk, column)); Tu = T diag(beta), Tw = T diag(beta 2^G),
+    //         rounded once, written straight from the solved columns
     if (wid == 0) {
-      const int bb = lane >> 4, c = lane & 15;
-      const SR_LDS float* Ab = Am + (16 * bb) * kFP + 16 * bb;
+      const int sb = g, c = li;
+      const SR_LDS float* Ab = Am + 16 * sb * kAP;
+      float arow[16][16];
+#pragma unroll
+      for (int i = 1; i < 16; ++i)
+#pragma unroll
+        for (int q = 0; q < (i + 3) / 4; ++q) {
+          const float4 v = lds_ldf4((const lchar*)(Ab + i * kAP + 4 * q));
+          arow[i][4 * q + 0] = v.x; arow[i][4 * q + 1] = v.y; arow[i][4 * q + 2] = v.z; arow[i][4 * q + 3] = v.w;
+        }
       float x[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i) x[i] = (i == c) ? 1.f : 0.f;
-      // four columns per group; the scheduling fences keep the compiler from
-      // hoisting all 120 A loads at once (register pressure)
 #pragma unroll
-      for (int m0 = 0; m0 < 16; m0 += 4) {
-        __builtin_amdgcn_sched_barrier(0);
+      for (int m = 0; m < 15; ++m)
 #pragma unroll
-        for (int m = m0; m < m0 + 4 && m < 15; ++m)
+        for (int i = m + 1; i < 16; ++i) x[i] = fmaf(-arow[i][m], x[m], x[i]);
+      const float bc = bs[16 * sb + c];
+      const float wc = bc * eG[16 * sb + c];
 #pragma unroll
-          for (int i = m + 1; i < 16; ++i) x[i] = fmaf(-Ab[i * kFP + m], x[m], x[i]);
+      for (int i = 0; i < 16; ++i) {
+        *reinterpret_cast<SR_LDS uint16_t*>(Tu + ((16 * sb + i) * kTP + c) * 2) = f32_to_bf16_bits(x[i] * bc);
+        *reinterpret_cast<SR_LDS uint16_t*>(Tw + ((16 * sb + i) * kTP + c) * 2) = f32_to_bf16_bits(x[i] * wc);
       }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) Tm[(16 * bb + i) * kTP + 16 * bb + c] = x[i];
     }
     lds_barrier();
 
-    // ---- 5. block rows 1..3: T_bc = -T_bb sum_{m=c}^{b-1} A_bm T_mc (fp32 MFMA)
-    {
-      const int k4 = lane >> 4;
-#pragma unroll
-      for (int lv = 1; lv < 4; ++lv) {
-        for (int c = wid; c < lv; c += NW) {
-          f32x4 Y = zero4();
-          for (int m = c; m < lv; ++m) {
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-              const float fa = Am[(16 * lv + li) * kFP + 16 * m + 4 * ks + k4];
-              const float fb = Tm[(16 * m + 4 * ks + k4) * kTP + 16 * c + li];
-              Y = __builtin_amdgcn_mfma_f32_16x16x4f32(fa, fb, Y, 0, 0, 0);
-            }
-          }
-          f32x4 Z = zero4();
-#pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            const float fa = Tm[(16 * lv + li) * kTP + 16 * lv + 4 * k4 + s];
-            Z = __builtin_amdgcn_mfma_f32_16x16x4f32(fa, Y[s], Z, 0, 0, 0);
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) Tm[(16 * lv + 4 * k4 + r) * kTP + 16 * c + li] = -Z[r];
-        }
-        lds_barrier();
-      }
-    }
-
-    // ---- 6. Tu = T diag(beta), Tw = T diag(beta 2^G), rounded once
-    {
-      float4 tv[CF::EPT];
-#pragma unroll
-      for (int k = 0; k < CF::EPT; ++k) {
-        const int e = 4 * (tid + k * CF::THREADS);
-        tv[k] = lds_ldf4((const lchar*)(Tm + (e >> 6) * kTP + (e & 63)));
-      }
-#pragma unroll
-      for (int k = 0; k < CF::EPT; ++k) {
-        const int e = 4 * (tid + k * CF::THREADS);
-        const int i = e >> 6, j = e & 63;
-        const float4 b4 = lds_ldf4((const lchar*)(bs + j));
-        const float4 g4 = lds_ldf4((const lchar*)(eG + j));
-        const float u0 = tv[k].x * b4.x, u1 = tv[k].y * b4.y, u2 = tv[k].z * b4.z, u3 = tv[k].w * b4.w;
-        lds_st8(Tu + (i * WP + j) * 2, make_uint2(pack2(u0, u1), pack2(u2, u3)));
-        lds_st8(Tw + (i * WP + j) * 2, make_uint2(pack2(u0 * g4.x, u1 * g4.y), pack2(u2 * g4.z, u3 * g4.w)));
-      }
-      lds_barrier();
-    }
-
-    // ---- 7. U (this wave's 16 columns) and 4 tiles of W = Tw K, stored as W^T
+    // ---- 4. U_b = Tu_b V_b (this wave's columns, kept in registers) and
+    //         W_b = Tw_b K_b (4 tiles per wave, stored as W^T)
     f32x4 U[4];
 #pragma unroll
-    for (int ti = 0; ti < 4; ++ti) {
-      U[ti] = zero4();
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        // k slots of group g: rows 32s + 4g + 0..3 and 32s + 16 + 4g + 0..3
-        const bf16x8 fa = join(lds_ld8(Tu + t_row4 + (16 * ti * WP + 32 * s) * 2),
-                               lds_ld8(Tu + t_row4 + (16 * ti * WP + 32 * s + 16) * 2), false);
-        const bf16x8 fb = join(tr4(Vr + tr_kv4 + ((32 * s) * KP + 16 * wid) * 2),
-                               tr4(Vr + tr_kv4 + ((32 * s + 16) * KP + 16 * wid) * 2), false);
-        U[ti] = mma16(U[ti], fa, fb);
-      }
-    }
-    f32x4 Wacc[4];
+    for (int sb = 0; sb < 4; ++sb)
+      U[sb] = mma_k16(zero4(), as_v4(lds_ld8(Tu + t_row + 16 * sb * kTP * 2)),
+                      as_v4(tr4(Vr + tr_kv + (16 * sb * KP + 16 * wid) * 2)));
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       const int q = wid + n * NW;   // 4 NT tiles, exactly 4 per wave
-      const int ti = q / NT, td = q % NT;
-      Wacc[n] = zero4();
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const bf16x8 fa = join(lds_ld8(Tw + t_row4 + (16 * ti * WP + 32 * s) * 2),
-                               lds_ld8(Tw + t_row4 + (16 * ti * WP + 32 * s + 16) * 2), false);
-        const bf16x8 fb = join(tr4(Kr + tr_kv4 + ((32 * s) * KP + 16 * td) * 2),
-                               tr4(Kr + tr_kv4 + ((32 * s + 16) * KP + 16 * td) * 2), false);
-        Wacc[n] = mma16(Wacc[n], fa, fb);
-      }
-      // W^T tile, rounded once (the previous chunk's readers are past the
-      // end-of-chunk barrier)
-      lds_st8(Wt + ((16 * td + li) * WP + 16 * ti + 4 * g) * 2,
-              make_uint2(pack2(Wacc[n][0], Wacc[n][1]), pack2(Wacc[n][2], Wacc[n][3])));
+      const int sb = q / NT, td = q % NT;
+      const f32x4 w = mma_k16(zero4(), as_v4(lds_ld8(Tw + t_row + 16 * sb * kTP * 2)),
+                              as_v4(tr4(Kr + tr_kv + (16 * sb * KP + 16 * td) * 2)));
+      lds_st8(Wt + ((16 * td + li) * WP + 16 * sb + 4 * g) * 2,
+              make_uint2(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3])));
     }
     lds_barrier();
 
-    // ---- 9. Delta = U - W M0 (state from registers), Delta' = 2^{G_C - G} Delta
-    bf16x8 mfrag[NT / 2];   // the state as a bf16 operand, packed once per chunk
+    // ---- 5. four state steps, in registers
 #pragma unroll
-    for (int p = 0; p < NT / 2; ++p) mfrag[p] = acc_pair(M[2 * p], M[2 * p + 1]);
-    f32x4 dl[4];
+    for (int sb = 0; sb < 4; ++sb) {
+      f32x4 dl = U[sb];
 #pragma unroll
-    for (int ti = 0; ti < 4; ++ti) {
-      f32x4 acc = U[ti];
+      for (int p = 0; p < NT / 2; ++p)   // Delta = U - W M0, W rows read in the state's k order
+        dl = mma_k32(dl,
+                     join(tr4(Wt + tr_w + ((32 * p) * WP + 16 * sb) * 2),
+                          tr4(Wt + tr_w + ((32 * p + 16) * WP + 16 * sb) * 2), true),
+                     acc_pair(M[2 * p], M[2 * p + 1]));
+      const float4 ed = lds_ldf4((const lchar*)(eD + 16 * sb + 4 * g));
+      const v4i16 dfr = as_v4(make_uint2(pack_bf16x2(dl[0] * ed.x, dl[1] * ed.y), pack_bf16x2(dl[2] * ed.z, dl[3] * ed.w)));
+      const float decay = eG[16 * sb + 15];
 #pragma unroll
-      for (int p = 0; p < NT / 2; ++p) {
-        const bf16x8 fa = join(tr4(Wt + tr_w4 + ((32 * p) * WP + 16 * ti) * 2),
-                               tr4(Wt + tr_w4 + ((32 * p + 16) * WP + 16 * ti) * 2), true);
-        acc = mma16(acc, fa, mfrag[p]);
+      for (int td = 0; td < NT; ++td) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) M[td][r] *= decay;
+        M[td] = mma_k16(M[td], as_v4(tr4(Kr + tr_kv + (16 * sb * KP + 16 * td) * 2)), dfr);
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] *= eD[16 * ti + 4 * g + r];
-      dl[ti] = acc;
-    }
-    const bf16x8 d01 = acc_pair(dl[0], dl[1]);
-    const bf16x8 d23 = acc_pair(dl[2], dl[3]);
-
-    // ---- 10. M = 2^{G_C} M0 + K^T Delta'
-    const float eGC = eG[kC - 1];
-#pragma unroll
-    for (int td = 0; td < NT; ++td) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) M[td][r] *= eGC;
-      const bf16x8 f0 = join(tr4(Kr + tr_kv4 + (16 * td) * 2), tr4(Kr + tr_kv4 + (16 * KP + 16 * td) * 2), false);
-      M[td] = mma16(M[td], f0, d01);
-      const bf16x8 f1 = join(tr4(Kr + tr_kv4 + (32 * KP + 16 * td) * 2), tr4(Kr + tr_kv4 + (48 * KP + 16 * td) * 2), false);
-      M[td] = mma16(M[td], f1, d23);
     }
     lds_barrier();
   }
