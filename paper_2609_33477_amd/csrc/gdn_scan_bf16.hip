@@ -38,7 +38,6 @@ constexpr int kS = 16;       // sub-chunk rows
 constexpr int kAP = 20;      // fp32 pitch of the 16x16 A blocks
 constexpr int kTP = 20;      // bf16 pitch of the 16x16 Tu / Tw blocks
 constexpr int kSortMax = 256;
-constexpr float kLog2e = 1.4426950408889634f;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
@@ -148,7 +147,7 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
   SR_LDS float* Am = (SR_LDS float*)(L + CF::OFF_A);      // [64][kAP] fp32: block b = rows 16b..16b+15
   lchar* Tu = L + CF::OFF_T;                              // [64][kTP] bf16
   lchar* Tw = Tu + kC * kTP * 2;
-  SR_LDS float* gs = (SR_LDS float*)(L + CF::OFF_VEC);    // log2 alpha
+  SR_LDS float* gs = (SR_LDS float*)(L + CF::OFF_VEC);    // G: log2 alpha summed within the sub-chunk
   SR_LDS float* bs = gs + kC;                             // beta
   SR_LDS float* eG = bs + kC;                             // 2^{G_i}      (G: sub-chunk prefix, log2)
   SR_LDS float* eD = eG + kC;                             // 2^{G_15 - G_i}
@@ -194,7 +193,7 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
   }
 
   uint4 pk[CF::PER_T], pv[CF::PER_T];
-  float pg = 0.f, pb = 0.f;
+  float pg = 0.f, pg15 = 0.f, pb = 0.f;
   auto prefetch = [&](int64_t c0) {
 #pragma unroll
     for (int i = 0; i < CF::PER_T; ++i) {
@@ -210,9 +209,13 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
       }
     }
     if (tid < kC) {
-      const int64_t t = c0 + tid;
-      pg = (t < s1) ? Gp[t] : 0.f;
-      pb = (t < s1) ? Bp[t] : 0.f;
+      // G of this row and of its sub-chunk's last row; rows past the segment
+      // end carry log alpha = 0, so they repeat the last real row's G
+      const int64_t sub0 = c0 + (tid & ~15);
+      const int64_t t = min(c0 + tid, s1 - 1), t15 = min(sub0 + 15, s1 - 1);
+      pg = (t >= sub0) ? Gp[t] : 0.f;
+      pg15 = (t15 >= sub0) ? Gp[t15] : 0.f;
+      pb = (c0 + tid < s1) ? Bp[c0 + tid] : 0.f;
     }
   };
   if (s0 < s1) prefetch(s0);
@@ -228,24 +231,15 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
       lds_st16(Vr + (row * KP + cc * 8) * 2, pv[i]);
     }
     if (tid < kC) {
-      gs[tid] = pg * kLog2e;
+      gs[tid] = pg;
       bs[tid] = pb;
+      eG[tid] = exp2f(pg);
+      eD[tid] = exp2f(pg15 - pg);
     }
     lds_barrier();
     if (c0 + kC < s1) prefetch(c0 + kC);
 
-    // ---- 2. sub-chunk prefix G (registers: lane = row, scan within 16 lanes);
-    //         Gram blocks K_b K_b^T -> A_b = beta_i 2^{G_i - G_j} Gamma (i > j)
-    float Gx = gs[lane];
-#pragma unroll
-    for (int off = 1; off < kS; off <<= 1) {
-      const float y = __shfl_up(Gx, off, kS);
-      if (li >= off) Gx += y;
-    }
-    if (wid == 0) {
-      eG[lane] = exp2f(Gx);
-      eD[lane] = exp2f(__shfl(Gx, 16 * g + 15) - Gx);
-    }
+    // ---- 2. Gram blocks K_b K_b^T -> A_b = beta_i 2^{G_i - G_j} Gamma (i > j)
 #pragma unroll
     for (int n = 0; n < (4 + NW - 1) / NW; ++n) {
       const int sb = wid + n * NW;   // sub-chunk
@@ -255,37 +249,37 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
       for (int s = 0; s < D / 32; ++s)
         gam = mma_k32(gam, as_bf16x8(lds_ld16(Kr + kv_row + (16 * sb * KP + 32 * s) * 2)),
                       as_bf16x8(lds_ld16(Kr + kv_row + (16 * sb * KP + 32 * s) * 2)));
-      const float gj = __shfl(Gx, 16 * sb + li);
+      const float gj = gs[16 * sb + li];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = 4 * g + r;
-        const float gi = __shfl(Gx, 16 * sb + i);
+        const float gi = gs[16 * sb + i];
         Am[(16 * sb + i) * kAP + li] = (i > li) ? bs[16 * sb + i] * exp2f(fminf(gi - gj, 0.f)) * gam[r] : 0.f;
       }
     }
     lds_barrier();
 
-    // ---- 3. T_b = (I + A_b)^{-1} by column-sweep substitution (wave 0, lane =
+    // ---- 3. T_b = (I + A_b)^{-1} by forward substitution (wave 0, lane =
     //         (sub-chunk, column)); Tu = T diag(beta), Tw = T diag(beta 2^G),
     //         rounded once, written straight from the solved columns
     if (wid == 0) {
       const int sb = g, c = li;
       const SR_LDS float* Ab = Am + 16 * sb * kAP;
-      float arow[16][16];
+      float x[16];
 #pragma unroll
-      for (int i = 1; i < 16; ++i)
+      for (int i = 0; i < 16; ++i) {
+        if (i % 4 == 0) __builtin_amdgcn_sched_barrier(0);   // bound the hoisting of A loads
+        float s0 = (i == c) ? 1.f : 0.f, s1 = 0.f;
 #pragma unroll
         for (int q = 0; q < (i + 3) / 4; ++q) {
           const float4 v = lds_ldf4((const lchar*)(Ab + i * kAP + 4 * q));
-          arow[i][4 * q + 0] = v.x; arow[i][4 * q + 1] = v.y; arow[i][4 * q + 2] = v.z; arow[i][4 * q + 3] = v.w;
+          if (4 * q + 0 < i) s0 = fmaf(-v.x, x[4 * q + 0], s0);
+          if (4 * q + 1 < i) s1 = fmaf(-v.y, x[4 * q + 1], s1);
+          if (4 * q + 2 < i) s0 = fmaf(-v.z, x[4 * q + 2], s0);
+          if (4 * q + 3 < i) s1 = fmaf(-v.w, x[4 * q + 3], s1);
         }
-      float x[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) x[i] = (i == c) ? 1.f : 0.f;
-#pragma unroll
-      for (int m = 0; m < 15; ++m)
-#pragma unroll
-        for (int i = m + 1; i < 16; ++i) x[i] = fmaf(-arow[i][m], x[m], x[i]);
+        x[i] = s0 + s1;
+      }
       const float bc = bs[16 * sb + c];
       const float wc = bc * eG[16 * sb + c];
 #pragma unroll

@@ -217,6 +217,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       c.Vbuf = Vb + (int64_t)l * plan.v_stride * plan.op_bytes;
       c.Gbuf = Gb + (int64_t)l * plan.g_stride;
       c.Bbuf = Bb + (int64_t)l * plan.g_stride;
+      c.g_mode = plan.op_dtype == SR_BF16 ? 1 : 0;   // the bf16 scan reads sub-chunk prefixes
       c.tail = w > 1 ? L.tail_out : nullptr;
       c.c_tail = c_tail;
       c.tail_kv_off = c_q;

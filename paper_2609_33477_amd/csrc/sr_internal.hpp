@@ -46,7 +46,10 @@ struct ConvGateArgs {
   float eps;
   void* Kbuf;         // [H_k][T][d] operand dtype
   void* Vbuf;         // [H_v][T][d]
-  float* Gbuf;        // [H_v][T] log alpha
+  float* Gbuf;        // [H_v][T]: g_mode 0 -> ln alpha per row; 1 -> log2 alpha summed
+                      // from the start of the row's 16-row sub-chunk (sub-chunks
+                      // start at the segment start and every 16 rows after it)
+  int32_t g_mode;
   float* Bbuf;        // [H_v][T] beta
   void* tail;         // [slots][c_tail][w-1] or nullptr
   int32_t c_tail;
