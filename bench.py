@@ -46,7 +46,12 @@ def algorithmic_work(wl, with_q=True):
         # one launch per layer
         "proj_gemm": ("mfma", 2.0 * T * D * N),
         "conv_gate": ("hbm", T * N * 4 + T * c_kv * es + 2 * T * hv * 4),
+        # fused projection + conv epilogue: the contraction is the bound; its
+        # HBM traffic is anchors + weights in, k_hat | v | G | beta out
+        "proj_conv": ("mfma", 2.0 * T * D * N),
         "tail": ("hbm", c_q * D * wb + len(live) * (w - 1) * ((c_q + c_kv) * tb + D * es)),
+        # one launch per call: 16 bytes of segment info per row
+        "row_info": ("hbm", T * 16),
         # one launch covers all layers (up to 32)
         "gdn_scan": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * d * d * 4)),
     }

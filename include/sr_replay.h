@@ -168,11 +168,15 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
 
 /* Kernels the replay launches, as indexed by sr_kernel_timing_read(). */
 typedef enum sr_kernel_kind {
-  SR_KERNEL_PROJ_GEMM = 0,   /* anchor projection (MFMA)                      */
-  SR_KERNEL_CONV_GATE = 1,   /* conv + SiLU + key norm + gates + k|v tail     */
+  SR_KERNEL_PROJ_GEMM = 0,   /* anchor projection (MFMA), fp32 path           */
+  SR_KERNEL_CONV_GATE = 1,   /* conv + SiLU + key norm + gates + k|v tail,
+                                fp32 path                                     */
   SR_KERNEL_TAIL = 2,        /* q part of the conv tail + zero fill           */
   SR_KERNEL_GDN_SCAN = 3,    /* chunked state accumulation                    */
-  SR_KERNEL_KINDS = 4
+  SR_KERNEL_PROJ_CONV = 4,   /* projection fused with conv, SiLU, key norm,
+                                gates and the k|v tail (bf16 / fp8 path)      */
+  SR_KERNEL_ROW_INFO = 5,    /* per-row segment position and slot (bf16 path) */
+  SR_KERNEL_KINDS = 6
 } sr_kernel_kind;
 
 /* Benchmark instrumentation (not needed by the replay itself).  While

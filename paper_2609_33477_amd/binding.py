@@ -74,7 +74,7 @@ LIB = _load()
 EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
                     "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_status_str")
 
-KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan")
+KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan", "proj_conv", "row_info")
 
 
 def make_shape(shape) -> SrShape:

@@ -54,41 +54,15 @@ __global__ __launch_bounds__(kConvThreads) void conv_gate_kernel(ConvGateArgs a)
   const int C_kv = n_heads * DH;
 
   if ((int)blockIdx.y == (int)gridDim.y - 1) {
-    // ---- gates
-    if (a.g_mode == 0) {
-      // thread -> (head, row), rows fastest: ln alpha and beta per row
-      const int rows = (int)(r1 - r0);
-      for (int idx = tid; idx < rows * a.H_v; idx += kConvThreads) {
-        const int h = idx / rows;
-        const int64_t t = r0 + idx % rows;
-        const float av = a.P[t * a.ldp + C_kv + h];
-        const float bv = a.P[t * a.ldp + C_kv + a.H_v + h];
-        a.Gbuf[(int64_t)h * a.T + t] = -expf(a.a_log[h]) * softplus(av + a.dt_bias[h]);
-        a.Bbuf[(int64_t)h * a.T + t] = sigmoid(bv);
-      }
-      return;
-    }
-    // g_mode 1: one thread per value head walks the block's rows and keeps the
-    // running sum of log2 alpha inside the current 16-row sub-chunk.
-    constexpr float kLog2e = 1.4426950408889634f;
-    for (int h = tid; h < a.H_v; h += kConvThreads) {
-      const float rate = expf(a.a_log[h]), bias = a.dt_bias[h];
-      auto log2_alpha = [&](int64_t t) { return -rate * softplus(a.P[t * a.ldp + C_kv + h] + bias) * kLog2e; };
-      int b = segment_of_row(a.cu, a.n_seg, r0);
-      int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
-      float run = 0.f;
-      for (int64_t t = s0 + ((r0 - s0) / 16) * 16; t < r0; ++t) run += log2_alpha(t);  // carry-in
-      for (int64_t t = r0; t < r1; ++t) {
-        while (t >= s1) {
-          ++b;
-          s0 = a.cu[b];
-          s1 = a.cu[b + 1];
-        }
-        if ((t - s0) % 16 == 0) run = 0.f;
-        run += log2_alpha(t);
-        a.Gbuf[(int64_t)h * a.T + t] = run;
-        a.Bbuf[(int64_t)h * a.T + t] = sigmoid(a.P[t * a.ldp + C_kv + a.H_v + h]);
-      }
+    // ---- gates: thread -> (head, row), rows fastest: ln alpha and beta per row
+    const int rows = (int)(r1 - r0);
+    for (int idx = tid; idx < rows * a.H_v; idx += kConvThreads) {
+      const int h = idx / rows;
+      const int64_t t = r0 + idx % rows;
+      const float av = a.P[t * a.ldp + C_kv + h];
+      const float bv = a.P[t * a.ldp + C_kv + a.H_v + h];
+      a.Gbuf[(int64_t)h * a.T + t] = -expf(a.a_log[h]) * softplus(av + a.dt_bias[h]);
+      a.Bbuf[(int64_t)h * a.T + t] = sigmoid(bv);
     }
     return;
   }

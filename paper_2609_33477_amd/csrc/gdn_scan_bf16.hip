@@ -95,6 +95,19 @@ __device__ __forceinline__ f32x4 mma_k16(const f32x4& c, const v4i16& a, const v
 }
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// value of lane - N inside the lane's 16-lane row (0 for the first N lanes)
+template <int N>
+__device__ __forceinline__ float dpp_row_shr(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x110 + N, 0xf, 0xf, false));
+}
+// value at lane 15 of 16-lane row `row` (0..3); every lane of the wave calls it
+__device__ __forceinline__ float row_last(float x, int row) {
+  const int v = __builtin_bit_cast(int, x);
+  const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31);
+  const int r2 = __builtin_amdgcn_readlane(v, 47), r3 = __builtin_amdgcn_readlane(v, 63);
+  return __builtin_bit_cast(float, row == 0 ? r0 : row == 1 ? r1 : row == 2 ? r2 : r3);
+}
+
 template <int D>
 struct Cfg {
   static constexpr int NW = D / 16;                   // waves; wave w owns state columns [16w, 16w+16)
@@ -147,7 +160,7 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
   SR_LDS float* Am = (SR_LDS float*)(L + CF::OFF_A);      // [64][kAP] fp32: block b = rows 16b..16b+15
   lchar* Tu = L + CF::OFF_T;                              // [64][kTP] bf16
   lchar* Tw = Tu + kC * kTP * 2;
-  SR_LDS float* gs = (SR_LDS float*)(L + CF::OFF_VEC);    // G: log2 alpha summed within the sub-chunk
+  SR_LDS float* gs = (SR_LDS float*)(L + CF::OFF_VEC);    // G: log2 alpha summed from the sub-chunk start
   SR_LDS float* bs = gs + kC;                             // beta
   SR_LDS float* eG = bs + kC;                             // 2^{G_i}      (G: sub-chunk prefix, log2)
   SR_LDS float* eD = eG + kC;                             // 2^{G_15 - G_i}
@@ -193,7 +206,7 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
   }
 
   uint4 pk[CF::PER_T], pv[CF::PER_T];
-  float pg = 0.f, pg15 = 0.f, pb = 0.f;
+  float pg = 0.f, pb = 0.f;
   auto prefetch = [&](int64_t c0) {
 #pragma unroll
     for (int i = 0; i < CF::PER_T; ++i) {
@@ -209,12 +222,9 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
       }
     }
     if (tid < kC) {
-      // G of this row and of its sub-chunk's last row; rows past the segment
-      // end carry log alpha = 0, so they repeat the last real row's G
-      const int64_t sub0 = c0 + (tid & ~15);
-      const int64_t t = min(c0 + tid, s1 - 1), t15 = min(sub0 + 15, s1 - 1);
-      pg = (t >= sub0) ? Gp[t] : 0.f;
-      pg15 = (t15 >= sub0) ? Gp[t15] : 0.f;
+      // log2 alpha and beta of the row; rows past the segment end carry
+      // log2 alpha = 0 and beta = 0, which makes them inert
+      pg = (c0 + tid < s1) ? Gp[c0 + tid] : 0.f;
       pb = (c0 + tid < s1) ? Bp[c0 + tid] : 0.f;
     }
   };
@@ -231,10 +241,18 @@ __global__ __launch_bounds__(64 * (D / 16), 2) void gdn_scan_bf16_kernel(ScanArg
       lds_st16(Vr + (row * KP + cc * 8) * 2, pv[i]);
     }
     if (tid < kC) {
-      gs[tid] = pg;
+      // wave 0: inclusive prefix of log2 alpha inside each 16-row sub-chunk
+      // (one 16-lane DPP row per sub-chunk), then its last value
+      float gp = pg;
+      gp += dpp_row_shr<1>(gp);
+      gp += dpp_row_shr<2>(gp);
+      gp += dpp_row_shr<4>(gp);
+      gp += dpp_row_shr<8>(gp);
+      const float g15 = row_last(gp, g);
+      gs[tid] = gp;
       bs[tid] = pb;
-      eG[tid] = exp2f(pg);
-      eD[tid] = exp2f(pg15 - pg);
+      eG[tid] = exp2f(gp);
+      eD[tid] = exp2f(g15 - gp);
     }
     lds_barrier();
     if (c0 + kC < s1) prefetch(c0 + kC);

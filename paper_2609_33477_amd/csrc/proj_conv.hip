@@ -1,0 +1,456 @@
+// Projection GEMM fused with the short causal conv, SiLU, key L2 norm, the
+// decay / erase gates and the k | v conv tail (bf16 anchors; bf16 or fp8
+// weights).
+//
+// What it computes (Section 2.1: the update's key, value and gates are linear
+// maps of the layer input; Appendix A: a width-w depthwise conv over the q, k, v
+// projections whose state is the last w-1 inputs):
+//   P      = X [W_k; W_v; W_a; W_b]^T                       (fp32 accumulate)
+//   k, v   = SiLU(sum_i cw[c][i] P[t-w+1+i][c])             (zero before the segment start)
+//   k_hat  = k / sqrt(|k|^2 + eps)                           (per key head)
+//   G      = log2 alpha = -exp(A_log) softplus(a + dt_bias) log2(e)
+//   beta   = sigmoid(b)
+// The projection never reaches HBM: each 256 x 256 output tile is finished in
+// LDS and only k_hat / v (bf16, head-major [H][T][d]), G and beta ([H_v][T],
+// fp32) and the tail rows are written.
+//
+// Main loop (gfx950): 4 waves, each a 128 x 128 quarter of the tile on
+// v_mfma_f32_32x32x16_bf16 with fp32 accumulators in AGPRs.  A and B stream
+// global -> LDS with global_load_lds_dwordx4 (no register staging) into 4 LDS
+// stages of BK = 32, three K-steps ahead of the MFMAs; 16-byte chunks are
+// XOR-swizzled inside each 64-byte row so fragment reads are conflict free.
+// fp8 (E4M3) weights are staged as bytes and converted to bf16 after the
+// fragment read (exact), the per-channel scale multiplies the fp32 result.
+// Tiles are dealt in contiguous runs per XCD and walked in groups of 8
+// M-tiles so concurrently running tiles share A and B panels in L2.
+//
+// Conv epilogue: M-tiles overlap by 3 rows (stride 253), so every output row's
+// w-1 predecessors are in the tile.  Each 128-column half of the accumulator
+// tile is written column-major to LDS; then every lane owns one tile row and
+// walks the half's columns: the previous rows come from neighbouring lanes
+// (DPP wave shift), the key norm is a per-lane sum (the lane holds the whole
+// head of its row), and each row's d outputs leave as 16-byte stores.
+#include "sr_device.hpp"
+
+#include <type_traits>
+
+namespace sr {
+namespace {
+
+constexpr int BM = 256, BN = 256, BK = 32, NS = 4, THREADS = 256;
+constexpr int HALO = 3, SM = BM - HALO;           // tile row stride
+constexpr int EP = 260;                            // LDS column pitch of the epilogue tile (floats)
+constexpr int E_BYTES = 128 * EP * 4;
+constexpr int TAP_BYTES = 128 * 4 * 4;             // conv taps of one 128-column half
+constexpr float kLog2e = 1.4426950408889634f;
+
+typedef __attribute__((address_space(3))) char lchar;
+typedef __attribute__((address_space(3))) float lfloat;
+typedef unsigned int nu32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int nu32x2 __attribute__((ext_vector_type(2)));
+typedef float nf32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 ld16(const lchar* p) {
+  return __builtin_bit_cast(uint4, *reinterpret_cast<const __attribute__((address_space(3))) nu32x4*>(p));
+}
+__device__ __forceinline__ uint2 ld8(const lchar* p) {
+  return __builtin_bit_cast(uint2, *reinterpret_cast<const __attribute__((address_space(3))) nu32x2*>(p));
+}
+
+template <typename TB> struct BT;
+template <> struct BT<bf16_t> { static constexpr int ROW = 64, BLKS = 4; };  // B row bytes per K-step; 1 KB DMA blocks per wave
+template <> struct BT<fp8_t> { static constexpr int ROW = 32, BLKS = 2; };
+
+// 16 bytes per lane, global -> LDS at lds_base + 16 * lane (wave-uniform
+// base).  Inline asm: the compiler would otherwise wait for every such load
+// before any later LDS read; completion is tracked by hand (wait_vm) before
+// the barrier that publishes a stage.
+__device__ __forceinline__ void dma16(const void* src, lchar* lds_base) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(l), "v"(src) : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N) with lgkmcnt and expcnt left at their maxima
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// 16-byte chunk swizzle inside a 64-byte LDS row
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+// hardware block id -> (m tile, n tile): contiguous runs per XCD (blocks are
+// dealt round-robin to the 8 XCDs), then groups of 8 m-tiles walked n-major
+__device__ __forceinline__ void tile_of(int b, int tm, int tn, int& mt, int& nt) {
+  const int nb = tm * tn;
+  const int per = nb / 8, rem = nb % 8;
+  const int x = b % 8, loc = b / 8;
+  const int t = x * per + (x < rem ? x : rem) + loc;
+  constexpr int GM = 8;
+  const int grp = t / (GM * tn);
+  const int first = grp * GM;
+  const int gs = (tm - first) < GM ? (tm - first) : GM;
+  const int idx = t - grp * GM * tn;
+  mt = first + idx % gs;
+  nt = idx / gs;
+}
+
+// value of lane-1 (lane 0 receives `first`)
+__device__ __forceinline__ float shift_down1(float x, float first) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, first),
+                                                               __builtin_bit_cast(int, x), 0x138, 0xf, 0xf, false));
+}
+
+__device__ __forceinline__ float fast_sigmoid(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
+__device__ __forceinline__ float softplus(float x) { return fmaxf(x, 0.f) + log1pf(__expf(-fabsf(x))); }
+
+__device__ __forceinline__ float load_elem(const void* p, int64_t i, bool is_bf16) {
+  return is_bf16 ? bf16_bits_to_f32(static_cast<const uint16_t*>(p)[i]) : static_cast<const float*>(p)[i];
+}
+__device__ __forceinline__ void store_elem(void* p, int64_t i, float v, bool is_bf16) {
+  if (is_bf16) static_cast<uint16_t*>(p)[i] = f32_to_bf16_bits(v);
+  else static_cast<float*>(p)[i] = v;
+}
+
+template <typename TB, int D>
+__global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, int tiles_m, int tiles_n) {
+  constexpr int BROW = BT<TB>::ROW, BBLK = BT<TB>::BLKS;
+  constexpr int A_BYTES = BM * 64, B_BYTES = BN * BROW, STAGE = A_BYTES + B_BYTES;
+  constexpr int LPK = 4 + BBLK;  // DMA instructions per wave per K-step
+  constexpr int LDS = NS * STAGE > E_BYTES + TAP_BYTES ? NS * STAGE : E_BYTES + TAP_BYTES;
+  __shared__ __attribute__((aligned(1024))) char smem_raw[LDS];
+  lchar* smem = (lchar*)smem_raw;
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+  int mt, nt;
+  tile_of(blockIdx.x, tiles_m, tiles_n, mt, nt);
+  const int64_t row0 = (int64_t)mt * SM - HALO;  // tile row 0 (negative for the first tile)
+  const int n0 = nt * BN;
+  const int K = a.K;
+  const int64_t T = a.T;
+
+  // ------------------------------------------------------------ main loop
+  // DMA sources: wave wid fills A blocks 4 wid .. 4 wid + 3 (16 rows each)
+  const char* a_src[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = (wid * 4 + i) * 16 + (lane >> 2);
+    const int c = (lane & 3) ^ swz(row);
+    int64_t m = row0 + row;
+    m = m < 0 ? 0 : (m >= T ? T - 1 : m);   // rows outside [0, T) are never output
+    a_src[i] = static_cast<const char*>(a.A) + (m * K + c * 8) * 2;
+  }
+  const char* b_src[BBLK];
+#pragma unroll
+  for (int i = 0; i < BBLK; ++i) {
+    int row, coff;
+    if (std::is_same<TB, bf16_t>::value) {
+      row = (wid * 4 + i) * 16 + (lane >> 2);
+      coff = ((lane & 3) ^ swz(row)) * 8;   // elements
+    } else {
+      row = (wid * 2 + i) * 32 + (lane >> 1);
+      coff = (lane & 1) * 16;
+    }
+    const int n = (n0 + row < a.N) ? n0 + row : a.N - 1;
+    const char* p = static_cast<const char*>(a.seg[0].ptr);
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      if (s < a.n_wseg && n >= a.seg[s].n0 && n < a.seg[s].n1)
+        p = static_cast<const char*>(a.seg[s].ptr) + ((int64_t)(n - a.seg[s].n0) * K + coff) * Elem<TB>::bytes;
+    b_src[i] = p;
+  }
+
+  const int fl = swz(lane & 31), hi = lane >> 5;
+  const int a_row_off = (wm * 128 + (lane & 31)) * 64;
+  const int a_k0 = a_row_off + ((0 + hi) ^ fl) * 16;
+  const int a_k1 = a_row_off + ((2 + hi) ^ fl) * 16;
+  int b_k0, b_k1;
+  if (std::is_same<TB, bf16_t>::value) {
+    const int b_row_off = A_BYTES + (wn * 128 + (lane & 31)) * 64;
+    b_k0 = b_row_off + ((0 + hi) ^ fl) * 16;
+    b_k1 = b_row_off + ((2 + hi) ^ fl) * 16;
+  } else {
+    const int b_row_off = A_BYTES + (wn * 128 + (lane & 31)) * 32;
+    b_k0 = b_row_off + hi * 8;
+    b_k1 = b_row_off + 16 + hi * 8;
+  }
+
+  bf16x8 fa[2][4], fb[2][4];
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = zero16();
+
+  // read order A0, B0, B1, B2, B3, A1, A2, A3: the first MFMAs of a sub-step
+  // (A0 x B0..B3) need only the first five reads
+  auto read_one = [&](int stage, int ks, int slot, int qq) {
+    const int q = qq == 0 ? 0 : (qq <= 4 ? qq + 3 : qq - 4);
+    const lchar* sb = smem + stage * STAGE;
+    if (q < 4) {
+      fa[slot][q] = as_bf16x8(ld16(sb + (ks ? a_k1 : a_k0) + q * 32 * 64));
+    } else if (std::is_same<TB, bf16_t>::value) {
+      fb[slot][q - 4] = as_bf16x8(ld16(sb + (ks ? b_k1 : b_k0) + (q - 4) * 32 * 64));
+    } else {
+      const uint2 v = ld8(sb + (ks ? b_k1 : b_k0) + (q - 4) * 32 * 32);
+      uint4 o;
+      o.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, false));
+      o.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, true));
+      o.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, false));
+      o.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, true));
+      fb[slot][q - 4] = as_bf16x8(o);
+    }
+  };
+  auto mma_one = [&](int slot, int q) {
+    const int i = q >> 2, j = q & 3;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j], 0, 0, 0);
+  };
+  auto dma_one = [&](int kt, int stage, int q) {
+    lchar* sb = smem + stage * STAGE;
+    if (q < 4) dma16(a_src[q] + (int64_t)kt * BK * 2, sb + (wid * 4 + q) * 1024);
+    else if (q - 4 < BBLK)
+      dma16(b_src[q - 4] + (int64_t)kt * BK * Elem<TB>::bytes, sb + A_BYTES + (wid * BBLK + q - 4) * 1024);
+  };
+
+  const int KT = K / BK;
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dma_one(s < KT ? s : KT - 1, s, q);
+  wait_vm<3 * LPK>();
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // no scalar loads in flight at loop entry
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) read_one(0, 0, 0, q);
+
+  for (int kt = 0; kt < KT; ++kt) {
+    const int st = kt & (NS - 1);
+    const int kn = kt + NS < KT ? kt + NS : KT - 1;
+    // sub-step 0: MFMAs on slot 0, fragments of the second k16 into slot 1
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      mma_one(0, q);
+      read_one(st, 1, 1, q);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q = 8; q < 16; ++q) mma_one(0, q);
+    // sub-step 1, first half
+#pragma unroll
+    for (int q = 0; q < 8; ++q) mma_one(1, q);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm<2 * LPK>();             // this wave's loads for kt+1 have landed
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_s_barrier();    // everyone's loads for kt+1 landed; stage st is free
+    __builtin_amdgcn_sched_barrier(0);
+    // second half: refill stage st with K-step kt+NS (clamped: the surplus
+    // refills of the last steps land in stages nobody reads again) and read
+    // the first fragments of kt+1
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      mma_one(1, 8 + q);
+      if (q < 4) {
+        read_one((kt + 1) & (NS - 1), 0, 0, 2 * q);
+        read_one((kt + 1) & (NS - 1), 0, 0, 2 * q + 1);
+        dma_one(kn, st, 2 * q);
+        dma_one(kn, st, 2 * q + 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  wait_vm<0>();                      // no DMA may land in LDS once it is reused
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ------------------------------------------------------------ epilogue
+  lfloat* E = (lfloat*)smem_raw;
+  lfloat* TAPS = (lfloat*)(smem_raw + E_BYTES);   // [128 columns][4]: tap for the row j back
+  const int r = wid * 64 + lane;              // tile row owned by this lane
+  const int64_t m = row0 + r;
+  RowInfo ri = {0, 0, -1, 0};
+  if (m >= 0 && m < T) ri = a.info[m];
+  const bool out = r >= HALO && m < T;        // m >= 0 holds for r >= HALO
+  const bool need_mask = __builtin_amdgcn_ballot_w64(out && ri.pos < HALO) != 0;
+  const int w1 = a.w - 1;
+  const bool tail_row = a.tail != nullptr && out && ri.slot >= 0 && ri.rem <= w1;
+  const bool any_tail = __builtin_amdgcn_ballot_w64(tail_row) != 0;
+  const int hoff = wid > 0 ? wid * 64 - 4 : 0;  // 4 rows before the wave's first row
+  const bool conv_bf16 = a.conv_bf16 != 0, tail_bf16 = a.tail_bf16 != 0;
+
+  for (int h = 0; h < 2; ++h) {
+    const int nh0 = n0 + h * 128;
+    if (nh0 >= a.N) break;
+    if (h) {
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_s_barrier();     // every wave is done reading half 0
+    }
+    if (wn == h) {
+      float sc[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        sc[j] = 1.f;
+        if (std::is_same<TB, fp8_t>::value) {
+          const int n = nh0 + j * 32 + (lane & 31);
+#pragma unroll
+          for (int s = 0; s < 4; ++s)
+            if (s < a.n_wseg && n >= a.seg[s].n0 && n < a.seg[s].n1)
+              sc[j] = Elem<bf16_t>::load(a.seg[s].scale, n - a.seg[s].n0);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int R0 = wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5);
+            const int c = j * 32 + (lane & 31);
+            nf32x4 v = {acc[i][j][4 * q] * sc[j], acc[i][j][4 * q + 1] * sc[j], acc[i][j][4 * q + 2] * sc[j],
+                        acc[i][j][4 * q + 3] * sc[j]};
+            *reinterpret_cast<__attribute__((address_space(3))) nf32x4*>(E + c * EP + R0) = v;
+          }
+    }
+    {
+      // conv taps of this half's k | v columns, indexed by rows back
+      const int c = tid >> 1, j0 = (tid & 1) * 2;
+      const int n = nh0 + c;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = j0 + jj;
+        TAPS[c * 4 + j] = (n < a.C_kv && j <= w1) ? load_elem(a.conv_w, (int64_t)n * a.w + w1 - j, conv_bf16) : 0.f;
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_s_barrier();
+
+    for (int g = 0; g < 128 / D; ++g) {
+      const int nb = nh0 + g * D;     // first projection column of this head group
+      if (nb >= a.N) break;
+      const int cg = g * D;           // column inside the half
+      if (nb < a.C_kv) {
+        // ---- one k or v head: conv, SiLU, (key) L2 norm
+        const bool is_k = nb < a.C_k;
+        const int hh = is_k ? nb / D : (nb - a.C_k) / D;
+        float yv[D];
+        float ss = 0.f;
+#pragma unroll
+        for (int e = 0; e < D; ++e) {
+          const int c = cg + e;
+          const lfloat* col = E + c * EP;
+          const float x = col[r];
+          const nf32x4 hv = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(col + hoff);
+          float x1 = shift_down1(x, hv.w);
+          float x2 = shift_down1(x1, hv.z);
+          float x3 = shift_down1(x2, hv.y);
+          if (need_mask) {
+            x1 = ri.pos >= 1 ? x1 : 0.f;
+            x2 = ri.pos >= 2 ? x2 : 0.f;
+            x3 = ri.pos >= 3 ? x3 : 0.f;
+          }
+          const nf32x4 tp = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(TAPS + c * 4);
+          float y = tp.x * x;
+          y = fmaf(tp.y, x1, y);
+          y = fmaf(tp.z, x2, y);
+          y = fmaf(tp.w, x3, y);
+          y = y * fast_sigmoid(y);
+          yv[e] = y;
+          ss = fmaf(y, y, ss);
+          if ((e & 7) == 7) __builtin_amdgcn_sched_barrier(0);   // bound the live ranges
+        }
+        const float inv = is_k ? 1.f / sqrtf(ss + a.eps) : 1.f;
+        if (out) {
+          char* dst = static_cast<char*>(is_k ? a.Kbuf : a.Vbuf) + (((int64_t)hh * T + m) * D) * 2;
+#pragma unroll
+          for (int q = 0; q < D / 8; ++q) {
+            uint4 o;
+            o.x = pack_bf16x2(yv[8 * q] * inv, yv[8 * q + 1] * inv);
+            o.y = pack_bf16x2(yv[8 * q + 2] * inv, yv[8 * q + 3] * inv);
+            o.z = pack_bf16x2(yv[8 * q + 4] * inv, yv[8 * q + 5] * inv);
+            o.w = pack_bf16x2(yv[8 * q + 6] * inv, yv[8 * q + 7] * inv);
+            *reinterpret_cast<uint4*>(dst + q * 16) = o;
+          }
+        }
+        // (after the stores: y must not be live across this divergent loop)
+        if (any_tail && tail_row) {
+          // the raw projection of the segment's last w-1 rows is the conv state
+          for (int e = 0; e < D; ++e)
+            store_elem(a.tail, ((int64_t)ri.slot * a.c_tail + a.tail_kv_off + nb + e) * w1 + (w1 - ri.rem),
+                       E[(cg + e) * EP + r], tail_bf16);
+        }
+
+      } else {
+        // ---- gate columns: G = log2 alpha from a, beta from b (no conv)
+        for (int e = 0; e < D; ++e) {
+          const int n = nb + e;
+          if (n >= a.N) break;
+          const float x = E[(cg + e) * EP + r];
+          if (n < a.C_kv + a.H_v) {
+            const int hv = n - a.C_kv;
+            const float gl = -__expf(a.a_log[hv]) * softplus(x + a.dt_bias[hv]) * kLog2e;
+            if (out) a.Gbuf[(int64_t)hv * T + m] = gl;
+          } else {
+            const int hv = n - a.C_kv - a.H_v;
+            if (out) a.Bbuf[(int64_t)hv * T + m] = fast_sigmoid(x);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <typename TB, int D>
+hipError_t run(const ProjConvArgs& a, hipStream_t s) {
+  if (a.T == 0) return hipSuccess;
+  if (a.K % BK) return hipErrorInvalidValue;
+  const int tm = (int)((a.T + SM - 1) / SM), tn = (a.N + BN - 1) / BN;
+  hipLaunchKernelGGL((proj_conv_kernel<TB, D>), dim3(tm * tn), dim3(THREADS), 0, s, a, tm, tn);
+  return hipGetLastError();
+}
+
+template <typename TB>
+hipError_t by_head(int d, const ProjConvArgs& a, hipStream_t s) {
+  switch (d) {
+    case 32: return run<TB, 32>(a, s);
+    case 64: return run<TB, 64>(a, s);
+    case 128: return run<TB, 128>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+// One block per segment: position in the segment, rows left, slot.
+__global__ void row_info_kernel(const int32_t* cu, const int32_t* slot_ids, RowInfo* info) {
+  const int b = blockIdx.x;
+  const int32_t s0 = cu[b], s1 = cu[b + 1];
+  const int32_t slot = slot_ids ? slot_ids[b] : b;
+  for (int32_t t = s0 + (int32_t)threadIdx.x; t < s1; t += (int32_t)blockDim.x) {
+    RowInfo v;
+    v.pos = t - s0;
+    v.rem = s1 - t;
+    v.slot = slot;
+    v.seg = b;
+    info[t] = v;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, RowInfo* info,
+                           hipStream_t s) {
+  if (n_seg == 0) return hipSuccess;
+  hipLaunchKernelGGL(row_info_kernel, dim3(n_seg), dim3(256), 0, s, cu, slot_ids, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvArgs& a, hipStream_t s) {
+  if (weight_dtype == SR_BF16) return by_head<bf16_t>(d_head, a, s);
+  if (weight_dtype == SR_FP8_E4M3) return by_head<fp8_t>(d_head, a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace sr

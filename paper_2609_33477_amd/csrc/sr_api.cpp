@@ -1,11 +1,17 @@
 // C ABI of the replay library: argument validation, workspace plan and the
 // launch sequence per call.
 //
-// Per layer (stream-ordered):
-//   1. proj_gemm   anchors x [W_k; W_v; W_a; W_b]^T -> P (fp32 workspace)
-//   2. conv_gate   P -> k_hat, v (operand dtype, head-major), log alpha, beta,
-//                  and the k | v part of the conv tail
-//   3. tail        q part of the conv tail (+ zeros before a segment's start)
+// bf16 / fp8 path (stream-ordered):
+//   row_info       once per call: position in segment, rows left, slot per row
+//   per layer:
+//     proj_conv    anchors x [W_k; W_v; W_a; W_b]^T fused with conv, SiLU, key
+//                  norm and gates -> k_hat, v (bf16, head-major), log2 alpha,
+//                  beta, and the k | v part of the conv tail
+//     tail         q part of the conv tail (+ zeros before a segment's start)
+// fp32 path, per layer:
+//     proj_gemm    anchors x [W_k; W_v; W_a; W_b]^T -> P (fp32 workspace)
+//     conv_gate    P -> k_hat, v, ln alpha, beta, k | v tail
+//     tail
 // then one chunked-scan launch per group of <= 32 layers writes the states.
 #include <hip/hip_runtime.h>
 
@@ -51,7 +57,7 @@ sr_status check_shape(const sr_shape* s) {
 
 struct Plan {
   int64_t ldp;                       // row pitch of P (floats)
-  int64_t off_p, off_k, off_v, off_g, off_b, total;
+  int64_t off_p, off_info, off_k, off_v, off_g, off_b, total;
   int64_t k_stride, v_stride, g_stride;   // per-layer strides (elements)
   int op_dtype, op_bytes;
 };
@@ -67,7 +73,11 @@ Plan make_plan(const sr_shape* s, int32_t n_layers, int64_t T) {
   p.v_stride = hv * T * d;
   p.g_stride = hv * T;
   int64_t off = 0;
-  p.off_p = off; off = align_up(off + T * p.ldp * 4, kAlign);
+  if (p.op_dtype == SR_F32) {        // only the unfused fp32 path stores the projection
+    p.off_p = off; off = align_up(off + T * p.ldp * 4, kAlign);
+  } else {
+    p.off_info = off; off = align_up(off + T * (int64_t)sizeof(sr::RowInfo), kAlign);
+  }
   p.off_k = off; off = align_up(off + n_layers * p.k_stride * p.op_bytes, kAlign);
   p.off_v = off; off = align_up(off + n_layers * p.v_stride * p.op_bytes, kAlign);
   p.off_g = off; off = align_up(off + n_layers * p.g_stride * 4, kAlign);
@@ -179,21 +189,57 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
   float* Gb = reinterpret_cast<float*>(ws + plan.off_g);
   float* Bb = reinterpret_cast<float*>(ws + plan.off_b);
 
+  const bool fused = plan.op_dtype == SR_BF16;
+  sr::RowInfo* info = reinterpret_cast<sr::RowInfo*>(ws + plan.off_info);
+  if (fused && t_total > 0) {
+    if (timed(SR_KERNEL_ROW_INFO, s, [&] { return sr::launch_row_info(cu_seqlens, slot_ids, n_segments, info, s); }) != hipSuccess)
+      return SR_ERR_HIP;
+  }
+
   for (int l = 0; l < n_layers; ++l) {
     const sr_layer& L = layers[l];
     const int c_q = L.w_q ? c_k : 0;
     const int c_tail = c_q + c_k + c_v;
-    if (t_total > 0) {
+    const sr::WeightSeg wseg[4] = {{L.w_k, L.s_k, 0, c_k},
+                                   {L.w_v, L.s_v, c_k, c_k + c_v},
+                                   {L.w_a, L.s_a, c_k + c_v, c_k + c_v + hv},
+                                   {L.w_b, L.s_b, c_k + c_v + hv, c_k + c_v + 2 * hv}};
+    if (t_total > 0 && fused) {
+      sr::ProjConvArgs f{};
+      f.A = L.anchors;
+      f.T = t_total;
+      f.K = shape->d_model;
+      f.N = c_k + c_v + 2 * hv;
+      f.n_wseg = 4;
+      for (int i = 0; i < 4; ++i) f.seg[i] = wseg[i];
+      f.info = info;
+      f.conv_w = L.conv_w;
+      f.conv_bf16 = shape->conv_dtype == SR_BF16;
+      f.w = w;
+      f.a_log = L.a_log;
+      f.dt_bias = L.dt_bias;
+      f.C_k = c_k;
+      f.C_kv = c_k + c_v;
+      f.H_v = hv;
+      f.eps = shape->l2_eps;
+      f.Kbuf = Kb + (int64_t)l * plan.k_stride * plan.op_bytes;
+      f.Vbuf = Vb + (int64_t)l * plan.v_stride * plan.op_bytes;
+      f.Gbuf = Gb + (int64_t)l * plan.g_stride;
+      f.Bbuf = Bb + (int64_t)l * plan.g_stride;
+      f.tail = w > 1 ? L.tail_out : nullptr;
+      f.tail_bf16 = shape->tail_dtype == SR_BF16;
+      f.c_tail = c_tail;
+      f.tail_kv_off = c_q;
+      if (timed(SR_KERNEL_PROJ_CONV, s, [&] { return sr::launch_proj_conv(shape->weight_dtype, d, f, s); }) != hipSuccess)
+        return SR_ERR_HIP;
+    } else if (t_total > 0) {
       sr::GemmArgs g{};
       g.A = L.anchors;
       g.M = t_total;
       g.K = shape->d_model;
       g.N = c_k + c_v + 2 * hv;
       g.n_seg = 4;
-      g.seg[0] = {L.w_k, L.s_k, 0, c_k};
-      g.seg[1] = {L.w_v, L.s_v, c_k, c_k + c_v};
-      g.seg[2] = {L.w_a, L.s_a, c_k + c_v, c_k + c_v + hv};
-      g.seg[3] = {L.w_b, L.s_b, c_k + c_v + hv, c_k + c_v + 2 * hv};
+      for (int i = 0; i < 4; ++i) g.seg[i] = wseg[i];
       g.C = P;
       g.ldc = plan.ldp;
       if (timed(SR_KERNEL_PROJ_GEMM, s, [&] { return sr::launch_proj_gemm(shape->anchor_dtype, shape->weight_dtype, g, s); }) != hipSuccess)
@@ -217,7 +263,6 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       c.Vbuf = Vb + (int64_t)l * plan.v_stride * plan.op_bytes;
       c.Gbuf = Gb + (int64_t)l * plan.g_stride;
       c.Bbuf = Bb + (int64_t)l * plan.g_stride;
-      c.g_mode = plan.op_dtype == SR_BF16 ? 1 : 0;   // the bf16 scan reads sub-chunk prefixes
       c.tail = w > 1 ? L.tail_out : nullptr;
       c.c_tail = c_tail;
       c.tail_kv_off = c_q;

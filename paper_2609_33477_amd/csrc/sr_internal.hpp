@@ -30,6 +30,42 @@ struct GemmArgs {
 
 hipError_t launch_proj_gemm(int anchor_dtype, int weight_dtype, const GemmArgs& a, hipStream_t s);
 
+// ------------------------------- fused projection + conv + gates (bf16 path)
+// Per packed row: position inside its segment, rows left in the segment
+// (this one included) and the segment's slot id (< 0: sentinel).
+struct RowInfo {
+  int32_t pos, rem, slot, seg;
+};
+
+struct ProjConvArgs {
+  const void* A;        // anchors [T][K] bf16
+  int64_t T;
+  int32_t K;
+  int32_t N;            // projection width C_kv + 2 H_v (columns k | v | a | b)
+  int32_t n_wseg;
+  WeightSeg seg[4];
+  const RowInfo* info;  // [T]
+  const void* conv_w;   // [C_kv][w]
+  int32_t conv_bf16;    // conv_w dtype: 1 bf16, 0 fp32
+  int32_t w;
+  const float* a_log;
+  const float* dt_bias;
+  int32_t C_k, C_kv, H_v;
+  float eps;
+  void* Kbuf;           // [H_k][T][d] bf16
+  void* Vbuf;           // [H_v][T][d] bf16
+  float* Gbuf;          // [H_v][T] log2 alpha per row
+  float* Bbuf;          // [H_v][T] beta
+  void* tail;           // [slots][c_tail][w-1] or nullptr
+  int32_t tail_bf16;
+  int32_t c_tail;
+  int32_t tail_kv_off;
+};
+
+hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, RowInfo* info,
+                           hipStream_t s);
+hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvArgs& a, hipStream_t s);
+
 // --------------------------------------------------- conv, activations, gates
 struct ConvGateArgs {
   const float* P;     // [T][ldp] projection, columns k | v | a | b
@@ -46,10 +82,7 @@ struct ConvGateArgs {
   float eps;
   void* Kbuf;         // [H_k][T][d] operand dtype
   void* Vbuf;         // [H_v][T][d]
-  float* Gbuf;        // [H_v][T]: g_mode 0 -> ln alpha per row; 1 -> log2 alpha summed
-                      // from the start of the row's 16-row sub-chunk (sub-chunks
-                      // start at the segment start and every 16 rows after it)
-  int32_t g_mode;
+  float* Gbuf;        // [H_v][T] ln alpha per row
   float* Bbuf;        // [H_v][T] beta
   void* tail;         // [slots][c_tail][w-1] or nullptr
   int32_t c_tail;
@@ -83,7 +116,8 @@ constexpr int kScanMaxLayers = 32;
 struct ScanArgs {
   const void* Kbuf;     // layer l at Kbuf + l * kv_layer_stride elements: [H_k][T][d]
   const void* Vbuf;     // [H_v][T][d]
-  const float* Gbuf;    // layer l at + l * g_layer_stride: [H_v][T]
+  const float* Gbuf;    // layer l at + l * g_layer_stride: [H_v][T]; per-row log decay:
+                        // ln alpha (fp32 path) or log2 alpha (bf16 path)
   const float* Bbuf;
   int64_t k_layer_stride, v_layer_stride, g_layer_stride;
   int64_t T;

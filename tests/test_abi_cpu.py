@@ -53,11 +53,16 @@ def test_workspace_size_plan():
     shape = Shape(2560, 16, 32, 128, 128)
     t = 36672
     ws = sr.replay_workspace_size(shape, 1, t)
-    n = 16 * 128 + 32 * 128 + 64
-    # fp32 projection rows + bf16 k|v + fp32 log-alpha/beta, each 256-byte aligned
-    expect = t * n * 4 + t * (16 + 32) * 128 * 2 + 2 * t * 32 * 4
+    # bf16 path: per-row segment info (16 B) + bf16 k|v + fp32 log-alpha/beta,
+    # each region 256-byte aligned; the projection itself never reaches HBM
+    expect = t * 16 + t * (16 + 32) * 128 * 2 + 2 * t * 32 * 4
     assert expect <= ws <= expect + 5 * 256
-    assert sr.replay_workspace_size(shape, 12, t) > 11 * (ws - t * n * 4)
+    assert sr.replay_workspace_size(shape, 12, t) > 11 * (ws - t * 16)
+    # fp32 path keeps the fp32 projection rows in the workspace
+    f32 = Shape(256, 2, 2, 32, 32, anchor_dtype=F32, weight_dtype=F32, conv_dtype=F32, tail_dtype=F32)
+    n = (2 + 2) * 32 + 4
+    expect32 = 1000 * n * 4 + 1000 * 4 * 32 * 4 + 2 * 1000 * 2 * 4
+    assert expect32 <= sr.replay_workspace_size(f32, 1, 1000) <= expect32 + 5 * 256
 
 
 @pytest.mark.parametrize("bad,code", [
