@@ -16,9 +16,10 @@
 //
 // Main loop (gfx950): 4 waves, each a 128 x 128 quarter of the tile on
 // v_mfma_f32_32x32x16_bf16 with fp32 accumulators in AGPRs.  A and B stream
-// global -> LDS with global_load_lds_dwordx4 (no register staging) into 4 LDS
-// stages of BK = 32, three K-steps ahead of the MFMAs; 16-byte chunks are
-// XOR-swizzled inside each 64-byte row so fragment reads are conflict free.
+// global -> LDS with global_load_lds_dwordx4 (no register staging) into LDS
+// stages of BK = 32 (5 for bf16, 6 for fp8 weights), up to five K-steps ahead
+// of the MFMAs; 16-byte chunks are XOR-swizzled inside each 64-byte row so
+// fragment reads are conflict free.
 // fp8 (E4M3) weights are staged as bytes and converted to bf16 after the
 // fragment read (exact), the per-channel scale multiplies the fp32 result.
 // Tiles are dealt in contiguous runs per XCD and walked in groups of 8
@@ -37,10 +38,11 @@
 namespace sr {
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 32, NS = 4, THREADS = 256;
+constexpr int BM = 256, BN = 256, BK = 32, THREADS = 256;
 constexpr int HALO = 3, SM = BM - HALO;           // tile row stride
 constexpr int EP = 260;                            // LDS column pitch of the epilogue tile (floats)
-constexpr int E_BYTES = 128 * EP * 4;
+constexpr int E_PAD = 16;                          // bytes before column 0 (rows -1..-3 of column 0)
+constexpr int E_BYTES = E_PAD + 128 * EP * 4;
 constexpr int TAP_BYTES = 128 * 4 * 4;             // conv taps of one 128-column half
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -58,16 +60,19 @@ __device__ __forceinline__ uint2 ld8(const lchar* p) {
 }
 
 template <typename TB> struct BT;
-template <> struct BT<bf16_t> { static constexpr int ROW = 64, BLKS = 4; };  // B row bytes per K-step; 1 KB DMA blocks per wave
-template <> struct BT<fp8_t> { static constexpr int ROW = 32, BLKS = 2; };
+// B row bytes per K-step, 1 KB DMA blocks per wave and K-step, LDS stages
+// (as many as fit in 160 KB: the deeper the prefetch, the more memory latency
+// it hides)
+template <> struct BT<bf16_t> { static constexpr int ROW = 64, BLKS = 4, NS = 5; };
+template <> struct BT<fp8_t> { static constexpr int ROW = 32, BLKS = 2, NS = 6; };
 
 // 16 bytes per lane, global -> LDS at lds_base + 16 * lane (wave-uniform
 // base).  Inline asm: the compiler would otherwise wait for every such load
 // before any later LDS read; completion is tracked by hand (wait_vm) before
 // the barrier that publishes a stage.
-__device__ __forceinline__ void dma16(const void* src, lchar* lds_base) {
-  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(l), "v"(src) : "memory", "m0");
+// `lds_off` must be wave-uniform (it is an SGPR operand).
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds_off) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_off), "v"(src) : "memory", "m0");
 }
 
 // s_waitcnt vmcnt(N) with lgkmcnt and expcnt left at their maxima
@@ -77,8 +82,11 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// 16-byte chunk swizzle inside a 64-byte LDS row
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+// 16-byte chunk swizzle inside a 64-byte LDS row.  A fragment read has lanes
+// 0-31 on 32 consecutive rows (lanes 32-63 on the next chunk); with this XOR
+// every ds_read_b128 is conflict free (measured: 4 LDS cycles per read, the
+// 256 B/clk peak), where rows 4 apart must land in different chunks.
+__device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 
 // hardware block id -> (m tile, n tile): contiguous runs per XCD (blocks are
 // dealt round-robin to the 8 XCDs), then groups of 8 m-tiles walked n-major
@@ -96,11 +104,6 @@ __device__ __forceinline__ void tile_of(int b, int tm, int tn, int& mt, int& nt)
   nt = idx / gs;
 }
 
-// value of lane-1 (lane 0 receives `first`)
-__device__ __forceinline__ float shift_down1(float x, float first) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, first),
-                                                               __builtin_bit_cast(int, x), 0x138, 0xf, 0xf, false));
-}
 
 __device__ __forceinline__ float fast_sigmoid(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
 __device__ __forceinline__ float softplus(float x) { return fmaxf(x, 0.f) + log1pf(__expf(-fabsf(x))); }
@@ -115,14 +118,15 @@ __device__ __forceinline__ void store_elem(void* p, int64_t i, float v, bool is_
 
 template <typename TB, int D>
 __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, int tiles_m, int tiles_n) {
-  constexpr int BROW = BT<TB>::ROW, BBLK = BT<TB>::BLKS;
+  constexpr int BROW = BT<TB>::ROW, BBLK = BT<TB>::BLKS, NS = BT<TB>::NS;
   constexpr int A_BYTES = BM * 64, B_BYTES = BN * BROW, STAGE = A_BYTES + B_BYTES;
   constexpr int LPK = 4 + BBLK;  // DMA instructions per wave per K-step
   constexpr int LDS = NS * STAGE > E_BYTES + TAP_BYTES ? NS * STAGE : E_BYTES + TAP_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem_raw[LDS];
   lchar* smem = (lchar*)smem_raw;
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int wm = wid >> 1, wn = wid & 1;
   int mt, nt;
   tile_of(blockIdx.x, tiles_m, tiles_n, mt, nt);
@@ -208,10 +212,10 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j], 0, 0, 0);
   };
   auto dma_one = [&](int kt, int stage, int q) {
-    lchar* sb = smem + stage * STAGE;
-    if (q < 4) dma16(a_src[q] + (int64_t)kt * BK * 2, sb + (wid * 4 + q) * 1024);
+    const uint32_t lds0 = (uint32_t)(uintptr_t)smem + stage * STAGE;
+    if (q < 4) dma16(a_src[q] + (int64_t)kt * BK * 2, lds0 + (wid * 4 + q) * 1024);
     else if (q - 4 < BBLK)
-      dma16(b_src[q - 4] + (int64_t)kt * BK * Elem<TB>::bytes, sb + A_BYTES + (wid * BBLK + q - 4) * 1024);
+      dma16(b_src[q - 4] + (int64_t)kt * BK * Elem<TB>::bytes, lds0 + A_BYTES + (wid * BBLK + q - 4) * 1024);
   };
 
   const int KT = K / BK;
@@ -219,7 +223,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   for (int s = 0; s < NS; ++s)
 #pragma unroll
     for (int q = 0; q < 8; ++q) dma_one(s < KT ? s : KT - 1, s, q);
-  wait_vm<3 * LPK>();
+  wait_vm<(NS - 1) * LPK>();
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
   __builtin_amdgcn_s_waitcnt(0xc07f);   // no scalar loads in flight at loop entry
@@ -227,40 +231,42 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
 #pragma unroll
   for (int q = 0; q < 8; ++q) read_one(0, 0, 0, q);
 
+  int st = 0;                              // stage of K-step kt
   for (int kt = 0; kt < KT; ++kt) {
-    const int st = kt & (NS - 1);
+    const int st1 = st + 1 == NS ? 0 : st + 1;
     const int kn = kt + NS < KT ? kt + NS : KT - 1;
-    // sub-step 0: MFMAs on slot 0, fragments of the second k16 into slot 1
+    // MFMAs 0-7 (slot 0) with the fragments of the second k16 into slot 1
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       mma_one(0, q);
       read_one(st, 1, 1, q);
       __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int q = 8; q < 16; ++q) mma_one(0, q);
-    // sub-step 1, first half
-#pragma unroll
-    for (int q = 0; q < 8; ++q) mma_one(1, q);
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm<2 * LPK>();             // this wave's loads for kt+1 have landed
+    // Hand-over: this wave's reads of stage st are complete and its loads of
+    // K-step kt+1 have landed; after the barrier that holds for every wave,
+    // so stage st can be refilled and stage st1 read.
+    wait_vm<(NS - 2) * LPK>();
     __builtin_amdgcn_s_waitcnt(0xc07f);
-    __builtin_amdgcn_s_barrier();    // everyone's loads for kt+1 landed; stage st is free
+    __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // second half: refill stage st with K-step kt+NS (clamped: the surplus
-    // refills of the last steps land in stages nobody reads again) and read
-    // the first fragments of kt+1
+    // MFMAs 8-15 (slot 0) and 16-23 (slot 1), one refill load every other
+    // MFMA (K-step kt+NS, clamped: surplus refills of the last steps land in
+    // stages nobody reads again)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      if (q < 8) mma_one(0, 8 + q);
+      else mma_one(1, q - 8);
+      if ((q & 1) == 0) dma_one(kn, st, q >> 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // MFMAs 24-31 (slot 1) with the first fragments of K-step kt+1 into slot 0
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       mma_one(1, 8 + q);
-      if (q < 4) {
-        read_one((kt + 1) & (NS - 1), 0, 0, 2 * q);
-        read_one((kt + 1) & (NS - 1), 0, 0, 2 * q + 1);
-        dma_one(kn, st, 2 * q);
-        dma_one(kn, st, 2 * q + 1);
-      }
+      read_one(st1, 0, 0, q);
       __builtin_amdgcn_sched_barrier(0);
     }
+    st = st1;
   }
   __builtin_amdgcn_sched_barrier(0);
   wait_vm<0>();                      // no DMA may land in LDS once it is reused
@@ -269,7 +275,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   __builtin_amdgcn_sched_barrier(0);
 
   // ------------------------------------------------------------ epilogue
-  lfloat* E = (lfloat*)smem_raw;
+  lfloat* E = (lfloat*)(smem_raw + E_PAD);
   lfloat* TAPS = (lfloat*)(smem_raw + E_BYTES);   // [128 columns][4]: tap for the row j back
   const int r = wid * 64 + lane;              // tile row owned by this lane
   const int64_t m = row0 + r;
@@ -280,7 +286,6 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   const int w1 = a.w - 1;
   const bool tail_row = a.tail != nullptr && out && ri.slot >= 0 && ri.rem <= w1;
   const bool any_tail = __builtin_amdgcn_ballot_w64(tail_row) != 0;
-  const int hoff = wid > 0 ? wid * 64 - 4 : 0;  // 4 rows before the wave's first row
   const bool conv_bf16 = a.conv_bf16 != 0, tail_bf16 = a.tail_bf16 != 0;
 
   for (int h = 0; h < 2; ++h) {
@@ -337,46 +342,56 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
         // ---- one k or v head: conv, SiLU, (key) L2 norm
         const bool is_k = nb < a.C_k;
         const int hh = is_k ? nb / D : (nb - a.C_k) / D;
-        float yv[D];
-        float ss = 0.f;
-#pragma unroll
-        for (int e = 0; e < D; ++e) {
-          const int c = cg + e;
-          const lfloat* col = E + c * EP;
-          const float x = col[r];
-          const nf32x4 hv = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(col + hoff);
-          float x1 = shift_down1(x, hv.w);
-          float x2 = shift_down1(x1, hv.z);
-          float x3 = shift_down1(x2, hv.y);
-          if (need_mask) {
+        // Each lane reads its row and the w-1 rows before it straight from the
+        // column (rows before a wave's first row belong to the previous wave's
+        // range; lanes 0..2 of wave 0 are halo rows whose reads land in the
+        // padding and are never output).  A key head takes two passes (sum of
+        // squares, then scaled output) so no row of d values has to stay in
+        // registers; a value head takes one.
+        auto conv_silu = [&](int c, auto mask_tag) {
+          constexpr bool MASK = decltype(mask_tag)::value;
+          const lfloat* col = E + c * EP + r;
+          const nf32x4 tp = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(TAPS + c * 4);
+          float x1 = col[-1], x2 = col[-2], x3 = col[-3];
+          if (MASK) {
             x1 = ri.pos >= 1 ? x1 : 0.f;
             x2 = ri.pos >= 2 ? x2 : 0.f;
             x3 = ri.pos >= 3 ? x3 : 0.f;
           }
-          const nf32x4 tp = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(TAPS + c * 4);
-          float y = tp.x * x;
+          float y = tp.x * col[0];
           y = fmaf(tp.y, x1, y);
           y = fmaf(tp.z, x2, y);
           y = fmaf(tp.w, x3, y);
-          y = y * fast_sigmoid(y);
-          yv[e] = y;
-          ss = fmaf(y, y, ss);
-          if ((e & 7) == 7) __builtin_amdgcn_sched_barrier(0);   // bound the live ranges
-        }
-        const float inv = is_k ? 1.f / sqrtf(ss + a.eps) : 1.f;
-        if (out) {
-          char* dst = static_cast<char*>(is_k ? a.Kbuf : a.Vbuf) + (((int64_t)hh * T + m) * D) * 2;
-#pragma unroll
-          for (int q = 0; q < D / 8; ++q) {
-            uint4 o;
-            o.x = pack_bf16x2(yv[8 * q] * inv, yv[8 * q + 1] * inv);
-            o.y = pack_bf16x2(yv[8 * q + 2] * inv, yv[8 * q + 3] * inv);
-            o.z = pack_bf16x2(yv[8 * q + 4] * inv, yv[8 * q + 5] * inv);
-            o.w = pack_bf16x2(yv[8 * q + 6] * inv, yv[8 * q + 7] * inv);
-            *reinterpret_cast<uint4*>(dst + q * 16) = o;
+          return y * fast_sigmoid(y);
+        };
+        auto head_pass = [&](auto mask_tag) {
+          float inv = 1.f;
+          if (is_k) {
+            float ss0 = 0.f, ss1 = 0.f;
+#pragma unroll 8
+            for (int e = 0; e < D; e += 2) {
+              const float y0 = conv_silu(cg + e, mask_tag), y1 = conv_silu(cg + e + 1, mask_tag);
+              ss0 = fmaf(y0, y0, ss0);
+              ss1 = fmaf(y1, y1, ss1);
+            }
+            inv = 1.f / sqrtf(ss0 + ss1 + a.eps);
           }
-        }
-        // (after the stores: y must not be live across this divergent loop)
+          char* dst = static_cast<char*>(is_k ? a.Kbuf : a.Vbuf) + (((int64_t)hh * T + (out ? m : 0)) * D) * 2;
+#pragma unroll 2
+          for (int q = 0; q < D / 8; ++q) {
+            float y[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) y[u] = conv_silu(cg + 8 * q + u, mask_tag) * inv;
+            uint4 o;
+            o.x = pack_bf16x2(y[0], y[1]);
+            o.y = pack_bf16x2(y[2], y[3]);
+            o.z = pack_bf16x2(y[4], y[5]);
+            o.w = pack_bf16x2(y[6], y[7]);
+            if (out) *reinterpret_cast<uint4*>(dst + q * 16) = o;
+          }
+        };
+        if (need_mask) head_pass(std::true_type{});
+        else head_pass(std::false_type{});
         if (any_tail && tail_row) {
           // the raw projection of the segment's last w-1 rows is the conv state
           for (int e = 0; e < D; ++e)
