@@ -13,10 +13,14 @@
 // Outputs are head-major ([H][T][d], [H][T]) so the scan reads each 64-row
 // chunk of a head as one contiguous block.
 //
-// tail_kernel: per (segment, 64 tail channels): q channels are projected from
-// the anchors of the segment's last w-1 rows (W_q is used nowhere else);
-// positions before the segment's first row are zero-filled for every channel.
-// The k | v channels of existing rows are written by conv_gate_kernel.
+// Conv tail, q part (W_q is used nowhere else): the q projections of every
+// segment's last w-1 rows, and zeros at positions before a segment's first
+// row (every channel).  The k | v channels of existing rows are written with
+// k and v.
+//   tail_q_mfma_kernel (bf16 anchors): one small GEMM over the gathered tail
+//     rows of all segments x the q channels, on v_mfma_f32_32x32x16_bf16
+//     (32 x 32 outputs per block, reduction split over its 4 waves).
+//   tail_kernel (fp32 anchors): per (segment, 64 channels) dot products.
 #include "sr_device.hpp"
 
 #include <type_traits>
@@ -260,12 +264,112 @@ __global__ __launch_bounds__(kTailThreads) void tail_kernel(TailArgs a) {
   }
 }
 
+// 8 consecutive weights at element i as a bf16 MFMA operand (fp8: exact)
+template <typename TW>
+__device__ __forceinline__ bf16x8 load_w8(const void* p, int64_t i);
+template <>
+__device__ __forceinline__ bf16x8 load_w8<bf16_t>(const void* p, int64_t i) {
+  return as_bf16x8(*reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i));
+}
+template <>
+__device__ __forceinline__ bf16x8 load_w8<fp8_t>(const void* p, int64_t i) {
+  const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p) + i);
+  uint4 o;
+  o.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, false));
+  o.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, true));
+  o.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, false));
+  o.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, true));
+  return as_bf16x8(o);
+}
+
+// Tail row r = (segment r / (w-1), position r % (w-1)) -> anchor row, or -1
+// when the position precedes the segment's first row or the slot is a
+// sentinel.
+__device__ __forceinline__ int64_t tail_row(const TailArgs& a, int r, int* slot, int* pos) {
+  const int w1 = a.w - 1;
+  const int b = r / w1;
+  *pos = r - b * w1;
+  *slot = a.slot_ids ? a.slot_ids[b] : b;
+  const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
+  const int64_t t = s1 - w1 + *pos;
+  return (*slot >= 0 && t >= s0) ? t : -1;
+}
+
+// Block: 32 tail rows x 32 q channels; the 4 waves split the reduction over
+// d_model in quarters and combine their accumulators through LDS.
+template <typename TW, typename TT>
+__global__ __launch_bounds__(256) void tail_q_mfma_kernel(TailArgs a) {
+  __shared__ float part[3][16][64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int R = a.n_seg * (a.w - 1);
+  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+  int slot, pos;
+  const int r = r0 + (lane & 31);
+  const int64_t t = r < R ? tail_row(a, r, &slot, &pos) : -1;
+  const int c = min(c0 + (lane & 31), a.c_q - 1);
+  const uint16_t* xa = static_cast<const uint16_t*>(a.anchors) + (t >= 0 ? t : 0) * a.D;
+  const int64_t wrow = (int64_t)c * a.D;
+  const int kq = a.D / 4;                       // d_model is a multiple of 64
+  f32x16 acc = zero16();
+#pragma unroll 8
+  for (int k = wid * kq + 8 * (lane >> 5); k < (wid + 1) * kq; k += 16) {
+    const bf16x8 av = as_bf16x8(*reinterpret_cast<const uint4*>(xa + k));
+    const bf16x8 bv = load_w8<TW>(a.w_q, wrow + k);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
+  }
+  if (wid > 0) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) part[wid - 1][i][lane] = acc[i];
+  }
+  __syncthreads();
+  if (wid > 0) return;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] += part[0][i][lane] + part[1][i][lane] + part[2][i][lane];
+  const int col = c0 + (lane & 31);
+  if (col >= a.c_q) return;
+  const float scale = std::is_same<TW, fp8_t>::value ? Elem<bf16_t>::load(a.s_q, col) : 1.f;
+  const int w1 = a.w - 1;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int rr = r0 + acc_row(i, lane);
+    if (rr >= R) continue;
+    int sl, ps;
+    if (tail_row(a, rr, &sl, &ps) >= 0)
+      Elem<TT>::store(a.tail, ((int64_t)sl * a.c_tail + col) * w1 + ps, acc[i] * scale);
+  }
+}
+
+// Zeros at tail positions before a segment's first row, every channel.
+template <typename TT>
+__global__ __launch_bounds__(256) void tail_zero_kernel(TailArgs a) {
+  const int b = blockIdx.x;
+  const int slot = a.slot_ids ? a.slot_ids[b] : b;
+  const int w1 = a.w - 1;
+  const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
+  const int npos = (int)min<int64_t>(w1, max<int64_t>(0, s0 - (s1 - w1)));  // leading positions to clear
+  if (slot < 0 || npos == 0) return;
+  for (int idx = threadIdx.x; idx < a.c_tail * npos; idx += blockDim.x) {
+    const int c = idx / npos, p = idx % npos;
+    Elem<TT>::store(a.tail, ((int64_t)slot * a.c_tail + c) * w1 + p, 0.f);
+  }
+}
+
 template <typename TA, typename TW, typename TT>
 hipError_t run_tail(const TailArgs& a, hipStream_t s) {
   if (a.n_seg == 0 || a.w < 2 || a.c_tail == 0) return hipSuccess;
-  dim3 grid(a.n_seg, (a.c_tail + kTailChannels - 1) / kTailChannels);
-  hipLaunchKernelGGL((tail_kernel<TA, TW, TT>), grid, dim3(kTailThreads), 0, s, a);
-  return hipGetLastError();
+  if constexpr (std::is_same<TA, bf16_t>::value) {
+    hipLaunchKernelGGL((tail_zero_kernel<TT>), dim3(a.n_seg), dim3(256), 0, s, a);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+    if (a.c_q == 0) return hipSuccess;
+    const int R = a.n_seg * (a.w - 1);
+    dim3 grid((a.c_q + 31) / 32, (R + 31) / 32);
+    hipLaunchKernelGGL((tail_q_mfma_kernel<TW, TT>), grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  } else {
+    dim3 grid(a.n_seg, (a.c_tail + kTailChannels - 1) / kTailChannels);
+    hipLaunchKernelGGL((tail_kernel<TA, TW, TT>), grid, dim3(kTailThreads), 0, s, a);
+    return hipGetLastError();
+  }
 }
 
 template <typename TT>

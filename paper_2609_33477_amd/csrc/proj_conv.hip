@@ -40,10 +40,16 @@ namespace {
 
 constexpr int BM = 256, BN = 256, BK = 32, THREADS = 256;
 constexpr int HALO = 3, SM = BM - HALO;           // tile row stride
-constexpr int EP = 260;                            // LDS column pitch of the epilogue tile (floats)
-constexpr int E_PAD = 16;                          // bytes before column 0 (rows -1..-3 of column 0)
-constexpr int E_BYTES = E_PAD + 128 * EP * 4;
-constexpr int TAP_BYTES = 128 * 4 * 4;             // conv taps of one 128-column half
+// Epilogue tile in LDS: one 128-column half of the accumulator tile,
+// row-major (pitch EROW floats: 16-byte reads by 16 consecutive rows are
+// conflict free), split into 4 bands of 64 rows (one per wave).  Each band
+// holds its rows at slots 4..67 and copies of the 3 rows before it at slots
+// 1..3, so a lane reads its row and the w-1 rows before it at fixed offsets
+// and may overwrite its own row without racing a neighbouring wave.
+constexpr int EROW = 132;
+constexpr int EBAND = 68;
+constexpr int E_BYTES = 4 * EBAND * EROW * 4;
+constexpr int TAP_BYTES = 4 * 128 * 4;              // taps [rows back][column] of one half
 constexpr float kLog2e = 1.4426950408889634f;
 
 typedef __attribute__((address_space(3))) char lchar;
@@ -235,11 +241,12 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   for (int kt = 0; kt < KT; ++kt) {
     const int st1 = st + 1 == NS ? 0 : st + 1;
     const int kn = kt + NS < KT ? kt + NS : KT - 1;
-    // MFMAs 0-7 (slot 0) with the fragments of the second k16 into slot 1
+    // MFMAs 0-15 (first k16, slot 0) with the second k16's fragments into
+    // slot 1 over the first 8
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
+    for (int q = 0; q < 16; ++q) {
       mma_one(0, q);
-      read_one(st, 1, 1, q);
+      if (q < 8) read_one(st, 1, 1, q);
       __builtin_amdgcn_sched_barrier(0);
     }
     // Hand-over: this wave's reads of stage st are complete and its loads of
@@ -249,21 +256,15 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // MFMAs 8-15 (slot 0) and 16-23 (slot 1), one refill load every other
-    // MFMA (K-step kt+NS, clamped: surplus refills of the last steps land in
-    // stages nobody reads again)
+    // MFMAs 16-31 (slot 1): the next K-step's first fragments into slot 0
+    // over the first 8, one refill load every other MFMA (K-step kt+NS,
+    // clamped: the surplus refills of the last steps land in stages nobody
+    // reads again)
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
-      if (q < 8) mma_one(0, 8 + q);
-      else mma_one(1, q - 8);
+      mma_one(1, q);
+      if (q < 8) read_one(st1, 0, 0, q);
       if ((q & 1) == 0) dma_one(kn, st, q >> 1);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // MFMAs 24-31 (slot 1) with the first fragments of K-step kt+1 into slot 0
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      mma_one(1, 8 + q);
-      read_one(st1, 0, 0, q);
       __builtin_amdgcn_sched_barrier(0);
     }
     st = st1;
@@ -275,9 +276,10 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   __builtin_amdgcn_sched_barrier(0);
 
   // ------------------------------------------------------------ epilogue
-  lfloat* E = (lfloat*)(smem_raw + E_PAD);
-  lfloat* TAPS = (lfloat*)(smem_raw + E_BYTES);   // [128 columns][4]: tap for the row j back
+  lfloat* E = (lfloat*)smem_raw;
+  lfloat* TAPS = (lfloat*)(smem_raw + E_BYTES);
   const int r = wid * 64 + lane;              // tile row owned by this lane
+  lfloat* erow = E + (wid * EBAND + 4 + lane) * EROW;   // its slot
   const int64_t m = row0 + r;
   RowInfo ri = {0, 0, -1, 0};
   if (m >= 0 && m < T) ri = a.info[m];
@@ -311,24 +313,31 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int R0 = wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5);
-            const int c = j * 32 + (lane & 31);
-            nf32x4 v = {acc[i][j][4 * q] * sc[j], acc[i][j][4 * q + 1] * sc[j], acc[i][j][4 * q + 2] * sc[j],
-                        acc[i][j][4 * q + 3] * sc[j]};
-            *reinterpret_cast<__attribute__((address_space(3))) nf32x4*>(E + c * EP + R0) = v;
+          for (int e = 0; e < 4; ++e) {
+            const int R = wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5) + e;
+            const int band = R >> 6, rb = R & 63;
+            lfloat* dst = E + (band * EBAND + 4 + rb) * EROW + (lane & 31);
+            // the last 3 rows of a band are also the next band's halo
+            const bool halo = rb >= 61 && band < 3;
+            lfloat* hdst = E + ((band + 1) * EBAND + 1 + (rb - 61)) * EROW + (lane & 31);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const float v = acc[i][j][4 * q + e] * sc[j];
+              dst[j * 32] = v;
+              if (halo) hdst[j * 32] = v;
+            }
           }
     }
     {
-      // conv taps of this half's k | v columns, indexed by rows back
+      // conv taps of this half's k | v columns: TAPS[j][c] multiplies row t-j
       const int c = tid >> 1, j0 = (tid & 1) * 2;
       const int n = nh0 + c;
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj) {
         const int j = j0 + jj;
-        TAPS[c * 4 + j] = (n < a.C_kv && j <= w1) ? load_elem(a.conv_w, (int64_t)n * a.w + w1 - j, conv_bf16) : 0.f;
+        TAPS[j * 128 + c] = (n < a.C_kv && j <= w1) ? load_elem(a.conv_w, (int64_t)n * a.w + w1 - j, conv_bf16) : 0.f;
       }
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
@@ -339,72 +348,89 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
       if (nb >= a.N) break;
       const int cg = g * D;           // column inside the half
       if (nb < a.C_kv) {
-        // ---- one k or v head: conv, SiLU, (key) L2 norm
+        // ---- one k or v head: conv, SiLU, (key) L2 norm.  Columns go 4 at a
+        // time (16-byte reads of this row and the 3 before it).
         const bool is_k = nb < a.C_k;
         const int hh = is_k ? nb / D : (nb - a.C_k) / D;
-        // Each lane reads its row and the w-1 rows before it straight from the
-        // column (rows before a wave's first row belong to the previous wave's
-        // range; lanes 0..2 of wave 0 are halo rows whose reads land in the
-        // padding and are never output).  A key head takes two passes (sum of
-        // squares, then scaled output) so no row of d values has to stay in
-        // registers; a value head takes one.
-        auto conv_silu = [&](int c, auto mask_tag) {
+        auto conv4 = [&](int c, auto mask_tag) {
           constexpr bool MASK = decltype(mask_tag)::value;
-          const lfloat* col = E + c * EP + r;
-          const nf32x4 tp = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(TAPS + c * 4);
-          float x1 = col[-1], x2 = col[-2], x3 = col[-3];
-          if (MASK) {
-            x1 = ri.pos >= 1 ? x1 : 0.f;
-            x2 = ri.pos >= 2 ? x2 : 0.f;
-            x3 = ri.pos >= 3 ? x3 : 0.f;
-          }
-          float y = tp.x * col[0];
-          y = fmaf(tp.y, x1, y);
-          y = fmaf(tp.z, x2, y);
-          y = fmaf(tp.w, x3, y);
-          return y * fast_sigmoid(y);
-        };
-        auto head_pass = [&](auto mask_tag) {
-          float inv = 1.f;
-          if (is_k) {
-            float ss0 = 0.f, ss1 = 0.f;
-#pragma unroll 8
-            for (int e = 0; e < D; e += 2) {
-              const float y0 = conv_silu(cg + e, mask_tag), y1 = conv_silu(cg + e + 1, mask_tag);
-              ss0 = fmaf(y0, y0, ss0);
-              ss1 = fmaf(y1, y1, ss1);
-            }
-            inv = 1.f / sqrtf(ss0 + ss1 + a.eps);
-          }
-          char* dst = static_cast<char*>(is_k ? a.Kbuf : a.Vbuf) + (((int64_t)hh * T + (out ? m : 0)) * D) * 2;
-#pragma unroll 2
-          for (int q = 0; q < D / 8; ++q) {
-            float y[8];
+          nf32x4 x[4], tp[4];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) y[u] = conv_silu(cg + 8 * q + u, mask_tag) * inv;
-            uint4 o;
-            o.x = pack_bf16x2(y[0], y[1]);
-            o.y = pack_bf16x2(y[2], y[3]);
-            o.z = pack_bf16x2(y[4], y[5]);
-            o.w = pack_bf16x2(y[6], y[7]);
-            if (out) *reinterpret_cast<uint4*>(dst + q * 16) = o;
+          for (int j = 0; j < 4; ++j) {
+            x[j] = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow - j * EROW + c);
+            tp[j] = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(TAPS + j * 128 + c);
+          }
+          if (MASK) {
+#pragma unroll
+            for (int j = 1; j < 4; ++j)
+              if (ri.pos < j) x[j] = nf32x4{0.f, 0.f, 0.f, 0.f};
+          }
+          nf32x4 y;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            float v = tp[0][u] * x[0][u];
+            v = fmaf(tp[1][u], x[1][u], v);
+            v = fmaf(tp[2][u], x[2][u], v);
+            v = fmaf(tp[3][u], x[3][u], v);
+            y[u] = v * fast_sigmoid(v);
+          }
+          return y;
+        };
+        char* dst = static_cast<char*>(is_k ? a.Kbuf : a.Vbuf) + (((int64_t)hh * T + (out ? m : 0)) * D) * 2;
+        auto head_pass = [&](auto mask_tag) {
+          if (is_k) {
+            // pass 1: y and its sum of squares; y replaces x in this row's
+            // slot (rows after it have read x already: same wave, earlier
+            // instruction; the next band reads its own halo copy)
+            float ss0 = 0.f, ss1 = 0.f;
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+#pragma unroll 4
+            for (int c = cg; c < cg + D; c += 4) {
+              const nf32x4 y = conv4(c, mask_tag);
+              ss0 = fmaf(y[0], y[0], fmaf(y[1], y[1], ss0));
+              ss1 = fmaf(y[2], y[2], fmaf(y[3], y[3], ss1));
+              *reinterpret_cast<__attribute__((address_space(3))) nf32x4*>(erow + c) = y;
+            }
+            const float inv = 1.f / sqrtf(ss0 + ss1 + a.eps);
+#pragma unroll 4
+            for (int q = 0; q < D / 8; ++q) {
+              const nf32x4 y0 = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow + cg + 8 * q);
+              const nf32x4 y1 = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow + cg + 8 * q + 4);
+              uint4 o;
+              o.x = pack_bf16x2(y0[0] * inv, y0[1] * inv);
+              o.y = pack_bf16x2(y0[2] * inv, y0[3] * inv);
+              o.z = pack_bf16x2(y1[0] * inv, y1[1] * inv);
+              o.w = pack_bf16x2(y1[2] * inv, y1[3] * inv);
+              if (out) *reinterpret_cast<uint4*>(dst + q * 16) = o;
+            }
+          } else {
+#pragma unroll 2
+            for (int q = 0; q < D / 8; ++q) {
+              const nf32x4 y0 = conv4(cg + 8 * q, mask_tag), y1 = conv4(cg + 8 * q + 4, mask_tag);
+              uint4 o;
+              o.x = pack_bf16x2(y0[0], y0[1]);
+              o.y = pack_bf16x2(y0[2], y0[3]);
+              o.z = pack_bf16x2(y1[0], y1[1]);
+              o.w = pack_bf16x2(y1[2], y1[3]);
+              if (out) *reinterpret_cast<uint4*>(dst + q * 16) = o;
+            }
           }
         };
-        if (need_mask) head_pass(std::true_type{});
-        else head_pass(std::false_type{});
+        // the raw projection of the segment's last w-1 rows is the conv state
+        // (before a key head's pass overwrites the row)
         if (any_tail && tail_row) {
-          // the raw projection of the segment's last w-1 rows is the conv state
           for (int e = 0; e < D; ++e)
             store_elem(a.tail, ((int64_t)ri.slot * a.c_tail + a.tail_kv_off + nb + e) * w1 + (w1 - ri.rem),
-                       E[(cg + e) * EP + r], tail_bf16);
+                       erow[cg + e], tail_bf16);
         }
-
+        if (need_mask) head_pass(std::true_type{});
+        else head_pass(std::false_type{});
       } else {
         // ---- gate columns: G = log2 alpha from a, beta from b (no conv)
         for (int e = 0; e < D; ++e) {
           const int n = nb + e;
           if (n >= a.N) break;
-          const float x = E[(cg + e) * EP + r];
+          const float x = erow[cg + e];
           if (n < a.C_kv + a.H_v) {
             const int hv = n - a.C_kv;
             const float gl = -__expf(a.a_log[hv]) * softplus(x + a.dt_bias[hv]) * kLog2e;
