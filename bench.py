@@ -10,12 +10,21 @@ d_k=d_v=128, bf16 (the Qwen3.5-4B linear-layer shape), seeded synthetic data.
 Prints ONE JSON line on stdout; progress goes to stderr.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload varlen16]
+    python bench.py --copy-probe      # plain copy of known size, for HBM counter scaling
+
+`roofline.traffic` is the dominant kernel's measured HBM bytes per launch,
+read from profiles/traffic_<workload>.json (rocprofv3 FETCH_SIZE / WRITE_SIZE
+runs, scaled by what the same counters read for the copy probe); it is null
+when that file is missing or was taken from different kernel sources.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
 import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
 
 METRIC = "replayed anchor tokens/sec (state reconstruction) + % MFMA/HBM roofline"
 
@@ -57,6 +66,53 @@ def algorithmic_work(wl, with_q=True):
     }
 
 
+# sources each kernel is built from (the traffic record is void once they change)
+KERNEL_SOURCES = {
+    "proj_conv": ("proj_conv.hip", "sr_device.hpp", "sr_internal.hpp"),
+    "gdn_scan": ("gdn_scan_bf16.hip", "sr_device.hpp", "sr_internal.hpp"),
+    "proj_gemm": ("proj_gemm.hip", "sr_device.hpp", "sr_internal.hpp"),
+}
+
+
+def kernel_source_hash(kernel):
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES.get(kernel, ()):
+        with open(os.path.join(ROOT, "paper_2609_33477_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter record, or
+    None if there is none for these kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if kernel not in KERNEL_SOURCES or not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get("kernels", {}).get(kernel)
+    if not rec or rec.get("source_sha256") != kernel_source_hash(kernel):
+        return None
+    return rec.get("traffic_bytes")
+
+
+def copy_probe(n_bytes=1 << 30, launches=5):
+    """A plain elementwise copy (y = -x over fp32) that reads and writes
+    exactly n_bytes each: the reference for scaling FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    x = torch.ones(n_bytes // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    torch.neg(x, out=y)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(launches):
+        torch.neg(x, out=y)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / launches
+    print(json.dumps({"probe": "copy", "read_bytes": n_bytes, "write_bytes": n_bytes, "launches": launches + 1,
+                      "avg_ms": round(ms, 4), "GBps": round(2 * n_bytes / (ms * 1e-3) / 1e9, 1)}), flush=True)
+
+
 def cpu_baseline(wl, budget_s=15.0):
     """The fp64 oracle on a bounded sample of the same workload: whole
     segments, in order, until ~budget_s of CPU work."""
@@ -93,6 +149,7 @@ def main():
     ap.add_argument("--workload", default="varlen16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--copy-probe", action="store_true", help="time a plain 1 GiB copy and exit")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -100,6 +157,10 @@ def main():
         print(f"bench.py measures one MI355X: the replay path here runs on a single GPU "
               f"(--gpus {args.gpus}, WORLD_SIZE {world} requested). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_probe:
+        copy_probe()
+        return
 
     import torch
     import workloads as W
@@ -160,8 +221,9 @@ def main():
                       "frac": round(ach / peak, 4)}
     dom = max(kernels, key=lambda k: kernels[k]["share"])
     d = kernels[dom]
+    traffic = measured_traffic(wl.name, dom)
     roofline = {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
-                "frac": d["frac"], "traffic": None, "kernel": dom}
+                "frac": d["frac"], "traffic": traffic, "kernel": dom}
 
     cpu = None
     if not args.no_cpu_baseline:
