@@ -21,16 +21,25 @@
 // of the MFMAs; 16-byte chunks are XOR-swizzled inside each 64-byte row so
 // fragment reads are conflict free.
 // fp8 (E4M3) weights are staged as bytes and converted to bf16 after the
-// fragment read (exact), the per-channel scale multiplies the fp32 result.
+// fragment read (exact); the per-channel scale is folded into the conv taps
+// (the conv is linear per column) and applied to the gate and tail values.
+// Weights are the MFMA's first operand, so each lane's accumulators hold 4
+// consecutive columns of one output row.
 // Tiles are dealt in contiguous runs per XCD and walked in groups of 8
-// M-tiles so concurrently running tiles share A and B panels in L2.
+// M-tiles so concurrently running tiles share A and B panels in L2.  In a
+// narrow last N-tile (the 2 H_v gate columns) waves skip the MFMAs and
+// fragment reads of columns past N.
 //
 // Conv epilogue: M-tiles overlap by 3 rows (stride 253), so every output row's
 // w-1 predecessors are in the tile.  Each 128-column half of the accumulator
-// tile is written column-major to LDS; then every lane owns one tile row and
-// walks the half's columns: the previous rows come from neighbouring lanes
-// (DPP wave shift), the key norm is a per-lane sum (the lane holds the whole
-// head of its row), and each row's d outputs leave as 16-byte stores.
+// tile goes to LDS row-major with 16-byte writes, in 4 bands of 64 rows (one
+// per wave) that each also hold a copy of the 3 rows before them.  Every lane
+// then owns one row and walks the half's columns 4 at a time: conv over its
+// row and the 3 before it, SiLU, and for a key head the sum of squares, with
+// the activation written back in place (only this lane reads its row after
+// that) and scaled by the inverse norm on a second pass; each row's d outputs
+// leave as 16-byte stores.  The segment info and conv taps the epilogue needs
+// are loaded before the main loop.
 #include "sr_device.hpp"
 
 #include <type_traits>
@@ -111,6 +120,25 @@ __device__ __forceinline__ void tile_of(int b, int tm, int tn, int& mt, int& nt)
 }
 
 
+__device__ __forceinline__ void st_f4(lfloat* p, float x, float y, float z, float w) {
+  *reinterpret_cast<__attribute__((address_space(3))) nf32x4*>(p) = nf32x4{x, y, z, w};
+}
+
+// bf16 scale of fp8 weight column n (selected without branches, one load)
+__device__ __forceinline__ const uint16_t* col_scale_ptr(const ProjConvArgs& a, int n) {
+  const uint16_t* p = static_cast<const uint16_t*>(a.seg[0].scale) + (n - a.seg[0].n0);
+#pragma unroll
+  for (int s = 1; s < 4; ++s)
+    if (s < a.n_wseg && n >= a.seg[s].n0 && n < a.seg[s].n1) p = static_cast<const uint16_t*>(a.seg[s].scale) + (n - a.seg[s].n0);
+  return p;
+}
+// per-output-column scale of fp8 weights (1 for bf16 weights)
+template <typename TB>
+__device__ __forceinline__ float col_scale(const ProjConvArgs& a, int n) {
+  if constexpr (std::is_same<TB, fp8_t>::value) return bf16_bits_to_f32(*col_scale_ptr(a, n));
+  return 1.f;
+}
+
 __device__ __forceinline__ float fast_sigmoid(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
 __device__ __forceinline__ float softplus(float x) { return fmaxf(x, 0.f) + log1pf(__expf(-fabsf(x))); }
 
@@ -140,6 +168,38 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   const int n0 = nt * BN;
   const int K = a.K;
   const int64_t T = a.T;
+
+  // Epilogue inputs, fetched before the first DMA so their latency hides
+  // under the main loop (and no wait_vm count below has to include them):
+  // the segment info of the tile row this lane will own, and the conv taps
+  // (fp8 column scale folded in) this thread will stage for each half.
+  const int r = wid * 64 + lane;              // tile row owned by this lane
+  const int64_t m = row0 + r;
+  RowInfo ri = {0, 0, -1, 0};
+  if (m >= 0 && m < T) ri = a.info[m];
+  // Raw tap bits: nothing reads them before the epilogue, so no wait for
+  // these loads is placed ahead of the main loop.
+  uint32_t tap_bits[2][2] = {{0u, 0u}, {0u, 0u}};
+  uint32_t tap_sc[2] = {0x3f80u, 0x3f80u};   // bf16 bits of the column scale
+  {
+    const int c = tid >> 1, j0 = (tid & 1) * 2;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int n = n0 + h * 128 + c;
+      if (n < a.C_kv) {
+        if constexpr (std::is_same<TB, fp8_t>::value) tap_sc[h] = *col_scale_ptr(a, n);
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const int j = j0 + jj;
+          const int64_t i = (int64_t)n * a.w + a.w - 1 - j;
+          if (j <= a.w - 1) {
+            if (a.conv_bf16) tap_bits[h][jj] = static_cast<const uint16_t*>(a.conv_w)[i];
+            else tap_bits[h][jj] = static_cast<const uint32_t*>(a.conv_w)[i];
+          }
+        }
+      }
+    }
+  }
 
   // ------------------------------------------------------------ main loop
   // DMA sources: wave wid fills A blocks 4 wid .. 4 wid + 3 (16 rows each)
@@ -213,9 +273,12 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
       fb[slot][q - 4] = as_bf16x8(o);
     }
   };
+  // Weights go in as the MFMA's first operand, so acc[i][j] is the
+  // transposed 32x32 block: lane l holds row 32 i + l%32 of the wave's
+  // sub-tile, columns 32 j + 8 q + 4 (l/32) .. +3 in registers 4q .. 4q+3.
   auto mma_one = [&](int slot, int q) {
     const int i = q >> 2, j = q & 3;
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j], 0, 0, 0);
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][j], fa[slot][i], acc[i][j], 0, 0, 0);
   };
   auto dma_one = [&](int kt, int stage, int q) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem + stage * STAGE;
@@ -224,51 +287,63 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
       dma16(b_src[q - 4] + (int64_t)kt * BK * Elem<TB>::bytes, lds0 + A_BYTES + (wid * BBLK + q - 4) * 1024);
   };
 
-  const int KT = K / BK;
+  // The main loop, specialised on the number NJ of 32-column B fragments
+  // this wave multiplies: 4, or fewer in the narrow last N-tile (for the
+  // shapes here: the gate columns), where waves skip the MFMAs and fragment
+  // reads of columns past N but keep the DMA share and every barrier.
+  auto main_loop = [&](auto nj_tag) {
+    constexpr int NJ = decltype(nj_tag)::value;
+    auto read_used = [&](int qq) { return qq == 0 || qq > 4 || qq - 1 < NJ; };
+    const int KT = K / BK;
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
-    for (int q = 0; q < 8; ++q) dma_one(s < KT ? s : KT - 1, s, q);
-  wait_vm<(NS - 1) * LPK>();
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_sched_barrier(0);
-  __builtin_amdgcn_s_waitcnt(0xc07f);   // no scalar loads in flight at loop entry
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int q = 0; q < 8; ++q) read_one(0, 0, 0, q);
-
-  int st = 0;                              // stage of K-step kt
-  for (int kt = 0; kt < KT; ++kt) {
-    const int st1 = st + 1 == NS ? 0 : st + 1;
-    const int kn = kt + NS < KT ? kt + NS : KT - 1;
-    // MFMAs 0-15 (first k16, slot 0) with the second k16's fragments into
-    // slot 1 over the first 8
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      mma_one(0, q);
-      if (q < 8) read_one(st, 1, 1, q);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // Hand-over: this wave's reads of stage st are complete and its loads of
-    // K-step kt+1 have landed; after the barrier that holds for every wave,
-    // so stage st can be refilled and stage st1 read.
-    wait_vm<(NS - 2) * LPK>();
-    __builtin_amdgcn_s_waitcnt(0xc07f);
+      for (int q = 0; q < 8; ++q) dma_one(s < KT ? s : KT - 1, s, q);
+    wait_vm<(NS - 1) * LPK>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // MFMAs 16-31 (slot 1): the next K-step's first fragments into slot 0
-    // over the first 8, one refill load every other MFMA (K-step kt+NS,
-    // clamped: the surplus refills of the last steps land in stages nobody
-    // reads again)
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // no scalar loads in flight at loop entry
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      mma_one(1, q);
-      if (q < 8) read_one(st1, 0, 0, q);
-      if ((q & 1) == 0) dma_one(kn, st, q >> 1);
+    for (int q = 0; q < 8; ++q) if (read_used(q)) read_one(0, 0, 0, q);
+
+    int st = 0;                              // stage of K-step kt
+    for (int kt = 0; kt < KT; ++kt) {
+      const int st1 = st + 1 == NS ? 0 : st + 1;
+      const int kn = kt + NS < KT ? kt + NS : KT - 1;
+      // MFMAs 0-15 (first k16, slot 0) with the second k16's fragments into
+      // slot 1 over the first 8
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        if ((q & 3) < NJ) mma_one(0, q);
+        if (q < 8 && read_used(q)) read_one(st, 1, 1, q);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // Hand-over: this wave's reads of stage st are complete and its loads of
+      // K-step kt+1 have landed; after the barrier that holds for every wave,
+      // so stage st can be refilled and stage st1 read.
+      wait_vm<(NS - 2) * LPK>();
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
+      // MFMAs 16-31 (slot 1): the next K-step's first fragments into slot 0
+      // over the first 8, one refill load every other MFMA (K-step kt+NS,
+      // clamped: the surplus refills of the last steps land in stages nobody
+      // reads again)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        if ((q & 3) < NJ) mma_one(1, q);
+        if (q < 8 && read_used(q)) read_one(st1, 0, 0, q);
+        if ((q & 1) == 0) dma_one(kn, st, q >> 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      st = st1;
     }
-    st = st1;
-  }
+  };
+  const int n_wave = a.N - (n0 + wn * 128);        // valid columns of this wave's 128
+  if (n_wave > 64) main_loop(std::integral_constant<int, 4>{});
+  else if (n_wave > 0) main_loop(std::integral_constant<int, 2>{});
+  else main_loop(std::integral_constant<int, 0>{});
   __builtin_amdgcn_sched_barrier(0);
   wait_vm<0>();                      // no DMA may land in LDS once it is reused
   __builtin_amdgcn_s_waitcnt(0xc07f);
@@ -278,17 +353,13 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   // ------------------------------------------------------------ epilogue
   lfloat* E = (lfloat*)smem_raw;
   lfloat* TAPS = (lfloat*)(smem_raw + E_BYTES);
-  const int r = wid * 64 + lane;              // tile row owned by this lane
-  lfloat* erow = E + (wid * EBAND + 4 + lane) * EROW;   // its slot
-  const int64_t m = row0 + r;
-  RowInfo ri = {0, 0, -1, 0};
-  if (m >= 0 && m < T) ri = a.info[m];
+  lfloat* erow = E + (wid * EBAND + 4 + lane) * EROW;   // slot of row r
   const bool out = r >= HALO && m < T;        // m >= 0 holds for r >= HALO
   const bool need_mask = __builtin_amdgcn_ballot_w64(out && ri.pos < HALO) != 0;
   const int w1 = a.w - 1;
   const bool tail_row = a.tail != nullptr && out && ri.slot >= 0 && ri.rem <= w1;
   const bool any_tail = __builtin_amdgcn_ballot_w64(tail_row) != 0;
-  const bool conv_bf16 = a.conv_bf16 != 0, tail_bf16 = a.tail_bf16 != 0;
+  const bool tail_bf16 = a.tail_bf16 != 0;
 
   for (int h = 0; h < 2; ++h) {
     const int nh0 = n0 + h * 128;
@@ -298,47 +369,37 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
       __builtin_amdgcn_s_barrier();     // every wave is done reading half 0
     }
     if (wn == h) {
-      float sc[4];
+      // 16-byte row-major writes (4 consecutive columns per lane); 16 rows
+      // 132 floats apart cover all 64 banks once
+      const int lr = lane & 31, c4 = 4 * (lane >> 5);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        sc[j] = 1.f;
-        if (std::is_same<TB, fp8_t>::value) {
-          const int n = nh0 + j * 32 + (lane & 31);
+      for (int i = 0; i < 4; ++i) {
+        const int band = wm * 2 + (i >> 1), rb = (i & 1) * 32 + lr;
+        lfloat* dst = E + (band * EBAND + 4 + rb) * EROW + c4;
 #pragma unroll
-          for (int s = 0; s < 4; ++s)
-            if (s < a.n_wseg && n >= a.seg[s].n0 && n < a.seg[s].n1)
-              sc[j] = Elem<bf16_t>::load(a.seg[s].scale, n - a.seg[s].n0);
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            st_f4(dst + j * 32 + 8 * q, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+        // the last 3 rows of a band are also the next band's halo
+        if ((i & 1) && band < 3 && lr >= 61 - 32) {
+          lfloat* hdst = E + ((band + 1) * EBAND + 1 + (rb - 61)) * EROW + c4;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              st_f4(hdst + j * 32 + 8 * q, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
         }
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int R = wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5) + e;
-            const int band = R >> 6, rb = R & 63;
-            lfloat* dst = E + (band * EBAND + 4 + rb) * EROW + (lane & 31);
-            // the last 3 rows of a band are also the next band's halo
-            const bool halo = rb >= 61 && band < 3;
-            lfloat* hdst = E + ((band + 1) * EBAND + 1 + (rb - 61)) * EROW + (lane & 31);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const float v = acc[i][j][4 * q + e] * sc[j];
-              dst[j * 32] = v;
-              if (halo) hdst[j * 32] = v;
-            }
-          }
     }
     {
       // conv taps of this half's k | v columns: TAPS[j][c] multiplies row t-j
+      // (an fp8 column's scale is folded in: the conv is linear per column)
       const int c = tid >> 1, j0 = (tid & 1) * 2;
-      const int n = nh0 + c;
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        const int j = j0 + jj;
-        TAPS[j * 128 + c] = (n < a.C_kv && j <= w1) ? load_elem(a.conv_w, (int64_t)n * a.w + w1 - j, conv_bf16) : 0.f;
-      }
+      const float sc = bf16_bits_to_f32((uint16_t)(h ? tap_sc[1] : tap_sc[0]));
+      const int sh = a.conv_bf16 ? 16 : 0;
+      TAPS[j0 * 128 + c] = __builtin_bit_cast(float, (h ? tap_bits[1][0] : tap_bits[0][0]) << sh) * sc;
+      TAPS[(j0 + 1) * 128 + c] = __builtin_bit_cast(float, (h ? tap_bits[1][1] : tap_bits[0][1]) << sh) * sc;
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_s_barrier();
@@ -421,7 +482,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
         if (any_tail && tail_row) {
           for (int e = 0; e < D; ++e)
             store_elem(a.tail, ((int64_t)ri.slot * a.c_tail + a.tail_kv_off + nb + e) * w1 + (w1 - ri.rem),
-                       erow[cg + e], tail_bf16);
+                       erow[cg + e] * col_scale<TB>(a, nb + e), tail_bf16);
         }
         if (need_mask) head_pass(std::true_type{});
         else head_pass(std::false_type{});
@@ -430,7 +491,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
         for (int e = 0; e < D; ++e) {
           const int n = nb + e;
           if (n >= a.N) break;
-          const float x = erow[cg + e];
+          const float x = erow[cg + e] * col_scale<TB>(a, n);
           if (n < a.C_kv + a.H_v) {
             const int hv = n - a.C_kv;
             const float gl = -__expf(a.a_log[hv]) * softplus(x + a.dt_bias[hv]) * kLog2e;
