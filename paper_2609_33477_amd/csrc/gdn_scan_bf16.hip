@@ -1,36 +1,41 @@
 // Chunked Gated DeltaNet state accumulation, bf16 operands (gfx950).
 //
-// Same recurrence as the fp32 kernel (gdn_scan.hip).  Rows go 64 at a time
-// (a chunk) as four 16-row sub-chunks b; within a sub-chunk that starts from
-// state M0 (= S^T), with G the sub-chunk prefix of log alpha:
-//   A_ij  = beta_i e^{G_i - G_j} k_i.k_j  (i > j)        T = (I + A)^{-1}  (16x16)
-//   U     = T diag(beta) V,    W = T diag(beta e^G) K
+// Same recurrence as the fp32 kernel (gdn_scan.hip).  Rows go 32 at a time
+// (a sub-chunk); a sub-chunk that starts from state M0 (= S^T), with G the
+// sub-chunk prefix of log2 alpha, does
+//   A_ij  = beta_i 2^{G_i - G_j} k_i.k_j  (i > j)        T = (I + A)^{-1}  (32x32)
+//   U     = T diag(beta) V,    W = T diag(beta 2^G) K
 //   Delta = U - W M0
-//   M_16  = e^{G_15} M0 + K^T diag(e^{G_15 - G}) Delta
-// Only the last two lines touch the state.  The workgroup is split in two
-// roles that run one chunk apart:
-//   prep waves (4, one per sub-chunk) build T, Tu = T diag(beta) and W for
-//     chunk c+1 -- Gram block, gates, a 16x16 forward substitution, one
-//     16x16xd product;
-//   state waves (d/16, wave s owning state columns [16s, 16s+16) as d/16
-//     16x16 fp32 accumulator tiles) form U for their columns, run the four
-//     state steps of chunk c back to back in registers, and stage the rows
-//     of chunks c+2 (K) and c+1 (V) from registers loaded a step earlier.
-// So per chunk the serial path is the state steps alone; the triangular
-// solves of the next chunk overlap them.  Two barriers per chunk hand the
-// double-buffered K, W, Tu and gate vectors from one role to the other.
+//   M_32  = 2^{G_31} M0 + K^T diag(2^{G_31 - G}) Delta
+// Only the last two lines touch the state.  The workgroup runs a pipeline
+// with one barrier per sub-chunk step:
+//   4 prep waves: wave p builds everything but the state lines for the
+//     sub-chunks m = p (mod 4), spread over the 4 steps before the state
+//     needs them -- gates, Gram block and A (step m-4), a 32-step forward
+//     substitution in fp32, lane = column of T (steps m-3 and m-2), then
+//     Tu = T diag(beta) and W^T = K^T (T diag(beta 2^G))^T, which leaves W
+//     row-major (step m-1);
+//   d/32 state waves, wave s owning state columns [32s, 32s+32) as 2 d/16
+//     16x16 fp32 accumulator tiles for the whole segment: at step m they
+//     form U for their columns and run the state lines of sub-chunk m, and
+//     they stage K five sub-chunks ahead and V one ahead from registers
+//     loaded a step earlier.
+// K lives in a ring of 6 sub-chunk slots, V, W and Tu in rings of 2.
 //
-// Products use v_mfma_f32_16x16x32_bf16 (reduction over d) and
-// v_mfma_f32_16x16x16_bf16 (reduction over a sub-chunk's 16 rows).  K and V
-// stay row-major in LDS; operands whose reduction index runs down the rows of
-// an LDS matrix are read with ds_read_b64_tr_b16, which hands lane i of each
+// Every product is v_mfma_f32_16x16x32_bf16.  A 32-wide reduction over
+// sub-chunk rows uses the k-slot order {4g..4g+3, 16+4g..16+4g+3} for lane
+// group g, which is the row order of two stacked 16x16 accumulator tiles,
+// so Delta and the state feed later products straight from accumulator
+// registers; operands whose reduction index runs down the rows of an LDS
+// matrix are read with ds_read_b64_tr_b16, which hands lane i of each
 // 16-lane group rows kbase..kbase+3 of column n0 + i when lane j of the group
-// addresses row kbase + j/4, columns n0 + 4 (j%4) .. +3.  W M0 takes the state
-// straight from accumulator registers, with the MFMA k slots permuted to the
-// accumulator row order and W read in the same order.
+// addresses row kbase + j/4, columns n0 + 4 (j%4) .. +3.
 //
-// LDS (d = 128): K x2, V, W^T x2 (~18 KB each), A 5 KB, Tu x2 | Tw 8 KB,
-// vectors 2 KB: ~105 KB, one workgroup (12 waves) per CU.
+// LDS (d = 128): K ring 54 KB, V and W rings 37 KB, Tu ring 6 KB, per prep
+// wave A^T (reused for Tw^T) and gate scratch 19 KB: ~117 KB, one workgroup
+// (8 waves) per CU.  Pitches are the measured conflict-free ones: row pitch
+// = 8 mod 64 dwords for 16-byte row and transposed reads, 2 mod 8 dwords for
+// 8-byte row reads and writes.
 #include "sr_device.hpp"
 
 #include <cstddef>
@@ -39,9 +44,9 @@ namespace sr {
 namespace {
 
 constexpr int kC = 64;       // rows staged per step
-constexpr int kS = 16;       // sub-chunk rows
-constexpr int kAP = 20;      // fp32 pitch of the 16x16 A blocks
-constexpr int kTP = 20;      // bf16 pitch of the 16x16 Tu / Tw blocks
+constexpr int kS = 32;       // sub-chunk rows
+constexpr int kAP = 36;      // fp32 pitch of a sub-chunk's A (rows read as float4)
+constexpr int kTP = 48;      // bf16 pitch of the T^T blocks (transposed reads)
 constexpr int kSortMax = 256;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -66,6 +71,9 @@ __device__ __forceinline__ float4 lds_ldf4(const lchar* p) {
 }
 __device__ __forceinline__ void lds_st16(lchar* p, const uint4& v) {
   *reinterpret_cast<SR_LDS nu32x4*>(p) = __builtin_bit_cast(nu32x4, v);
+}
+__device__ __forceinline__ void lds_stf4(lchar* p, const float* v) {
+  *reinterpret_cast<SR_LDS nf32x4*>(p) = nf32x4{v[0], v[1], v[2], v[3]};
 }
 __device__ __forceinline__ void lds_st8(lchar* p, const uint2& v) {
   *reinterpret_cast<SR_LDS nu32x2*>(p) = __builtin_bit_cast(nu32x2, v);
@@ -115,32 +123,33 @@ __device__ __forceinline__ float row_last(float x, int row) {
 
 template <int D>
 struct Cfg {
-  static constexpr int NS = D / 16;                   // state waves; wave s owns columns [16s, 16s+16)
-  static constexpr int NP = 4;                        // prep waves, one per sub-chunk
-  static constexpr int THREADS = 64 * (NS + NP);
+  static constexpr int NSW = D / 32;                  // state waves; wave s owns columns [32s, 32s+32)
+  static constexpr int NP = 4;                        // prep waves
+  static constexpr int THREADS = 64 * (NSW + NP);
   static constexpr int NT = D / 16;                   // 16-row tiles along d
-  static constexpr int KP = D + 16;                   // K / V row pitch (bf16): conflict-free 16-byte and
-                                                      // transposed reads
-  static constexpr int WP = kC + 8;                   // W^T row pitch (bf16)
-  static constexpr int SZ_KV = kC * KP * 2;
-  static constexpr int SZ_W = D * WP * 2;
-  static constexpr int SZ_TU = kC * kTP * 2;          // Tu of one chunk (four 16x16 bf16 blocks)
-  static constexpr int SZ_TW = kS * kTP * 2;          // Tw of one sub-chunk (prep-wave private)
-  static constexpr int SZ_A = kS * kAP * 4;           // A of one sub-chunk (prep-wave private)
-  static constexpr int SZ_VEC = 2 * kC * 4;           // eG | eD of one chunk
-  static constexpr int SZ_SCR = 2 * kS * 4;           // G prefix | beta of one sub-chunk (prep-wave private)
-  static constexpr int OFF_K = 0;                     // two K buffers
-  static constexpr int OFF_V = OFF_K + 2 * SZ_KV;
-  static constexpr int OFF_W = OFF_V + SZ_KV;         // two W^T buffers
-  static constexpr int OFF_TU = OFF_W + 2 * SZ_W;     // two Tu buffers
-  static constexpr int OFF_TW = OFF_TU + 2 * SZ_TU;
-  static constexpr int OFF_A = OFF_TW + NP * SZ_TW;
-  static constexpr int OFF_VEC = OFF_A + NP * SZ_A;   // two vector buffers
-  static constexpr int OFF_SCR = OFF_VEC + 2 * SZ_VEC;
+  static constexpr int KP = D + 16;                   // K / V row pitch (bf16)
+  static constexpr int WP = D + 20;                   // W row pitch (bf16)
+  static constexpr int NK = 6;                        // K ring slots
+  static constexpr int SZ_KV = kS * KP * 2;           // one sub-chunk of K or V
+  static constexpr int SZ_W = kS * WP * 2;
+  static constexpr int SZ_TT = kS * kTP * 2;          // one T^T block (bf16)
+  static constexpr int SZ_A = kS * kAP * 4;           // A^T of one sub-chunk (prep-wave private; later Tw^T)
+  static constexpr int SZ_VEC = 2 * kS * 4;           // eG | eD of one sub-chunk
+  static constexpr int SZ_SCR = 2 * kS * 4;           // G prefix | beta (prep-wave private)
+  static constexpr int OFF_K = 0;
+  static constexpr int OFF_V = OFF_K + NK * SZ_KV;
+  static constexpr int OFF_W = OFF_V + 2 * SZ_KV;
+  static constexpr int OFF_TU = OFF_W + 2 * SZ_W;
+  static constexpr int OFF_A = OFF_TU + 2 * SZ_TT;
+  static constexpr int OFF_VEC = OFF_A + NP * SZ_A;
+  static constexpr int OFF_SCR = OFF_VEC + NK * SZ_VEC;
   static constexpr int LDS = OFF_SCR + NP * SZ_SCR;
   static constexpr int PPR = D / 8;                   // 16-byte pieces per row
-  static constexpr int PER_S = kC * PPR / (64 * NS);  // pieces per state thread per matrix (2)
-  static_assert(kC * PPR % (64 * NS) == 0, "staging split");
+  static constexpr int PER_S = kS * PPR / (64 * NSW); // pieces per state thread per matrix
+  static constexpr int QS = 10;                       // solve steps in the first solve segment
+  static_assert(kS * PPR % (64 * NSW) == 0, "staging split");
+  static_assert(NT % 2 == 0, "state tiles pair up along d");
+  static_assert(SZ_TT <= SZ_A, "Tw^T reuses the A^T area");
 };
 
 __device__ int rank_to_segment(const ScanArgs& a, int rank, int* shared_sel) {
@@ -163,9 +172,9 @@ __device__ int rank_to_segment(const ScanArgs& a, int rank, int* shared_sel) {
 }
 
 template <int D>
-__global__ __launch_bounds__(64 * (D / 16 + 4), 1) void gdn_scan_bf16_kernel(ScanArgs a) {
+__global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(ScanArgs a) {
   using CF = Cfg<D>;
-  constexpr int NS = CF::NS, NP = CF::NP, NT = CF::NT, KP = CF::KP, WP = CF::WP;
+  constexpr int NSW = CF::NSW, NP = CF::NP, NT = CF::NT, KP = CF::KP, WP = CF::WP, NK = CF::NK;
   __shared__ __attribute__((aligned(16))) char smem[CF::LDS];
   __shared__ int sel;
 
@@ -175,9 +184,9 @@ __global__ __launch_bounds__(64 * (D / 16 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int g = lane >> 4, li = lane & 15;
   // per-lane byte offsets; everything else is a compile-time immediate
   const int kv_row = (li * KP + 8 * g) * 2;                           // 16-byte row reads of K
-  const int t_row = (li * kTP + 4 * g) * 2;                           // 8-byte row reads of Tu / Tw
+  const int w_row = (li * WP + 4 * g) * 2;                            // 8-byte row reads / writes of W
   const int tr_kv = ((li >> 2) * KP + 4 * (li & 3) + 4 * g * KP) * 2; // transposed reads of K / V, rows 4g + ..
-  const int tr_w = ((li >> 2) * WP + 4 * (li & 3) + 4 * g * WP) * 2;  // transposed reads of W^T, rows 4g + ..
+  const int tr_t = ((li >> 2) * kTP + 4 * (li & 3) + 4 * g * kTP) * 2; // transposed reads of T^T, rows 4g + ..
 
   const int u = blockIdx.x;
   const int head = u % a.H_v;
@@ -187,7 +196,7 @@ __global__ __launch_bounds__(64 * (D / 16 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int slot = a.slot_ids ? a.slot_ids[b] : b;
   if (slot < 0) return;
   const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
-  const int nch = (int)((s1 - s0 + kC - 1) / kC);
+  const int nsc = (int)((s1 - s0 + kS - 1) / kS);     // sub-chunks
   const int hk = (head * a.H_k) / a.H_v;
 
   const char* Kplane = static_cast<const char*>(a.Kbuf) + (layer * a.k_layer_stride + (int64_t)hk * a.T * D) * 2;
@@ -201,217 +210,287 @@ __global__ __launch_bounds__(64 * (D / 16 + 4), 1) void gdn_scan_bf16_kernel(Sca
   float* st_out = *reinterpret_cast<float* const*>(kargs + offsetof(ScanArgs, state_out) + sizeof(void*) * layer);
   const size_t state_base = ((size_t)slot * a.H_v + head) * D * D;
 
-  auto kbuf = [&](int c) { return L + CF::OFF_K + (c & 1) * CF::SZ_KV; };
-  auto wbuf = [&](int c) { return L + CF::OFF_W + (c & 1) * CF::SZ_W; };
-  auto tubuf = [&](int c) { return L + CF::OFF_TU + (c & 1) * CF::SZ_TU; };
-  auto vecbuf = [&](int c) { return (SR_LDS float*)(L + CF::OFF_VEC + (c & 1) * CF::SZ_VEC); };  // eG[64] | eD[64]
-  lchar* Vr = L + CF::OFF_V;
+  auto kbuf = [&](int m) { return L + CF::OFF_K + (m % NK) * CF::SZ_KV; };
+  auto vbuf = [&](int m) { return L + CF::OFF_V + (m & 1) * CF::SZ_KV; };
+  auto wbuf = [&](int m) { return L + CF::OFF_W + (m & 1) * CF::SZ_W; };
+  auto tubuf = [&](int m) { return L + CF::OFF_TU + (m & 1) * CF::SZ_TT; };
+  auto vecbuf = [&](int m) { return (SR_LDS float*)(L + CF::OFF_VEC + (m % NK) * CF::SZ_VEC); };  // eG[32] | eD[32]
 
-  const bool prep = wid < NP;
-  // ---- prep-wave state
-  const int sb = prep ? wid : 0;                         // sub-chunk of a prep wave
-  lchar* Tw = L + CF::OFF_TW + sb * CF::SZ_TW;
-  SR_LDS float* Am = (SR_LDS float*)(L + CF::OFF_A + sb * CF::SZ_A);
-  SR_LDS float* gsc = (SR_LDS float*)(L + CF::OFF_SCR + sb * CF::SZ_SCR);   // G prefix [16] | beta [16]
-  // ---- state-wave state: tile td holds M[16 td + 4g + r][16 s + li]; the
-  // state waves also stage the K / V rows (prefetched a step ahead)
-  const int sw = prep ? 0 : wid - NP;
+  // A 32-wide reduction operand from a transposed-read matrix: rows
+  // kbase + {4g..4g+3} and kbase + 16 + {4g..4g+3} of the lane's column.
+  auto tr_pair = [&](const lchar* p, int pitch_bytes, bool negate) {
+    return join(tr4(p), tr4(p + 16 * pitch_bytes), negate);
+  };
+
+  if (wid < NP) {
+    // ================================================================ prep
+    const int p = wid;
+    SR_LDS float* At = (SR_LDS float*)(L + CF::OFF_A + p * CF::SZ_A);   // A^T, later Tw^T (private)
+    lchar* Tw = (lchar*)At;
+    SR_LDS float* gsc = (SR_LDS float*)(L + CF::OFF_SCR + p * CF::SZ_SCR);   // G prefix [32] | beta [32]
+    const int col = lane & 31;                           // column of T this lane solves
+
+    // log2 alpha and beta of sub-chunk m's 32 rows (lanes 0..31; rows past
+    // the segment end carry 0 and 0, which makes them inert)
+    auto load_gb = [&](int m, float& gv, float& bv) {
+      const int64_t t = s0 + (int64_t)m * kS + col;
+      const bool ok = lane < 32 && m < nsc && t < s1;
+      gv = ok ? Gp[t] : 0.f;
+      bv = ok ? Bp[t] : 0.f;
+    };
+
+    float x[kS];                                         // column `col` of T, carried across segments
+    // S1: prefix, gate vectors, Gram block, A^T
+    auto seg_a = [&](int m, float gv, float bv) {
+      const lchar* Kc = kbuf(m);
+      float gp = gv;
+      gp += dpp_row_shr<1>(gp);
+      gp += dpp_row_shr<2>(gp);
+      gp += dpp_row_shr<4>(gp);
+      gp += dpp_row_shr<8>(gp);
+      const float g15 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gp), 15));
+      if (lane >= 16) gp += g15;
+      const float g31 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gp), 31));
+      SR_LDS float* vec = vecbuf(m);
+      if (lane < 32) {
+        gsc[col] = gp;
+        gsc[kS + col] = bv;
+        vec[col] = exp2f(gp);                 // 2^{G_i}
+        vec[kS + col] = exp2f(g31 - gp);      // 2^{G_31 - G_i}
+      }
+      f32x4 g00 = zero4(), g10 = zero4(), g11 = zero4();
+#pragma unroll
+      for (int q = 0; q < D / 32; ++q) {
+        const bf16x8 k0 = as_bf16x8(lds_ld16(Kc + kv_row + 32 * q * 2));
+        const bf16x8 k1 = as_bf16x8(lds_ld16(Kc + kv_row + (16 * KP + 32 * q) * 2));
+        g00 = mma_k32(g00, k0, k0);
+        g10 = mma_k32(g10, k1, k0);
+        g11 = mma_k32(g11, k1, k1);
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);          // this wave's writes of gsc have landed
+      const float gj0 = gsc[li], gj1 = gsc[16 + li];
+      float a00[4], a10[4], a11[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i0 = 4 * g + r, i1 = 16 + 4 * g + r;
+        const float b0 = gsc[kS + i0], b1 = gsc[kS + i1], gi0 = gsc[i0], gi1 = gsc[i1];
+        a00[r] = (i0 > li) ? b0 * exp2f(fminf(gi0 - gj0, 0.f)) * g00[r] : 0.f;
+        a10[r] = b1 * exp2f(fminf(gi1 - gj0, 0.f)) * g10[r];
+        a11[r] = (i1 > 16 + li) ? b1 * exp2f(fminf(gi1 - gj1, 0.f)) * g11[r] : 0.f;
+      }
+      // stored transposed, At[j][i] = A_ij: one 16-byte store per block
+      lds_stf4((lchar*)(At + li * kAP + 4 * g), a00);
+      lds_stf4((lchar*)(At + li * kAP + 16 + 4 * g), a10);
+      lds_stf4((lchar*)(At + (16 + li) * kAP + 16 + 4 * g), a11);
+    };
+    // S2 / S3: T = (I + A)^{-1}, lane = column, column-oriented: once
+    // x_q = T[q][col] is final it is eliminated from every later row.  Each
+    // step needs one column of A (a row of A^T), read two steps ahead; the
+    // empty asm keeps each step's updates in place (later loads may not be
+    // hoisted above them, nor the updates sunk below).
+    auto solve = [&](auto q0_tag, auto q1_tag) {
+      constexpr int Q0 = decltype(q0_tag)::value, Q1 = decltype(q1_tag)::value;
+      float4 cb[3][kS / 4];
+      auto load_col = [&](int q, float4* dst) {
+#pragma unroll
+        for (int v = (q + 1) / 4; v < kS / 4; ++v) dst[v] = lds_ldf4((const lchar*)(At + q * kAP + 4 * v));
+      };
+      load_col(Q0, cb[Q0 % 3]);
+      if (Q0 + 1 < Q1) load_col(Q0 + 1, cb[(Q0 + 1) % 3]);
+#pragma unroll
+      for (int q = Q0; q < Q1; ++q) {
+        if (q + 2 < Q1) load_col(q + 2, cb[(q + 2) % 3]);
+        const float xq = x[q];
+        const float4* cv = cb[q % 3];
+#pragma unroll
+        for (int i = q + 1; i < kS; ++i) {
+          const float4 v = cv[i / 4];
+          const float aiq = (i & 3) == 0 ? v.x : (i & 3) == 1 ? v.y : (i & 3) == 2 ? v.z : v.w;
+          x[i] = fmaf(-aiq, xq, x[i]);
+        }
+#pragma unroll
+        for (int i = q + 1; i < kS; ++i) asm volatile("" : "+v"(x[i]));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    // S4: Tu^T and Tw^T rows (columns of T diag(beta) and T diag(beta 2^G),
+    // each rounded once; lane `col` writes row `col`), then W^T = K^T Tw^T:
+    // lane (li, g) of tile (td, bi) ends with W[16 bi + li][16 td + 4g ..],
+    // an 8-byte row-major store
+    auto seg_d = [&](int m) {
+      const float bc = gsc[kS + col];
+      const float wc = bc * exp2f(gsc[col]);
+      lchar* Tu = tubuf(m);
+      if (lane < 32) {
+#pragma unroll
+        for (int q = 0; q < kS / 8; ++q) {
+          uint4 tu, tw;
+          tu.x = pack_bf16x2(x[8 * q + 0] * bc, x[8 * q + 1] * bc);
+          tu.y = pack_bf16x2(x[8 * q + 2] * bc, x[8 * q + 3] * bc);
+          tu.z = pack_bf16x2(x[8 * q + 4] * bc, x[8 * q + 5] * bc);
+          tu.w = pack_bf16x2(x[8 * q + 6] * bc, x[8 * q + 7] * bc);
+          tw.x = pack_bf16x2(x[8 * q + 0] * wc, x[8 * q + 1] * wc);
+          tw.y = pack_bf16x2(x[8 * q + 2] * wc, x[8 * q + 3] * wc);
+          tw.z = pack_bf16x2(x[8 * q + 4] * wc, x[8 * q + 5] * wc);
+          tw.w = pack_bf16x2(x[8 * q + 6] * wc, x[8 * q + 7] * wc);
+          lds_st16(Tu + (col * kTP + 8 * q) * 2, tu);
+          lds_st16(Tw + (col * kTP + 8 * q) * 2, tw);
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      const lchar* Kc = kbuf(m);
+      lchar* Wc = wbuf(m);
+      const bf16x8 tw0 = tr_pair(Tw + tr_t, kTP * 2, false);
+      const bf16x8 tw1 = tr_pair(Tw + tr_t + 16 * 2, kTP * 2, false);
+#pragma unroll
+      for (int td = 0; td < NT; ++td) {
+        const bf16x8 kt = tr_pair(Kc + tr_kv + 16 * td * 2, KP * 2, false);
+        const f32x4 w0 = mma_k32(zero4(), kt, tw0);
+        const f32x4 w1 = mma_k32(zero4(), kt, tw1);
+        lds_st8(Wc + w_row + 16 * td * 2, make_uint2(pack_bf16x2(w0[0], w0[1]), pack_bf16x2(w0[2], w0[3])));
+        lds_st8(Wc + w_row + (16 * WP + 16 * td) * 2, make_uint2(pack_bf16x2(w1[0], w1[1]), pack_bf16x2(w1[2], w1[3])));
+      }
+    };
+
+    // after the barrier that publishes K(0): steps -4 .. nsc-1, one barrier
+    // each; this wave runs sub-chunks
+    // m = p, p + 4, ... in steps m-4 .. m-1
+    lds_barrier();                                       // K(0) is in place
+    int n = -4;
+    for (; n < p - 4; ++n) lds_barrier();
+    float gv, bv, gv_nx, bv_nx;
+    load_gb(p, gv, bv);
+    for (int m = p; m < nsc; m += 4) {
+      load_gb(m + 4, gv_nx, bv_nx);
+      seg_a(m, gv, bv);
+      lds_barrier();
+      int cl = col;
+      asm volatile("" : "+v"(cl));
+#pragma unroll
+      for (int i = 0; i < kS; ++i) x[i] = (i == cl) ? 1.f : 0.f;
+      solve(std::integral_constant<int, 0>{}, std::integral_constant<int, CF::QS>{});
+      lds_barrier();
+      solve(std::integral_constant<int, CF::QS>{}, std::integral_constant<int, kS>{});
+      lds_barrier();
+      seg_d(m);
+      lds_barrier();
+      gv = gv_nx;
+      bv = bv_nx;
+      n += 4;
+    }
+    for (; n < nsc; ++n) lds_barrier();
+    return;
+  }
+
+  // ================================================================== state
+  // tile (td, cc) holds M[16 td + 4g + r][32 sw + 16 cc + li]
+  const int sw = wid - NP;
   const int stid = tid - 64 * NP;
-  f32x4 M[NT];
+  f32x4 M[NT][2];
   uint4 pk[CF::PER_S], pv[CF::PER_S];
 
-  // rows of chunk c as 16-byte pieces (zero past the segment end)
-  auto load_rows = [&](const char* plane, int c, uint4* dst) {
-    const int64_t c0 = s0 + (int64_t)c * kC;
+  // rows of sub-chunk m as 16-byte pieces (zero past the segment end)
+  auto load_rows = [&](const char* plane, int m, uint4* dst) {
+    const int64_t c0 = s0 + (int64_t)m * kS;
 #pragma unroll
     for (int i = 0; i < CF::PER_S; ++i) {
-      const int p = stid + i * 64 * NS;
-      const int row = p / CF::PPR, cc = p % CF::PPR;
+      const int q = stid + i * 64 * NSW;
+      const int row = q / CF::PPR, cc = q % CF::PPR;
       const int64_t t = c0 + row;
-      dst[i] = (c < nch && t < s1) ? *reinterpret_cast<const uint4*>(plane + (t * D + cc * 8) * 2) : make_uint4(0, 0, 0, 0);
+      dst[i] = (m >= 0 && m < nsc && t < s1) ? *reinterpret_cast<const uint4*>(plane + (t * D + cc * 8) * 2)
+                                             : make_uint4(0, 0, 0, 0);
     }
   };
   auto store_rows = [&](lchar* buf, const uint4* src) {
 #pragma unroll
     for (int i = 0; i < CF::PER_S; ++i) {
-      const int p = stid + i * 64 * NS;
-      const int row = p / CF::PPR, cc = p % CF::PPR;
+      const int q = stid + i * 64 * NSW;
+      const int row = q / CF::PPR, cc = q % CF::PPR;
       lds_st16(buf + (row * KP + cc * 8) * 2, src[i]);
     }
   };
-  // log2 alpha and beta of sub-chunk sb's 16 rows of chunk c (lanes 0..15;
-  // rows past the segment end carry 0 and 0, which makes them inert)
-  auto load_gb = [&](int c, float& gv, float& bv) {
-    const int64_t t = s0 + (int64_t)c * kC + 16 * sb + li;
-    const bool ok = lane < 16 && c < nch && t < s1;
-    gv = ok ? Gp[t] : 0.f;
-    bv = ok ? Bp[t] : 0.f;
-  };
 
-  // prep: T, Tu, W and the gate vectors of sub-chunk sb of chunk c
-  auto prep_chunk = [&](int c, float gv, float bv) {
-    const lchar* Kc = kbuf(c);
-    // inclusive prefix of log2 alpha over the 16 rows (lanes 0..15)
-    float gp = gv;
-    gp += dpp_row_shr<1>(gp);
-    gp += dpp_row_shr<2>(gp);
-    gp += dpp_row_shr<4>(gp);
-    gp += dpp_row_shr<8>(gp);
-    const float g15 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gp), 15));
-    SR_LDS float* vec = vecbuf(c);
-    if (lane < 16) {
-      gsc[li] = gp;
-      gsc[16 + li] = bv;
-      vec[16 * sb + li] = exp2f(gp);             // 2^{G_i}
-      vec[kC + 16 * sb + li] = exp2f(g15 - gp);  // 2^{G_15 - G_i}
-    }
-    // Gram block and A = beta_i 2^{G_i - G_j} Gamma (i > j)
-    f32x4 gam = zero4();
+  // the state lines of sub-chunk m for this wave's 32 columns
+  auto state_step = [&](int m) {
+    const lchar* Kc = kbuf(m);
+    const lchar* Vc = vbuf(m);
+    const lchar* Wc = wbuf(m);
+    const lchar* Tu = tubuf(m);
+    const SR_LDS float* vec = vecbuf(m);
+    // U = Tu V for row halves bi and column tiles cc
+    f32x4 dl[2][2];
+    {
+      const bf16x8 t0 = tr_pair(Tu + tr_t, kTP * 2, false);
+      const bf16x8 t1 = tr_pair(Tu + tr_t + 16 * 2, kTP * 2, false);
 #pragma unroll
-    for (int s = 0; s < D / 32; ++s) {
-      const bf16x8 kf = as_bf16x8(lds_ld16(Kc + kv_row + (16 * sb * KP + 32 * s) * 2));
-      gam = mma_k32(gam, kf, kf);
-    }
-    __builtin_amdgcn_s_waitcnt(0xc07f);          // this wave's writes of gsc have landed
-    const float gj = gsc[li];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int i = 4 * g + r;
-      Am[i * kAP + li] = (i > li) ? gsc[16 + i] * exp2f(fminf(gsc[i] - gj, 0.f)) * gam[r] : 0.f;
-    }
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-    // T = (I + A)^{-1} by forward substitution, lane = column (every 16-lane
-    // group solves the same block; group 0 writes).  The column index goes
-    // through an empty asm so the 16 identity selects stay inside the loop
-    // instead of being hoisted into registers live across all chunks.
-    int col = li;
-    asm volatile("" : "+v"(col));
-    float x[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      if (i % 4 == 0) __builtin_amdgcn_sched_barrier(0);   // bound the hoisting of A loads
-      float t0 = (i == col) ? 1.f : 0.f, t1 = 0.f;
-#pragma unroll
-      for (int q = 0; q < (i + 3) / 4; ++q) {
-        const float4 v = lds_ldf4((const lchar*)(Am + i * kAP + 4 * q));
-        if (4 * q + 0 < i) t0 = fmaf(-v.x, x[4 * q + 0], t0);
-        if (4 * q + 1 < i) t1 = fmaf(-v.y, x[4 * q + 1], t1);
-        if (4 * q + 2 < i) t0 = fmaf(-v.z, x[4 * q + 2], t0);
-        if (4 * q + 3 < i) t1 = fmaf(-v.w, x[4 * q + 3], t1);
-      }
-      x[i] = t0 + t1;
-    }
-    // Tu = T diag(beta), Tw = T diag(beta 2^G), each rounded once
-    const float bc = gsc[16 + li];
-    const float wc = bc * exp2f(gsc[li]);
-    lchar* Tu = tubuf(c);
-    if (lane < 16) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        *reinterpret_cast<SR_LDS uint16_t*>(Tu + ((16 * sb + i) * kTP + li) * 2) = f32_to_bf16_bits(x[i] * bc);
-        *reinterpret_cast<SR_LDS uint16_t*>(Tw + (i * kTP + li) * 2) = f32_to_bf16_bits(x[i] * wc);
+      for (int cc = 0; cc < 2; ++cc) {
+        const bf16x8 vf = tr_pair(Vc + tr_kv + (32 * sw + 16 * cc) * 2, KP * 2, false);
+        dl[0][cc] = mma_k32(zero4(), t0, vf);
+        dl[1][cc] = mma_k32(zero4(), t1, vf);
       }
     }
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-    // W = Tw K of this sub-chunk, stored as W^T
-    lchar* Wt = wbuf(c);
-    const v4i16 twf = as_v4(lds_ld8(Tw + t_row));
+    // Delta = U - W M0, W rows read in the state's k order
+#pragma unroll
+    for (int q = 0; q < NT / 2; ++q) {
+      const bf16x8 m0 = acc_pair(M[2 * q][0], M[2 * q + 1][0]);
+      const bf16x8 m1 = acc_pair(M[2 * q][1], M[2 * q + 1][1]);
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+        const lchar* wr = Wc + w_row + (16 * bi * WP + 32 * q) * 2;
+        const bf16x8 wf = join(lds_ld8(wr), lds_ld8(wr + 16 * 2), true);
+        dl[bi][0] = mma_k32(dl[bi][0], wf, m0);
+        dl[bi][1] = mma_k32(dl[bi][1], wf, m1);
+      }
+    }
+    // scale the rows by 2^{G_31 - G_i}; decay the state; M += K^T Delta
+    const float4 e0 = lds_ldf4((const lchar*)(vec + kS + 4 * g));
+    const float4 e1 = lds_ldf4((const lchar*)(vec + kS + 16 + 4 * g));
+    bf16x8 dfr[2];
+#pragma unroll
+    for (int cc = 0; cc < 2; ++cc)
+      dfr[cc] = as_bf16x8(make_uint4(pack_bf16x2(dl[0][cc][0] * e0.x, dl[0][cc][1] * e0.y),
+                                     pack_bf16x2(dl[0][cc][2] * e0.z, dl[0][cc][3] * e0.w),
+                                     pack_bf16x2(dl[1][cc][0] * e1.x, dl[1][cc][1] * e1.y),
+                                     pack_bf16x2(dl[1][cc][2] * e1.z, dl[1][cc][3] * e1.w)));
+    const float decay = vec[kS - 1];
 #pragma unroll
     for (int td = 0; td < NT; ++td) {
-      const f32x4 w = mma_k16(zero4(), twf, as_v4(tr4(Kc + tr_kv + (16 * sb * KP + 16 * td) * 2)));
-      lds_st8(Wt + ((16 * td + li) * WP + 16 * sb + 4 * g) * 2,
-              make_uint2(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3])));
-    }
-  };
-
-  // state: U for this wave's columns, then the four state steps of chunk c
-  auto state_chunk = [&](int c) {
-    const lchar* Kc = kbuf(c);
-    const lchar* Tu = tubuf(c);
-    const lchar* Wt = wbuf(c);
-    const SR_LDS float* vec = vecbuf(c);
+      const bf16x8 kt = tr_pair(Kc + tr_kv + 16 * td * 2, KP * 2, false);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      // U for this sub-chunk and this wave's columns
-      f32x4 dl = mma_k16(zero4(), as_v4(lds_ld8(Tu + t_row + 16 * s * kTP * 2)),
-                         as_v4(tr4(Vr + tr_kv + (16 * s * KP + 16 * sw) * 2)));
+      for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
-      for (int p = 0; p < NT / 2; ++p)   // Delta = U - W M0, W rows read in the state's k order
-        dl = mma_k32(dl,
-                     join(tr4(Wt + tr_w + ((32 * p) * WP + 16 * s) * 2),
-                          tr4(Wt + tr_w + ((32 * p + 16) * WP + 16 * s) * 2), true),
-                     acc_pair(M[2 * p], M[2 * p + 1]));
-      const float4 ed = lds_ldf4((const lchar*)(vec + kC + 16 * s + 4 * g));
-      const v4i16 dfr = as_v4(make_uint2(pack_bf16x2(dl[0] * ed.x, dl[1] * ed.y), pack_bf16x2(dl[2] * ed.z, dl[3] * ed.w)));
-      const float decay = vec[16 * s + 15];
-#pragma unroll
-      for (int td = 0; td < NT; ++td) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) M[td][r] *= decay;
-        M[td] = mma_k16(M[td], as_v4(tr4(Kc + tr_kv + (16 * s * KP + 16 * td) * 2)), dfr);
+        for (int r = 0; r < 4; ++r) M[td][cc][r] *= decay;
+        M[td][cc] = mma_k32(M[td][cc], kt, dfr[cc]);
       }
-      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // The two roles run separate loops (wave-uniform branch) so that neither
-  // keeps the other's loop-invariant addresses live; both meet the same
-  // sequence of barriers: two in the prologue and two per chunk.
-  if (prep) {
-    float g_nx = 0.f, b_nx = 0.f, g_pf = 0.f, b_pf = 0.f;
-    if (nch > 0) {
-      load_gb(1, g_nx, b_nx);
-      load_gb(2, g_pf, b_pf);
-    }
-    lds_barrier();
-    if (nch > 0) {
-      float g0, b0;
-      load_gb(0, g0, b0);
-      prep_chunk(0, g0, b0);     // T / W of chunk 0
-    }
-    lds_barrier();
-    for (int c = 0; c < nch; ++c) {
-      if (c + 1 < nch) prep_chunk(c + 1, g_nx, b_nx);
-      lds_barrier();
-      g_nx = g_pf;
-      b_nx = b_pf;
-      load_gb(c + 3, g_pf, b_pf);
-      lds_barrier();
-    }
-    return;
-  }
-
-  // ---- state waves.  Prologue: chunks 0 and 1 resident, the state loaded
-  if (nch > 0) {
-    load_rows(Kplane, 0, pk);
-    load_rows(Vplane, 0, pv);
-    store_rows(kbuf(0), pk);
-    store_rows(Vr, pv);
-    load_rows(Kplane, 1, pk);
-    store_rows(kbuf(1), pk);
-    load_rows(Kplane, 2, pk);       // K(2) -> K buffer 0 after step 0
-    load_rows(Vplane, 1, pv);       // V(1) -> the V buffer after step 0
-  }
+  // ---- prologue: K(0) resident, K(1) and the state in registers
+  load_rows(Kplane, 0, pk);
+  store_rows(kbuf(0), pk);
+  load_rows(Kplane, 1, pk);
 #pragma unroll
-  for (int td = 0; td < NT; ++td) {
-    M[td] = zero4();
-    if (st_in) {
+  for (int td = 0; td < NT; ++td)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) M[td][r] = st_in[state_base + (size_t)(16 * td + 4 * g + r) * D + 16 * sw + li];
+    for (int cc = 0; cc < 2; ++cc) {
+      M[td][cc] = zero4();
+      if (st_in) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          M[td][cc][r] = st_in[state_base + (size_t)(16 * td + 4 * g + r) * D + 32 * sw + 16 * cc + li];
+      }
     }
-  }
-  lds_barrier();
-  lds_barrier();
 
-  // ---- pipeline: step c runs the state steps of chunk c while the prep
-  // waves prepare c+1
-  for (int c = 0; c < nch; ++c) {
-    state_chunk(c);
-    lds_barrier();
-    if (c + 2 < nch) store_rows(kbuf(c), pk);
-    if (c + 1 < nch) store_rows(Vr, pv);
-    load_rows(Kplane, c + 3, pk);
-    load_rows(Vplane, c + 2, pv);
+  lds_barrier();                    // publishes K(0) to the prep waves
+
+  // ---- steps -4 .. nsc-1: the state lines of sub-chunk n; K(n+5) and
+  // V(n+1) go to their slots from registers loaded a step earlier
+  for (int n = -4; n < nsc; ++n) {
+    if (n >= 0) state_step(n);
+    if (n + 5 < nsc) store_rows(kbuf(n + 5), pk);
+    load_rows(Kplane, n + 6, pk);
+    if (n + 1 >= 0 && n + 1 < nsc) store_rows(vbuf(n + 1), pv);
+    load_rows(Vplane, n + 2, pv);
     lds_barrier();
   }
 
@@ -419,7 +498,9 @@ __global__ __launch_bounds__(64 * (D / 16 + 4), 1) void gdn_scan_bf16_kernel(Sca
 #pragma unroll
   for (int td = 0; td < NT; ++td)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) out[(size_t)(16 * td + 4 * g + r) * D + 16 * sw + li] = M[td][r];
+    for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) out[(size_t)(16 * td + 4 * g + r) * D + 32 * sw + 16 * cc + li] = M[td][cc][r];
 }
 
 template <int D>
