@@ -316,7 +316,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     // S4: Tu^T and Tw^T rows (columns of T diag(beta) and T diag(beta 2^G),
     // each rounded once; lane `col` writes row `col`), then W^T = K^T Tw^T:
     // lane (li, g) of tile (td, bi) ends with W[16 bi + li][16 td + 4g ..],
-    // an 8-byte row-major store
+    // stored negated (the state subtracts W M0) as an 8-byte row-major store
     auto seg_d = [&](int m) {
       const float bc = gsc[kS + col];
       const float wc = bc * exp2f(gsc[col]);
@@ -347,8 +347,8 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
         const bf16x8 kt = tr_pair(Kc + tr_kv + 16 * td * 2, KP * 2, false);
         const f32x4 w0 = mma_k32(zero4(), kt, tw0);
         const f32x4 w1 = mma_k32(zero4(), kt, tw1);
-        lds_st8(Wc + w_row + 16 * td * 2, make_uint2(pack_bf16x2(w0[0], w0[1]), pack_bf16x2(w0[2], w0[3])));
-        lds_st8(Wc + w_row + (16 * WP + 16 * td) * 2, make_uint2(pack_bf16x2(w1[0], w1[1]), pack_bf16x2(w1[2], w1[3])));
+        lds_st8(Wc + w_row + 16 * td * 2, make_uint2(pack_bf16x2(-w0[0], -w0[1]), pack_bf16x2(-w0[2], -w0[3])));
+        lds_st8(Wc + w_row + (16 * WP + 16 * td) * 2, make_uint2(pack_bf16x2(-w1[0], -w1[1]), pack_bf16x2(-w1[2], -w1[3])));
       }
     };
 
@@ -410,41 +410,52 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     }
   };
 
-  // the state lines of sub-chunk m for this wave's 32 columns
+  // the state lines of sub-chunk m for this wave's 32 columns.  Every LDS
+  // read of the step is issued first, so their latencies overlap instead of
+  // each one stalling the MFMA that needs it.
   auto state_step = [&](int m) {
     const lchar* Kc = kbuf(m);
     const lchar* Vc = vbuf(m);
     const lchar* Wc = wbuf(m);
     const lchar* Tu = tubuf(m);
     const SR_LDS float* vec = vecbuf(m);
-    // U = Tu V for row halves bi and column tiles cc
-    f32x4 dl[2][2];
-    {
-      const bf16x8 t0 = tr_pair(Tu + tr_t, kTP * 2, false);
-      const bf16x8 t1 = tr_pair(Tu + tr_t + 16 * 2, kTP * 2, false);
+    const bf16x8 t0 = tr_pair(Tu + tr_t, kTP * 2, false);
+    const bf16x8 t1 = tr_pair(Tu + tr_t + 16 * 2, kTP * 2, false);
+    bf16x8 vf[2], wf[NT / 2][2], kt[NT];
 #pragma unroll
-      for (int cc = 0; cc < 2; ++cc) {
-        const bf16x8 vf = tr_pair(Vc + tr_kv + (32 * sw + 16 * cc) * 2, KP * 2, false);
-        dl[0][cc] = mma_k32(zero4(), t0, vf);
-        dl[1][cc] = mma_k32(zero4(), t1, vf);
+    for (int cc = 0; cc < 2; ++cc) vf[cc] = tr_pair(Vc + tr_kv + (32 * sw + 16 * cc) * 2, KP * 2, false);
+#pragma unroll
+    for (int q = 0; q < NT / 2; ++q)
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+        const lchar* wr = Wc + w_row + (16 * bi * WP + 32 * q) * 2;
+        wf[q][bi] = join(lds_ld8(wr), lds_ld8(wr + 16 * 2), false);
       }
+    const float4 e0 = lds_ldf4((const lchar*)(vec + kS + 4 * g));
+    const float4 e1 = lds_ldf4((const lchar*)(vec + kS + 16 + 4 * g));
+    const float decay = vec[kS - 1];
+#pragma unroll
+    for (int td = 0; td < NT; ++td) kt[td] = tr_pair(Kc + tr_kv + 16 * td * 2, KP * 2, false);
+    __builtin_amdgcn_sched_barrier(0);
+    // U = Tu V for row halves bi and column tiles cc; Delta = U + (-W) M0,
+    // W rows read in the state's k order
+    f32x4 dl[2][2];
+#pragma unroll
+    for (int cc = 0; cc < 2; ++cc) {
+      dl[0][cc] = mma_k32(zero4(), t0, vf[cc]);
+      dl[1][cc] = mma_k32(zero4(), t1, vf[cc]);
     }
-    // Delta = U - W M0, W rows read in the state's k order
 #pragma unroll
     for (int q = 0; q < NT / 2; ++q) {
       const bf16x8 m0 = acc_pair(M[2 * q][0], M[2 * q + 1][0]);
       const bf16x8 m1 = acc_pair(M[2 * q][1], M[2 * q + 1][1]);
 #pragma unroll
       for (int bi = 0; bi < 2; ++bi) {
-        const lchar* wr = Wc + w_row + (16 * bi * WP + 32 * q) * 2;
-        const bf16x8 wf = join(lds_ld8(wr), lds_ld8(wr + 16 * 2), true);
-        dl[bi][0] = mma_k32(dl[bi][0], wf, m0);
-        dl[bi][1] = mma_k32(dl[bi][1], wf, m1);
+        dl[bi][0] = mma_k32(dl[bi][0], wf[q][bi], m0);
+        dl[bi][1] = mma_k32(dl[bi][1], wf[q][bi], m1);
       }
     }
     // scale the rows by 2^{G_31 - G_i}; decay the state; M += K^T Delta
-    const float4 e0 = lds_ldf4((const lchar*)(vec + kS + 4 * g));
-    const float4 e1 = lds_ldf4((const lchar*)(vec + kS + 16 + 4 * g));
     bf16x8 dfr[2];
 #pragma unroll
     for (int cc = 0; cc < 2; ++cc)
@@ -452,17 +463,14 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
                                      pack_bf16x2(dl[0][cc][2] * e0.z, dl[0][cc][3] * e0.w),
                                      pack_bf16x2(dl[1][cc][0] * e1.x, dl[1][cc][1] * e1.y),
                                      pack_bf16x2(dl[1][cc][2] * e1.z, dl[1][cc][3] * e1.w)));
-    const float decay = vec[kS - 1];
 #pragma unroll
-    for (int td = 0; td < NT; ++td) {
-      const bf16x8 kt = tr_pair(Kc + tr_kv + 16 * td * 2, KP * 2, false);
+    for (int td = 0; td < NT; ++td)
 #pragma unroll
       for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) M[td][cc][r] *= decay;
-        M[td][cc] = mma_k32(M[td][cc], kt, dfr[cc]);
+        M[td][cc] = mma_k32(M[td][cc], kt[td], dfr[cc]);
       }
-    }
   };
 
   // ---- prologue: K(0) resident, K(1) and the state in registers
@@ -485,12 +493,13 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
 
   // ---- steps -4 .. nsc-1: the state lines of sub-chunk n; K(n+5) and
   // V(n+1) go to their slots from registers loaded a step earlier
+  // (the staging goes first so its LDS writes and loads overlap the step)
   for (int n = -4; n < nsc; ++n) {
-    if (n >= 0) state_step(n);
     if (n + 5 < nsc) store_rows(kbuf(n + 5), pk);
     load_rows(Kplane, n + 6, pk);
     if (n + 1 >= 0 && n + 1 < nsc) store_rows(vbuf(n + 1), pv);
     load_rows(Vplane, n + 2, pv);
+    if (n >= 0) state_step(n);
     lds_barrier();
   }
 
