@@ -14,8 +14,8 @@
 // LDS and only k_hat / v (bf16, head-major [H][T][d]), G and beta ([H_v][T],
 // fp32) and the tail rows are written.
 //
-// Main loop (gfx950): 4 waves, each a 128 x 128 quarter of the tile on
-// v_mfma_f32_32x32x16_bf16 with fp32 accumulators in AGPRs.  A and B stream
+// Main loop (gfx950): 8 waves (two per SIMD), each a 64 x 128 piece of the
+// tile on v_mfma_f32_32x32x16_bf16 with fp32 accumulators.  A and B stream
 // global -> LDS with global_load_lds_dwordx4 (no register staging) into LDS
 // stages of BK = 32 (5 for bf16, 6 for fp8 weights), up to five K-steps ahead
 // of the MFMAs; 16-byte chunks are XOR-swizzled inside each 64-byte row so
@@ -32,14 +32,15 @@
 //
 // Conv epilogue: M-tiles overlap by 3 rows (stride 253), so every output row's
 // w-1 predecessors are in the tile.  Each 128-column half of the accumulator
-// tile goes to LDS row-major with 16-byte writes, in 4 bands of 64 rows (one
-// per wave) that each also hold a copy of the 3 rows before them.  Every lane
-// then owns one row and walks the half's columns 4 at a time: conv over its
-// row and the 3 before it, SiLU, and for a key head the sum of squares, with
-// the activation written back in place (only this lane reads its row after
-// that) and scaled by the inverse norm on a second pass; each row's d outputs
-// leave as 16-byte stores.  The segment info and conv taps the epilogue needs
-// are loaded before the main loop.
+// tile goes to LDS row-major with 16-byte writes, in 8 bands of 32 rows (one
+// per wave) that each also hold a copy of the 3 rows before them.  Lanes l
+// and l+32 then own one row, 64 columns each, and walk them 4 at a time:
+// conv over the row and the 3 before it, SiLU, and for a key head the sum of
+// squares (the two lanes' partial sums combined), with the activation written
+// back in place (only these lanes read the row's columns after that) and
+// scaled by the inverse norm on a second pass; the outputs leave as 16-byte
+// stores.  The segment info and conv taps the epilogue needs are loaded
+// before the main loop.
 #include "sr_device.hpp"
 
 #include <type_traits>
@@ -47,17 +48,17 @@
 namespace sr {
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 32, THREADS = 256;
+constexpr int BM = 256, BN = 256, BK = 32, THREADS = 512, WAVES = THREADS / 64;
 constexpr int HALO = 3, SM = BM - HALO;           // tile row stride
 // Epilogue tile in LDS: one 128-column half of the accumulator tile,
 // row-major (pitch EROW floats: 16-byte reads by 16 consecutive rows are
-// conflict free), split into 4 bands of 64 rows (one per wave).  Each band
-// holds its rows at slots 4..67 and copies of the 3 rows before it at slots
+// conflict free), split into 8 bands of 32 rows (one per wave).  Each band
+// holds its rows at slots 4..35 and copies of the 3 rows before it at slots
 // 1..3, so a lane reads its row and the w-1 rows before it at fixed offsets
 // and may overwrite its own row without racing a neighbouring wave.
 constexpr int EROW = 132;
-constexpr int EBAND = 68;
-constexpr int E_BYTES = 4 * EBAND * EROW * 4;
+constexpr int EBAND = 36;
+constexpr int E_BYTES = WAVES * EBAND * EROW * 4;
 constexpr int TAP_BYTES = 4 * 128 * 4;              // taps [rows back][column] of one half
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -78,8 +79,8 @@ template <typename TB> struct BT;
 // B row bytes per K-step, 1 KB DMA blocks per wave and K-step, LDS stages
 // (as many as fit in 160 KB: the deeper the prefetch, the more memory latency
 // it hides)
-template <> struct BT<bf16_t> { static constexpr int ROW = 64, BLKS = 4, NS = 5; };
-template <> struct BT<fp8_t> { static constexpr int ROW = 32, BLKS = 2, NS = 6; };
+template <> struct BT<bf16_t> { static constexpr int ROW = 64, BLKS = 2, NS = 5; };
+template <> struct BT<fp8_t> { static constexpr int ROW = 32, BLKS = 1, NS = 6; };
 
 // 16 bytes per lane, global -> LDS at lds_base + 16 * lane (wave-uniform
 // base).  Inline asm: the compiler would otherwise wait for every such load
@@ -154,14 +155,14 @@ template <typename TB, int D>
 __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, int tiles_m, int tiles_n) {
   constexpr int BROW = BT<TB>::ROW, BBLK = BT<TB>::BLKS, NS = BT<TB>::NS;
   constexpr int A_BYTES = BM * 64, B_BYTES = BN * BROW, STAGE = A_BYTES + B_BYTES;
-  constexpr int LPK = 4 + BBLK;  // DMA instructions per wave per K-step
+  constexpr int LPK = 2 + BBLK;  // DMA instructions per wave per K-step
   constexpr int LDS = NS * STAGE > E_BYTES + TAP_BYTES ? NS * STAGE : E_BYTES + TAP_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem_raw[LDS];
   lchar* smem = (lchar*)smem_raw;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
-  const int wm = wid >> 1, wn = wid & 1;
+  const int wm = wid >> 1, wn = wid & 1;                       // 64-row x 128-column sub-tile
   int mt, nt;
   tile_of(blockIdx.x, tiles_m, tiles_n, mt, nt);
   const int64_t row0 = (int64_t)mt * SM - HALO;  // tile row 0 (negative for the first tile)
@@ -171,56 +172,54 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
 
   // Epilogue inputs, fetched before the first DMA so their latency hides
   // under the main loop (and no wait_vm count below has to include them):
-  // the segment info of the tile row this lane will own, and the conv taps
-  // (fp8 column scale folded in) this thread will stage for each half.
-  const int r = wid * 64 + lane;              // tile row owned by this lane
+  // the segment info of the tile row this lane will own (lanes l and l+32
+  // share a row), and the conv tap (fp8 column scale folded in) this thread
+  // stages for each half.
+  const int lr = lane & 31, ch = lane >> 5;
+  const int r = wid * 32 + lr;                // tile row owned by this lane
   const int64_t m = row0 + r;
   RowInfo ri = {0, 0, -1, 0};
   if (m >= 0 && m < T) ri = a.info[m];
   // Raw tap bits: nothing reads them before the epilogue, so no wait for
   // these loads is placed ahead of the main loop.
-  uint32_t tap_bits[2][2] = {{0u, 0u}, {0u, 0u}};
+  uint32_t tap_bits[2] = {0u, 0u};
   uint32_t tap_sc[2] = {0x3f80u, 0x3f80u};   // bf16 bits of the column scale
   {
-    const int c = tid >> 1, j0 = (tid & 1) * 2;
+    const int c = tid >> 2, j = tid & 3;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int n = n0 + h * 128 + c;
       if (n < a.C_kv) {
         if constexpr (std::is_same<TB, fp8_t>::value) tap_sc[h] = *col_scale_ptr(a, n);
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const int j = j0 + jj;
-          const int64_t i = (int64_t)n * a.w + a.w - 1 - j;
-          if (j <= a.w - 1) {
-            if (a.conv_bf16) tap_bits[h][jj] = static_cast<const uint16_t*>(a.conv_w)[i];
-            else tap_bits[h][jj] = static_cast<const uint32_t*>(a.conv_w)[i];
-          }
+        const int64_t i = (int64_t)n * a.w + a.w - 1 - j;
+        if (j <= a.w - 1) {
+          if (a.conv_bf16) tap_bits[h] = static_cast<const uint16_t*>(a.conv_w)[i];
+          else tap_bits[h] = static_cast<const uint32_t*>(a.conv_w)[i];
         }
       }
     }
   }
 
   // ------------------------------------------------------------ main loop
-  // DMA sources: wave wid fills A blocks 4 wid .. 4 wid + 3 (16 rows each)
-  const char* a_src[4];
+  // DMA sources: wave wid fills A blocks 2 wid, 2 wid + 1 (16 rows each)
+  const char* a_src[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = (wid * 4 + i) * 16 + (lane >> 2);
+  for (int i = 0; i < 2; ++i) {
+    const int row = (wid * 2 + i) * 16 + (lane >> 2);
     const int c = (lane & 3) ^ swz(row);
-    int64_t m = row0 + row;
-    m = m < 0 ? 0 : (m >= T ? T - 1 : m);   // rows outside [0, T) are never output
-    a_src[i] = static_cast<const char*>(a.A) + (m * K + c * 8) * 2;
+    int64_t mr = row0 + row;
+    mr = mr < 0 ? 0 : (mr >= T ? T - 1 : mr);   // rows outside [0, T) are never output
+    a_src[i] = static_cast<const char*>(a.A) + (mr * K + c * 8) * 2;
   }
   const char* b_src[BBLK];
 #pragma unroll
   for (int i = 0; i < BBLK; ++i) {
     int row, coff;
     if (std::is_same<TB, bf16_t>::value) {
-      row = (wid * 4 + i) * 16 + (lane >> 2);
+      row = (wid * 2 + i) * 16 + (lane >> 2);
       coff = ((lane & 3) ^ swz(row)) * 8;   // elements
     } else {
-      row = (wid * 2 + i) * 32 + (lane >> 1);
+      row = wid * 32 + (lane >> 1);
       coff = (lane & 1) * 16;
     }
     const int n = (n0 + row < a.N) ? n0 + row : a.N - 1;
@@ -233,7 +232,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   }
 
   const int fl = swz(lane & 31), hi = lane >> 5;
-  const int a_row_off = (wm * 128 + (lane & 31)) * 64;
+  const int a_row_off = (wm * 64 + (lane & 31)) * 64;
   const int a_k0 = a_row_off + ((0 + hi) ^ fl) * 16;
   const int a_k1 = a_row_off + ((2 + hi) ^ fl) * 16;
   int b_k0, b_k1;
@@ -247,30 +246,30 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     b_k1 = b_row_off + 16 + hi * 8;
   }
 
-  bf16x8 fa[2][4], fb[2][4];
-  f32x16 acc[4][4];
+  bf16x8 fa[2][2], fb[2][4];
+  f32x16 acc[2][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = zero16();
 
-  // read order A0, B0, B1, B2, B3, A1, A2, A3: the first MFMAs of a sub-step
+  // read order A0, B0, B1, B2, B3, A1: the first MFMAs of a sub-step
   // (A0 x B0..B3) need only the first five reads
   auto read_one = [&](int stage, int ks, int slot, int qq) {
-    const int q = qq == 0 ? 0 : (qq <= 4 ? qq + 3 : qq - 4);
+    const int q = qq == 0 ? 0 : (qq <= 4 ? qq + 1 : 1);   // 0,1: A fragments; 2..5: B fragments
     const lchar* sb = smem + stage * STAGE;
-    if (q < 4) {
+    if (q < 2) {
       fa[slot][q] = as_bf16x8(ld16(sb + (ks ? a_k1 : a_k0) + q * 32 * 64));
     } else if (std::is_same<TB, bf16_t>::value) {
-      fb[slot][q - 4] = as_bf16x8(ld16(sb + (ks ? b_k1 : b_k0) + (q - 4) * 32 * 64));
+      fb[slot][q - 2] = as_bf16x8(ld16(sb + (ks ? b_k1 : b_k0) + (q - 2) * 32 * 64));
     } else {
-      const uint2 v = ld8(sb + (ks ? b_k1 : b_k0) + (q - 4) * 32 * 32);
+      const uint2 v = ld8(sb + (ks ? b_k1 : b_k0) + (q - 2) * 32 * 32);
       uint4 o;
       o.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, false));
       o.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, true));
       o.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, false));
       o.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, true));
-      fb[slot][q - 4] = as_bf16x8(o);
+      fb[slot][q - 2] = as_bf16x8(o);
     }
   };
   // Weights go in as the MFMA's first operand, so acc[i][j] is the
@@ -282,9 +281,9 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   };
   auto dma_one = [&](int kt, int stage, int q) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem + stage * STAGE;
-    if (q < 4) dma16(a_src[q] + (int64_t)kt * BK * 2, lds0 + (wid * 4 + q) * 1024);
-    else if (q - 4 < BBLK)
-      dma16(b_src[q - 4] + (int64_t)kt * BK * Elem<TB>::bytes, lds0 + A_BYTES + (wid * BBLK + q - 4) * 1024);
+    if (q < 2) dma16(a_src[q] + (int64_t)kt * BK * 2, lds0 + (wid * 2 + q) * 1024);
+    else if (q - 2 < BBLK)
+      dma16(b_src[q - 2] + (int64_t)kt * BK * Elem<TB>::bytes, lds0 + A_BYTES + (wid * BBLK + q - 2) * 1024);
   };
 
   // The main loop, specialised on the number NJ of 32-column B fragments
@@ -298,25 +297,25 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
-      for (int q = 0; q < 8; ++q) dma_one(s < KT ? s : KT - 1, s, q);
+      for (int q = 0; q < LPK; ++q) dma_one(s < KT ? s : KT - 1, s, q);
     wait_vm<(NS - 1) * LPK>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0xc07f);   // no scalar loads in flight at loop entry
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) if (read_used(q)) read_one(0, 0, 0, q);
+    for (int q = 0; q < 6; ++q) if (read_used(q)) read_one(0, 0, 0, q);
 
     int st = 0;                              // stage of K-step kt
     for (int kt = 0; kt < KT; ++kt) {
       const int st1 = st + 1 == NS ? 0 : st + 1;
       const int kn = kt + NS < KT ? kt + NS : KT - 1;
-      // MFMAs 0-15 (first k16, slot 0) with the second k16's fragments into
-      // slot 1 over the first 8
+      // MFMAs 0-7 (first k16, slot 0) with the second k16's fragments into
+      // slot 1 over the first 6
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
+      for (int q = 0; q < 8; ++q) {
         if ((q & 3) < NJ) mma_one(0, q);
-        if (q < 8 && read_used(q)) read_one(st, 1, 1, q);
+        if (q < 6 && read_used(q)) read_one(st, 1, 1, q);
         __builtin_amdgcn_sched_barrier(0);
       }
       // Hand-over: this wave's reads of stage st are complete and its loads of
@@ -326,15 +325,15 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
       __builtin_amdgcn_s_waitcnt(0xc07f);
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      // MFMAs 16-31 (slot 1): the next K-step's first fragments into slot 0
-      // over the first 8, one refill load every other MFMA (K-step kt+NS,
+      // MFMAs 8-15 (slot 1): the next K-step's first fragments into slot 0
+      // over the first 6, one refill load every other MFMA (K-step kt+NS,
       // clamped: the surplus refills of the last steps land in stages nobody
       // reads again)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
+      for (int q = 0; q < 8; ++q) {
         if ((q & 3) < NJ) mma_one(1, q);
-        if (q < 8 && read_used(q)) read_one(st1, 0, 0, q);
-        if ((q & 1) == 0) dma_one(kn, st, q >> 1);
+        if (q < 6 && read_used(q)) read_one(st1, 0, 0, q);
+        if ((q & 1) == 0 && (q >> 1) < LPK) dma_one(kn, st, q >> 1);
         __builtin_amdgcn_sched_barrier(0);
       }
       st = st1;
@@ -351,9 +350,13 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   __builtin_amdgcn_sched_barrier(0);
 
   // ------------------------------------------------------------ epilogue
+  // Lanes l and l+32 own tile row 32 wid + l%32; lane half ch handles
+  // columns [64 ch, 64 ch + 64) of each 128-column half.
+  constexpr int CW = D < 64 ? D : 64;          // columns of one head a lane handles
+  constexpr int HPL = 64 / CW;                 // heads (or head halves) per lane
   lfloat* E = (lfloat*)smem_raw;
   lfloat* TAPS = (lfloat*)(smem_raw + E_BYTES);
-  lfloat* erow = E + (wid * EBAND + 4 + lane) * EROW;   // slot of row r
+  lfloat* erow = E + (wid * EBAND + 4 + lr) * EROW;   // slot of row r
   const bool out = r >= HALO && m < T;        // m >= 0 holds for r >= HALO
   const bool need_mask = __builtin_amdgcn_ballot_w64(out && ri.pos < HALO) != 0;
   const int w1 = a.w - 1;
@@ -371,19 +374,19 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     if (wn == h) {
       // 16-byte row-major writes (4 consecutive columns per lane); 16 rows
       // 132 floats apart cover all 64 banks once
-      const int lr = lane & 31, c4 = 4 * (lane >> 5);
+      const int c4 = 4 * (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int band = wm * 2 + (i >> 1), rb = (i & 1) * 32 + lr;
-        lfloat* dst = E + (band * EBAND + 4 + rb) * EROW + c4;
+      for (int i = 0; i < 2; ++i) {
+        const int band = wm * 2 + i;
+        lfloat* dst = E + (band * EBAND + 4 + lr) * EROW + c4;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q)
             st_f4(dst + j * 32 + 8 * q, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
         // the last 3 rows of a band are also the next band's halo
-        if ((i & 1) && band < 3 && lr >= 61 - 32) {
-          lfloat* hdst = E + ((band + 1) * EBAND + 1 + (rb - 61)) * EROW + c4;
+        if (band < WAVES - 1 && lr >= 29) {
+          lfloat* hdst = E + ((band + 1) * EBAND + 1 + (lr - 29)) * EROW + c4;
 #pragma unroll
           for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -395,21 +398,21 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     {
       // conv taps of this half's k | v columns: TAPS[j][c] multiplies row t-j
       // (an fp8 column's scale is folded in: the conv is linear per column)
-      const int c = tid >> 1, j0 = (tid & 1) * 2;
+      const int c = tid >> 2, j = tid & 3;
       const float sc = bf16_bits_to_f32((uint16_t)(h ? tap_sc[1] : tap_sc[0]));
       const int sh = a.conv_bf16 ? 16 : 0;
-      TAPS[j0 * 128 + c] = __builtin_bit_cast(float, (h ? tap_bits[1][0] : tap_bits[0][0]) << sh) * sc;
-      TAPS[(j0 + 1) * 128 + c] = __builtin_bit_cast(float, (h ? tap_bits[1][1] : tap_bits[0][1]) << sh) * sc;
+      TAPS[j * 128 + c] = __builtin_bit_cast(float, (h ? tap_bits[1] : tap_bits[0]) << sh) * sc;
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_s_barrier();
 
-    for (int g = 0; g < 128 / D; ++g) {
-      const int nb = nh0 + g * D;     // first projection column of this head group
-      if (nb >= a.N) break;
-      const int cg = g * D;           // column inside the half
+    for (int hl = 0; hl < HPL; ++hl) {
+      const int c0 = 64 * ch + hl * CW;       // first column of this lane's piece, in the half
+      const int e0 = c0 % D;                  // its offset inside the head
+      const int nb = nh0 + c0 - e0;           // first projection column of the head
+      if (nb >= a.N) continue;
       if (nb < a.C_kv) {
-        // ---- one k or v head: conv, SiLU, (key) L2 norm.  Columns go 4 at a
+        // ---- k or v head: conv, SiLU, (key) L2 norm.  Columns go 4 at a
         // time (16-byte reads of this row and the 3 before it).
         const bool is_k = nb < a.C_k;
         const int hh = is_k ? nb / D : (nb - a.C_k) / D;
@@ -437,61 +440,53 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
           }
           return y;
         };
-        char* dst = static_cast<char*>(is_k ? a.Kbuf : a.Vbuf) + (((int64_t)hh * T + (out ? m : 0)) * D) * 2;
+        char* dst = static_cast<char*>(is_k ? a.Kbuf : a.Vbuf) + (((int64_t)hh * T + (out ? m : 0)) * D + e0) * 2;
         auto head_pass = [&](auto mask_tag) {
-          if (is_k) {
-            // pass 1: y and its sum of squares; y replaces x in this row's
-            // slot (rows after it have read x already: same wave, earlier
-            // instruction; the next band reads its own halo copy)
-            float ss0 = 0.f, ss1 = 0.f;
-            __builtin_amdgcn_s_waitcnt(0xc07f);
+          // pass 1: y and (keys) its sum of squares; y replaces x in this
+          // row's slot (rows after it have read x already: same wave,
+          // earlier instruction; the next band reads its own halo copy)
+          float ss0 = 0.f, ss1 = 0.f;
+          __builtin_amdgcn_s_waitcnt(0xc07f);
 #pragma unroll 4
-            for (int c = cg; c < cg + D; c += 4) {
-              const nf32x4 y = conv4(c, mask_tag);
-              ss0 = fmaf(y[0], y[0], fmaf(y[1], y[1], ss0));
-              ss1 = fmaf(y[2], y[2], fmaf(y[3], y[3], ss1));
-              *reinterpret_cast<__attribute__((address_space(3))) nf32x4*>(erow + c) = y;
-            }
-            const float inv = 1.f / sqrtf(ss0 + ss1 + a.eps);
+          for (int c = c0; c < c0 + CW; c += 4) {
+            const nf32x4 y = conv4(c, mask_tag);
+            ss0 = fmaf(y[0], y[0], fmaf(y[1], y[1], ss0));
+            ss1 = fmaf(y[2], y[2], fmaf(y[3], y[3], ss1));
+            *reinterpret_cast<__attribute__((address_space(3))) nf32x4*>(erow + c) = y;
+          }
+          float ss = ss0 + ss1;
+          if constexpr (D > 64) {
+            // the other 64 columns of the head are in lane l ^ 32
+            ss += __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __builtin_bit_cast(int, ss)));
+          }
+          const float inv = is_k ? 1.f / sqrtf(ss + a.eps) : 1.f;
 #pragma unroll 4
-            for (int q = 0; q < D / 8; ++q) {
-              const nf32x4 y0 = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow + cg + 8 * q);
-              const nf32x4 y1 = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow + cg + 8 * q + 4);
-              uint4 o;
-              o.x = pack_bf16x2(y0[0] * inv, y0[1] * inv);
-              o.y = pack_bf16x2(y0[2] * inv, y0[3] * inv);
-              o.z = pack_bf16x2(y1[0] * inv, y1[1] * inv);
-              o.w = pack_bf16x2(y1[2] * inv, y1[3] * inv);
-              if (out) *reinterpret_cast<uint4*>(dst + q * 16) = o;
-            }
-          } else {
-#pragma unroll 2
-            for (int q = 0; q < D / 8; ++q) {
-              const nf32x4 y0 = conv4(cg + 8 * q, mask_tag), y1 = conv4(cg + 8 * q + 4, mask_tag);
-              uint4 o;
-              o.x = pack_bf16x2(y0[0], y0[1]);
-              o.y = pack_bf16x2(y0[2], y0[3]);
-              o.z = pack_bf16x2(y1[0], y1[1]);
-              o.w = pack_bf16x2(y1[2], y1[3]);
-              if (out) *reinterpret_cast<uint4*>(dst + q * 16) = o;
-            }
+          for (int q = 0; q < CW / 8; ++q) {
+            const nf32x4 y0 = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow + c0 + 8 * q);
+            const nf32x4 y1 = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow + c0 + 8 * q + 4);
+            uint4 o;
+            o.x = pack_bf16x2(y0[0] * inv, y0[1] * inv);
+            o.y = pack_bf16x2(y0[2] * inv, y0[3] * inv);
+            o.z = pack_bf16x2(y1[0] * inv, y1[1] * inv);
+            o.w = pack_bf16x2(y1[2] * inv, y1[3] * inv);
+            if (out) *reinterpret_cast<uint4*>(dst + q * 16) = o;
           }
         };
         // the raw projection of the segment's last w-1 rows is the conv state
-        // (before a key head's pass overwrites the row)
+        // (before the pass overwrites the row)
         if (any_tail && tail_row) {
-          for (int e = 0; e < D; ++e)
-            store_elem(a.tail, ((int64_t)ri.slot * a.c_tail + a.tail_kv_off + nb + e) * w1 + (w1 - ri.rem),
-                       erow[cg + e] * col_scale<TB>(a, nb + e), tail_bf16);
+          for (int e = 0; e < CW; ++e)
+            store_elem(a.tail, ((int64_t)ri.slot * a.c_tail + a.tail_kv_off + nb + e0 + e) * w1 + (w1 - ri.rem),
+                       erow[c0 + e] * col_scale<TB>(a, nb + e0 + e), tail_bf16);
         }
         if (need_mask) head_pass(std::true_type{});
         else head_pass(std::false_type{});
       } else {
         // ---- gate columns: G = log2 alpha from a, beta from b (no conv)
-        for (int e = 0; e < D; ++e) {
-          const int n = nb + e;
+        for (int e = 0; e < CW; ++e) {
+          const int n = nb + e0 + e;
           if (n >= a.N) break;
-          const float x = erow[cg + e] * col_scale<TB>(a, n);
+          const float x = erow[c0 + e] * col_scale<TB>(a, n);
           if (n < a.C_kv + a.H_v) {
             const int hv = n - a.C_kv;
             const float gl = -__expf(a.a_log[hv]) * softplus(x + a.dt_bias[hv]) * kLog2e;
