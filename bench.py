@@ -9,7 +9,7 @@ d_k=d_v=128, bf16 (the Qwen3.5-4B linear-layer shape), seeded synthetic data.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload varlen16]
+    python bench.py [--gpus 1] [--steps 100] [--warmup 50] [--workload varlen16]
     python bench.py --copy-probe      # plain copy of known size, for HBM counter scaling
 
 `roofline.traffic` is the dominant kernel's measured HBM bytes per launch,
@@ -144,8 +144,10 @@ def cpu_baseline(wl, budget_s=15.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    # the clock needs ~50 steps (~80 ms of this load) to settle; the default
+    # warmup covers that so the timed steps measure the steady state
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="varlen16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
