@@ -140,7 +140,7 @@ struct Cfg {
   static constexpr int OFF_V = OFF_K + NK * SZ_KV;
   static constexpr int OFF_W = OFF_V + 2 * SZ_KV;
   static constexpr int OFF_TU = OFF_W + 2 * SZ_W;
-  static constexpr int OFF_A = OFF_TU + 2 * SZ_TT;
+  static constexpr int OFF_A = OFF_TU + 4 * SZ_TT;     // two (Tu_hi^T | Tu_lo^T) slots
   static constexpr int OFF_VEC = OFF_A + NP * SZ_A;
   static constexpr int OFF_SCR = OFF_VEC + NK * SZ_VEC;
   static constexpr int LDS = OFF_SCR + NP * SZ_SCR;
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   auto kbuf = [&](int m) { return L + CF::OFF_K + (m % NK) * CF::SZ_KV; };
   auto vbuf = [&](int m) { return L + CF::OFF_V + (m & 1) * CF::SZ_KV; };
   auto wbuf = [&](int m) { return L + CF::OFF_W + (m & 1) * CF::SZ_W; };
-  auto tubuf = [&](int m) { return L + CF::OFF_TU + (m & 1) * CF::SZ_TT; };
+  auto tubuf = [&](int m) { return L + CF::OFF_TU + (m & 1) * 2 * CF::SZ_TT; };   // Tu_hi^T, then Tu_lo^T
   auto vecbuf = [&](int m) { return (SR_LDS float*)(L + CF::OFF_VEC + (m % NK) * CF::SZ_VEC); };  // eG[32] | eD[32]
 
   // A 32-wide reduction operand from a transposed-read matrix: rows
@@ -324,16 +324,22 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       if (lane < 32) {
 #pragma unroll
         for (int q = 0; q < kS / 8; ++q) {
-          uint4 tu, tw;
-          tu.x = pack_bf16x2(x[8 * q + 0] * bc, x[8 * q + 1] * bc);
-          tu.y = pack_bf16x2(x[8 * q + 2] * bc, x[8 * q + 3] * bc);
-          tu.z = pack_bf16x2(x[8 * q + 4] * bc, x[8 * q + 5] * bc);
-          tu.w = pack_bf16x2(x[8 * q + 6] * bc, x[8 * q + 7] * bc);
+          // Tu in two bf16 parts (hi + lo): U = Tu V is the state's only
+          // product whose rounding does not average over the segment
+          uint32_t th[4], tl[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float u0 = x[8 * q + 2 * e] * bc, u1 = x[8 * q + 2 * e + 1] * bc;
+            th[e] = pack_bf16x2(u0, u1);
+            tl[e] = pack_bf16x2(u0 - bf16_bits_to_f32((uint16_t)th[e]), u1 - bf16_bits_to_f32((uint16_t)(th[e] >> 16)));
+          }
+          uint4 tw;
           tw.x = pack_bf16x2(x[8 * q + 0] * wc, x[8 * q + 1] * wc);
           tw.y = pack_bf16x2(x[8 * q + 2] * wc, x[8 * q + 3] * wc);
           tw.z = pack_bf16x2(x[8 * q + 4] * wc, x[8 * q + 5] * wc);
           tw.w = pack_bf16x2(x[8 * q + 6] * wc, x[8 * q + 7] * wc);
-          lds_st16(Tu + (col * kTP + 8 * q) * 2, tu);
+          lds_st16(Tu + (col * kTP + 8 * q) * 2, make_uint4(th[0], th[1], th[2], th[3]));
+          lds_st16(Tu + CF::SZ_TT + (col * kTP + 8 * q) * 2, make_uint4(tl[0], tl[1], tl[2], tl[3]));
           lds_st16(Tw + (col * kTP + 8 * q) * 2, tw);
         }
       }
@@ -421,6 +427,8 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     const SR_LDS float* vec = vecbuf(m);
     const bf16x8 t0 = tr_pair(Tu + tr_t, kTP * 2, false);
     const bf16x8 t1 = tr_pair(Tu + tr_t + 16 * 2, kTP * 2, false);
+    const bf16x8 t0l = tr_pair(Tu + CF::SZ_TT + tr_t, kTP * 2, false);
+    const bf16x8 t1l = tr_pair(Tu + CF::SZ_TT + tr_t + 16 * 2, kTP * 2, false);
     bf16x8 vf[2], wf[NT / 2][2], kt[NT];
 #pragma unroll
     for (int cc = 0; cc < 2; ++cc) vf[cc] = tr_pair(Vc + tr_kv + (32 * sw + 16 * cc) * 2, KP * 2, false);
@@ -442,8 +450,8 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     f32x4 dl[2][2];
 #pragma unroll
     for (int cc = 0; cc < 2; ++cc) {
-      dl[0][cc] = mma_k32(zero4(), t0, vf[cc]);
-      dl[1][cc] = mma_k32(zero4(), t1, vf[cc]);
+      dl[0][cc] = mma_k32(mma_k32(zero4(), t0l, vf[cc]), t0, vf[cc]);
+      dl[1][cc] = mma_k32(mma_k32(zero4(), t1l, vf[cc]), t1, vf[cc]);
     }
 #pragma unroll
     for (int q = 0; q < NT / 2; ++q) {

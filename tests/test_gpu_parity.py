@@ -157,3 +157,47 @@ def test_hip_graph_capture_replays():
         torch.cuda.synchronize()
         assert torch.equal(dev.layers[0].state_out, eager)
         assert torch.equal(dev.layers[0].tail_out, eager_tail)
+
+
+def test_fp32_conv_weights_and_tail_with_bf16_anchors():
+    """The fused projection with fp32 conv weights and an fp32 conv tail (the
+    taps and the tail are the dtype-dependent parts of its epilogue)."""
+    shape = W.Shape(256, 2, 4, 128, 128, conv_dtype=W.F32, tail_dtype=W.F32)
+    wl = W.make_workload("convf32", shape, [70, 5, 131], seed=81)
+    log(f"fp32 conv/tail: T={wl.t_total}")
+    dev = upload(wl)
+    run(dev)
+    check_pairs(dev, _live_pairs(wl), TOL_BF16)
+
+
+def test_no_decay_keeps_the_initial_state():
+    """alpha = 1 to fp32 precision (A_log = -40): nothing may decay the
+    carried state, across many 32-row steps and with a nonzero state_in."""
+    shape = W.Shape(256, 2, 2, 64, 64)
+    wl = W.make_workload("nodecay", shape, [300, 45], seed=91)
+    wl.layers[0].a_log[:] = -40.0
+    r = np.random.default_rng(1)
+    S0 = r.standard_normal((2, 2, 64, 64)).astype(np.float32)
+    dev = upload(wl, state_in=[S0])
+    run(dev)
+    cu = wl.cu_seqlens
+    L = wl.layers[0]
+    for b in range(2):
+        ref, _ = oracle.replay_segment(shape, L, L.anchors[cu[b]:cu[b + 1]], S0=S0[b].astype(np.float64))
+        got = dev.layers[0].state_out[b].cpu().numpy()
+        err = rel_frob(got, ref)
+        log(f"no decay seg {b}: state rel err {err:.3e}")
+        assert err <= TOL_BF16
+
+
+def test_more_segments_than_the_device_sort():
+    """Over 256 segments the scan takes work units in segment order instead
+    of sorting them longest-first; results must not depend on that."""
+    shape = W.Shape(128, 1, 2, 32, 32)
+    seg = [int(x) for x in np.random.default_rng(5).integers(0, 40, size=300)]
+    wl = W.make_workload("manyseg", shape, seg, seed=95)
+    log(f"{len(seg)} segments, T={wl.t_total}")
+    dev = upload(wl)
+    run(dev)
+    live = [p for p in _live_pairs(wl)]
+    check_pairs(dev, live[::17] + live[-3:], TOL_BF16)
