@@ -11,7 +11,7 @@
 //   G      = log2 alpha = -exp(A_log) softplus(a + dt_bias) log2(e)
 //   beta   = sigmoid(b)
 // The projection never reaches HBM: each 256 x 256 output tile is finished in
-// LDS and only k_hat / v (bf16, head-major [H][T][d]), G and beta ([H_v][T],
+// registers and only k_hat / v (bf16, head-major [H][T][d]), G and beta ([H_v][T],
 // fp32) and the tail rows are written.
 //
 // Main loop (gfx950): 8 waves (two per SIMD), each a 64 x 128 piece of the
@@ -23,44 +23,43 @@
 // fp8 (E4M3) weights are staged as bytes and converted to bf16 after the
 // fragment read (exact); the per-channel scale is folded into the conv taps
 // (the conv is linear per column) and applied to the gate and tail values.
-// Weights are the MFMA's first operand, so each lane's accumulators hold 4
-// consecutive columns of one output row.
+// Anchors are the MFMA's first operand and their rows are fed in the order
+// that leaves each lane's accumulators holding 32 consecutive rows of one
+// column (tok_row).
 // Tiles are dealt in contiguous runs per XCD and walked in groups of 8
 // M-tiles so concurrently running tiles share A and B panels in L2.  In a
 // narrow last N-tile (the 2 H_v gate columns) waves skip the MFMAs and
 // fragment reads of columns past N.
 //
-// Conv epilogue: M-tiles overlap by 3 rows (stride 253), so every output row's
-// w-1 predecessors are in the tile.  Each 128-column half of the accumulator
-// tile goes to LDS row-major with 16-byte writes, in 8 bands of 32 rows (one
-// per wave) that each also hold a copy of the 3 rows before them.  Lanes l
-// and l+32 then own one row, 64 columns each, and walk them 4 at a time:
-// conv over the row and the 3 before it, SiLU, and for a key head the sum of
-// squares (the two lanes' partial sums combined), with the activation written
-// back in place (only these lanes read the row's columns after that) and
-// scaled by the inverse norm on a second pass; the outputs leave as 16-byte
-// stores.  The segment info and conv taps the epilogue needs are loaded
-// before the main loop.
+// Conv epilogue, in registers: M-tiles overlap by 3 rows (stride 253), so
+// every output row's w-1 predecessors are in the tile.  Lane l of wave w
+// holds rows 64 (w / 2) + 32 (l / 32) + 0..31 of 4 columns; the conv runs
+// down those registers (the 3 rows above the lane's first come from the
+// lane before it through a small LDS exchange), then SiLU, in place.  A
+// key's sum of squares over its head's columns is summed over the lane's
+// blocks and then across the 32 lanes of the half-wave by a DPP
+// reduce-scatter; the inverse norms go back to the lanes through the LDS.
+// Outputs leave as bf16 pairs (two rows per pack).  Rows near a segment
+// start, a segment end (the conv tail) or the tile edge take masked
+// variants decided per row for the whole wave.  The segment info and conv
+// taps the epilogue needs are loaded before the main loop.
 #include "sr_device.hpp"
 
 #include <type_traits>
+#include <utility>
 
 namespace sr {
 namespace {
 
 constexpr int BM = 256, BN = 256, BK = 32, THREADS = 512, WAVES = THREADS / 64;
 constexpr int HALO = 3, SM = BM - HALO;           // tile row stride
-// Epilogue tile in LDS: one 128-column half of the accumulator tile,
-// row-major (pitch EROW floats: 16-byte reads by 16 consecutive rows are
-// conflict free), split into 8 bands of 32 rows (one per wave).  Each band
-// holds its rows at slots 4..35 and copies of the 3 rows before it at slots
-// 1..3, so a lane reads its row and the w-1 rows before it at fixed offsets
-// and may overwrite its own row without racing a neighbouring wave.
-constexpr int EROW = 132;
-constexpr int EBAND = 36;
-constexpr int E_BYTES = WAVES * EBAND * EROW * 4;
-constexpr int TAP_BYTES = 4 * 128 * 4;              // taps [rows back][column] of one half
+// Epilogue exchange area (in the last main-loop stage): the last 3 rows of
+// each lane's 4 columns, and the inverse key norms of each half-wave's rows.
+constexpr int XB_BYTES = WAVES * 64 * 12 * 4;
+constexpr int INV_BYTES = WAVES * 2 * 4 * 32 * 4;
+constexpr int EPI_BYTES = XB_BYTES + INV_BYTES;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
 
 typedef __attribute__((address_space(3))) char lchar;
 typedef __attribute__((address_space(3))) float lfloat;
@@ -98,11 +97,63 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// 16-byte chunk swizzle inside a 64-byte LDS row.  A fragment read has lanes
-// 0-31 on 32 consecutive rows (lanes 32-63 on the next chunk); with this XOR
-// every ds_read_b128 is conflict free (measured: 4 LDS cycles per read, the
-// 256 B/clk peak), where rows 4 apart must land in different chunks.
-__device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
+// 16-byte chunk swizzles inside a 64-byte LDS row.  A fragment read is
+// serviced 16 lanes at a time; rows r and r + 4 share a bank quarter, so the
+// 4 rows of each quarter a 16-lane group reads must sit in distinct chunks
+// (measured: 4 LDS cycles per ds_read_b128, the 256 B/clk peak).  Weight
+// fragments read 16 consecutive rows; anchor fragments read rows in the
+// order of tok_row, whose bank-quarter mates differ in bits 2 and 5.
+__device__ __forceinline__ int swz_b(int r) { return (r >> 2) & 3; }
+__device__ __forceinline__ int swz_a(int r) { return ((r >> 2) & 1) | ((r >> 4) & 2); }
+
+// Anchor row (within a wave's 64-row band, block 0; block 1 adds 16) fed to
+// MFMA row m.  The 32x32 accumulator puts MFMA row 8 (r / 4) + 4 (l / 32) +
+// r % 4 in register r of lane l, so with this order lane l holds rows
+// 32 (l / 32) + r: 32 consecutive rows per lane over the two blocks, which
+// lets the conv run down a lane's own registers.
+__device__ __forceinline__ int tok_row(int m) { return 32 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3); }
+
+// One step of a reduce-scatter over the 32 lanes of a half-wave: lanes whose
+// bit BIT is b keep half b of the N values and add the partner's copy of it
+// (partner: a lane with bit BIT flipped and bits below it equal; DPP control
+// CTRL, or ds_swizzle xor 16 when CTRL < 0).
+template <int N, int BIT, int CTRL>
+__device__ __forceinline__ void bfly_step(float* s, int lc) {
+  const bool b = (lc >> BIT) & 1;
+#pragma unroll
+  for (int i = 0; i < N / 2; ++i) {
+    const float lo = s[i], hi = s[i + N / 2];
+    const float send = b ? lo : hi, keep = b ? hi : lo;
+    int r;
+    if constexpr (CTRL < 0) r = __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, send), 0x401F);
+    else r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, send), CTRL, 0xF, 0xF, false);
+    s[i] = keep + __builtin_bit_cast(float, r);
+    if (i % 4 == 3) __builtin_amdgcn_sched_barrier(0);   // bounds the scheduler's interleaving
+  }
+}
+
+// OR / AND of a 32-bit value over the 64 lanes (the result is wave-uniform)
+template <bool OR>
+__device__ __forceinline__ uint32_t wave_reduce(uint32_t v) {
+  auto op = [](uint32_t x, int y) { return OR ? x | (uint32_t)y : x & (uint32_t)y; };
+  v = op(v, __builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false));    // lane ^ 1
+  v = op(v, __builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false));    // lane ^ 2
+  v = op(v, __builtin_amdgcn_mov_dpp((int)v, 0x124, 0xF, 0xF, false));   // quad g -/+ 1
+  v = op(v, __builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false));   // quads g -/+ 2, 3
+  v = op(v, __builtin_amdgcn_ds_swizzle((int)v, 0x401F));                // lane ^ 16
+  return op((uint32_t)__builtin_amdgcn_readlane((int)v, 0), __builtin_amdgcn_readlane((int)v, 32));
+}
+
+// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time
+// (register arrays indexed by i stay in registers)
+template <int N, typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl<N>(f, std::make_integer_sequence<int, N>{});
+}
 
 // hardware block id -> (m tile, n tile): contiguous runs per XCD (blocks are
 // dealt round-robin to the 8 XCDs), then groups of 8 m-tiles walked n-major
@@ -156,13 +207,15 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   constexpr int BROW = BT<TB>::ROW, BBLK = BT<TB>::BLKS, NS = BT<TB>::NS;
   constexpr int A_BYTES = BM * 64, B_BYTES = BN * BROW, STAGE = A_BYTES + B_BYTES;
   constexpr int LPK = 2 + BBLK;  // DMA instructions per wave per K-step
-  constexpr int LDS = NS * STAGE > E_BYTES + TAP_BYTES ? NS * STAGE : E_BYTES + TAP_BYTES;
+  constexpr int EPI_OFF = (NS - 1) * STAGE;   // epilogue exchange area: the last stage
+  constexpr int LDS = NS * STAGE > EPI_OFF + EPI_BYTES ? NS * STAGE : EPI_OFF + EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem_raw[LDS];
   lchar* smem = (lchar*)smem_raw;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int wm = wid >> 1, wn = wid & 1;                       // 64-row x 128-column sub-tile
+  const int hf = lane >> 5, lc = lane & 31;
   int mt, nt;
   tile_of(blockIdx.x, tiles_m, tiles_n, mt, nt);
   const int64_t row0 = (int64_t)mt * SM - HALO;  // tile row 0 (negative for the first tile)
@@ -170,31 +223,37 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   const int K = a.K;
   const int64_t T = a.T;
 
-  // Epilogue inputs, fetched before the first DMA so their latency hides
-  // under the main loop (and no wait_vm count below has to include them):
-  // the segment info of the tile row this lane will own (lanes l and l+32
-  // share a row), and the conv tap (fp8 column scale folded in) this thread
-  // stages for each half.
-  const int lr = lane & 31, ch = lane >> 5;
-  const int r = wid * 32 + lr;                // tile row owned by this lane
-  const int64_t m = row0 + r;
-  RowInfo ri = {0, 0, -1, 0};
-  if (m >= 0 && m < T) ri = a.info[m];
-  // Raw tap bits: nothing reads them before the epilogue, so no wait for
-  // these loads is placed ahead of the main loop.
-  uint32_t tap_bits[2] = {0u, 0u};
-  uint32_t tap_sc[2] = {0x3f80u, 0x3f80u};   // bf16 bits of the column scale
-  {
-    const int c = tid >> 2, j = tid & 3;
+  // The epilogue share of this lane: tile rows rbase .. rbase + 31 of the
+  // columns ncol + 32 j (j = 0..3).  Its inputs are fetched before the first
+  // DMA so their latency hides under the main loop (and no wait_vm count
+  // below has to include them): the segment position and rows left of the
+  // first row, the raw conv taps of the four columns and their fp8 scales.
+  const int rbase = wm * 64 + 32 * hf;
+  const int64_t t0 = row0 + rbase;
+  const int ncol = n0 + 128 * wn + lc;
+  int pos0 = -1, rem0 = 0;
+  if (t0 >= 0 && t0 < T) {
+    const int2 pr = *reinterpret_cast<const int2*>(a.info + t0);
+    pos0 = pr.x;
+    rem0 = pr.y;
+  }
+  uint32_t tap_raw[4][4], sc_raw[4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int n = n0 + h * 128 + c;
-      if (n < a.C_kv) {
-        if constexpr (std::is_same<TB, fp8_t>::value) tap_sc[h] = *col_scale_ptr(a, n);
-        const int64_t i = (int64_t)n * a.w + a.w - 1 - j;
-        if (j <= a.w - 1) {
-          if (a.conv_bf16) tap_bits[h] = static_cast<const uint16_t*>(a.conv_w)[i];
-          else tap_bits[h] = static_cast<const uint32_t*>(a.conv_w)[i];
+  for (int j = 0; j < 4; ++j) {
+    const int n = ncol + 32 * j;
+    sc_raw[j] = 0x3f80u;   // bf16 bits of 1
+#pragma unroll
+    for (int d = 0; d < 4; ++d) tap_raw[j][d] = 0u;
+    if (n < a.N) {
+      if constexpr (std::is_same<TB, fp8_t>::value) sc_raw[j] = *col_scale_ptr(a, n);
+    }
+    if (n < a.C_kv) {
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        if (d < a.w) {
+          const int64_t i = (int64_t)n * a.w + a.w - 1 - d;   // tap of row t - d
+          tap_raw[j][d] = a.conv_bf16 ? (uint32_t) static_cast<const uint16_t*>(a.conv_w)[i] << 16
+                                      : static_cast<const uint32_t*>(a.conv_w)[i];
         }
       }
     }
@@ -206,7 +265,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int row = (wid * 2 + i) * 16 + (lane >> 2);
-    const int c = (lane & 3) ^ swz(row);
+    const int c = (lane & 3) ^ swz_a(row);
     int64_t mr = row0 + row;
     mr = mr < 0 ? 0 : (mr >= T ? T - 1 : mr);   // rows outside [0, T) are never output
     a_src[i] = static_cast<const char*>(a.A) + (mr * K + c * 8) * 2;
@@ -217,7 +276,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     int row, coff;
     if (std::is_same<TB, bf16_t>::value) {
       row = (wid * 2 + i) * 16 + (lane >> 2);
-      coff = ((lane & 3) ^ swz(row)) * 8;   // elements
+      coff = ((lane & 3) ^ swz_b(row)) * 8;   // elements
     } else {
       row = wid * 32 + (lane >> 1);
       coff = (lane & 1) * 16;
@@ -231,19 +290,22 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     b_src[i] = p;
   }
 
-  const int fl = swz(lane & 31), hi = lane >> 5;
-  const int a_row_off = (wm * 64 + (lane & 31)) * 64;
-  const int a_k0 = a_row_off + ((0 + hi) ^ fl) * 16;
-  const int a_k1 = a_row_off + ((2 + hi) ^ fl) * 16;
+  // A fragment of lane l (MFMA row l % 32 of block i): the anchor row that
+  // makes lane l's accumulators rows rbase + 16 i .. + 15 in order (see
+  // tok_row)
+  const int fhi = lane >> 5;
+  const int arow = wm * 64 + tok_row(lc);
+  const int a_k0 = arow * 64 + ((0 + fhi) ^ swz_a(arow)) * 16;
+  const int a_k1 = arow * 64 + ((2 + fhi) ^ swz_a(arow)) * 16;
   int b_k0, b_k1;
   if (std::is_same<TB, bf16_t>::value) {
-    const int b_row_off = A_BYTES + (wn * 128 + (lane & 31)) * 64;
-    b_k0 = b_row_off + ((0 + hi) ^ fl) * 16;
-    b_k1 = b_row_off + ((2 + hi) ^ fl) * 16;
+    const int brow = wn * 128 + (lane & 31);
+    b_k0 = A_BYTES + brow * 64 + ((0 + fhi) ^ swz_b(brow)) * 16;
+    b_k1 = A_BYTES + brow * 64 + ((2 + fhi) ^ swz_b(brow)) * 16;
   } else {
     const int b_row_off = A_BYTES + (wn * 128 + (lane & 31)) * 32;
-    b_k0 = b_row_off + hi * 8;
-    b_k1 = b_row_off + 16 + hi * 8;
+    b_k0 = b_row_off + fhi * 8;
+    b_k1 = b_row_off + 16 + fhi * 8;
   }
 
   bf16x8 fa[2][2], fb[2][4];
@@ -259,7 +321,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     const int q = qq == 0 ? 0 : (qq <= 4 ? qq + 1 : 1);   // 0,1: A fragments; 2..5: B fragments
     const lchar* sb = smem + stage * STAGE;
     if (q < 2) {
-      fa[slot][q] = as_bf16x8(ld16(sb + (ks ? a_k1 : a_k0) + q * 32 * 64));
+      fa[slot][q] = as_bf16x8(ld16(sb + (ks ? a_k1 : a_k0) + q * 16 * 64));
     } else if (std::is_same<TB, bf16_t>::value) {
       fb[slot][q - 2] = as_bf16x8(ld16(sb + (ks ? b_k1 : b_k0) + (q - 2) * 32 * 64));
     } else {
@@ -272,12 +334,13 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
       fb[slot][q - 2] = as_bf16x8(o);
     }
   };
-  // Weights go in as the MFMA's first operand, so acc[i][j] is the
-  // transposed 32x32 block: lane l holds row 32 i + l%32 of the wave's
-  // sub-tile, columns 32 j + 8 q + 4 (l/32) .. +3 in registers 4q .. 4q+3.
+  // Anchors go in as the MFMA's first operand: acc[i][j] register r of lane
+  // l is column 32 j + l % 32 of the wave's sub-tile at MFMA row
+  // 8 (r / 4) + 4 (l / 32) + r % 4, which tok_row maps to tile row
+  // rbase + 16 i + r.
   auto mma_one = [&](int slot, int q) {
     const int i = q >> 2, j = q & 3;
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][j], fa[slot][i], acc[i][j], 0, 0, 0);
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j], 0, 0, 0);
   };
   auto dma_one = [&](int kt, int stage, int q) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem + stage * STAGE;
@@ -350,155 +413,201 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   __builtin_amdgcn_sched_barrier(0);
 
   // ------------------------------------------------------------ epilogue
-  // Lanes l and l+32 own tile row 32 wid + l%32; lane half ch handles
-  // columns [64 ch, 64 ch + 64) of each 128-column half.
-  constexpr int CW = D < 64 ? D : 64;          // columns of one head a lane handles
-  constexpr int HPL = 64 / CW;                 // heads (or head halves) per lane
-  lfloat* E = (lfloat*)smem_raw;
-  lfloat* TAPS = (lfloat*)(smem_raw + E_BYTES);
-  lfloat* erow = E + (wid * EBAND + 4 + lr) * EROW;   // slot of row r
-  const bool out = r >= HALO && m < T;        // m >= 0 holds for r >= HALO
-  const bool need_mask = __builtin_amdgcn_ballot_w64(out && ri.pos < HALO) != 0;
+  // Lane (hf, lc) holds x = the raw projection of its 4 columns at its 32
+  // consecutive tile rows: x(j, u) = acc[u / 16][j][u % 16] is row rbase + u
+  // of column ncol + 32 j.  The conv runs down those registers; only the 3
+  // rows before rbase come from another lane (lane l ^ 32 of this wave for
+  // hf = 1, of the wave above for hf = 0), through the LDS.
+#define XU(j, u) acc[(u) >> 4][j][(u) & 15]
+  lfloat* XB = (lfloat*)(smem_raw + EPI_OFF);
+  lfloat* INV = (lfloat*)(smem_raw + EPI_OFF + XB_BYTES);
+  {
+    lfloat* p = XB + (wid * 64 + lane) * 12;
+    st_f4(p, XU(0, 29), XU(1, 29), XU(2, 29), XU(3, 29));
+    st_f4(p + 4, XU(0, 30), XU(1, 30), XU(2, 30), XU(3, 30));
+    st_f4(p + 8, XU(0, 31), XU(1, 31), XU(2, 31), XU(3, 31));
+  }
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_s_barrier();
+  nf32x4 xp[3];    // xp[k][j]: row rbase - 3 + k of column j (zero above the tile)
+  {
+    const lfloat* p = XB + ((hf ? wid : (wid >= 2 ? wid - 2 : wid)) * 64 + (lane ^ 32)) * 12;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      xp[k] = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(p + 4 * k);
+      if (rbase == 0) xp[k] = nf32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+
   const int w1 = a.w - 1;
-  const bool tail_row = a.tail != nullptr && out && ri.slot >= 0 && ri.rem <= w1;
-  const bool any_tail = __builtin_amdgcn_ballot_w64(tail_row) != 0;
-  const bool tail_bf16 = a.tail_bf16 != 0;
-
-  for (int h = 0; h < 2; ++h) {
-    const int nh0 = n0 + h * 128;
-    if (nh0 >= a.N) break;
-    if (h) {
-      __builtin_amdgcn_s_waitcnt(0xc07f);
-      __builtin_amdgcn_s_barrier();     // every wave is done reading half 0
-    }
-    if (wn == h) {
-      // 16-byte row-major writes (4 consecutive columns per lane); 16 rows
-      // 132 floats apart cover all 64 banks once
-      const int c4 = 4 * (lane >> 5);
+  // Fast case: all 32 rows lie inside one segment, at least w - 1 rows past
+  // its start (or are the tile's first rows, which are not output) and more
+  // than w - 1 rows before its end (no tail rows).  Otherwise the masks are
+  // built from the rows' segment info.
+  const bool fast = rem0 >= 32 + w1 && (pos0 >= w1 || rbase == 0);
+  const bool wave_fast = __builtin_amdgcn_ballot_w64(!fast) == 0;
+  // bit u of m1 / m2 / m3: row u may use row u-1 / u-2 / u-3 (same segment);
+  // outm: row u is an output; tailm: row u is one of its segment's last w-1
+  // rows (the conv state)
+  uint32_t m1 = ~0u, m2 = ~0u, m3 = ~0u, outm = rbase ? ~0u : ~7u, tailm = 0u;
+  if (!wave_fast && !fast) {
+    m1 = m2 = m3 = outm = 0u;
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int band = wm * 2 + i;
-        lfloat* dst = E + (band * EBAND + 4 + lr) * EROW + c4;
+    for (int b = 0; b < 4; ++b) {
+      int2 pr[8];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            st_f4(dst + j * 32 + 8 * q, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-        // the last 3 rows of a band are also the next band's halo
-        if (band < WAVES - 1 && lr >= 29) {
-          lfloat* hdst = E + ((band + 1) * EBAND + 1 + (lr - 29)) * EROW + c4;
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              st_f4(hdst + j * 32 + 8 * q, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-        }
+      for (int k = 0; k < 8; ++k) {
+        const int64_t t = t0 + 8 * b + k;
+        pr[k] = int2{-1, 0};
+        if (t >= 0 && t < T) pr[k] = *reinterpret_cast<const int2*>(a.info + t);
       }
-    }
-    {
-      // conv taps of this half's k | v columns: TAPS[j][c] multiplies row t-j
-      // (an fp8 column's scale is folded in: the conv is linear per column)
-      const int c = tid >> 2, j = tid & 3;
-      const float sc = bf16_bits_to_f32((uint16_t)(h ? tap_sc[1] : tap_sc[0]));
-      const int sh = a.conv_bf16 ? 16 : 0;
-      TAPS[j * 128 + c] = __builtin_bit_cast(float, (h ? tap_bits[1] : tap_bits[0]) << sh) * sc;
-    }
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-    __builtin_amdgcn_s_barrier();
-
-    for (int hl = 0; hl < HPL; ++hl) {
-      const int c0 = 64 * ch + hl * CW;       // first column of this lane's piece, in the half
-      const int e0 = c0 % D;                  // its offset inside the head
-      const int nb = nh0 + c0 - e0;           // first projection column of the head
-      if (nb >= a.N) continue;
-      if (nb < a.C_kv) {
-        // ---- k or v head: conv, SiLU, (key) L2 norm.  Columns go 4 at a
-        // time (16-byte reads of this row and the 3 before it).
-        const bool is_k = nb < a.C_k;
-        const int hh = is_k ? nb / D : (nb - a.C_k) / D;
-        auto conv4 = [&](int c, auto mask_tag) {
-          constexpr bool MASK = decltype(mask_tag)::value;
-          nf32x4 x[4], tp[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            x[j] = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow - j * EROW + c);
-            tp[j] = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(TAPS + j * 128 + c);
-          }
-          if (MASK) {
-#pragma unroll
-            for (int j = 1; j < 4; ++j)
-              if (ri.pos < j) x[j] = nf32x4{0.f, 0.f, 0.f, 0.f};
-          }
-          nf32x4 y;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            float v = tp[0][u] * x[0][u];
-            v = fmaf(tp[1][u], x[1][u], v);
-            v = fmaf(tp[2][u], x[2][u], v);
-            v = fmaf(tp[3][u], x[3][u], v);
-            y[u] = v * fast_sigmoid(v);
-          }
-          return y;
-        };
-        char* dst = static_cast<char*>(is_k ? a.Kbuf : a.Vbuf) + (((int64_t)hh * T + (out ? m : 0)) * D + e0) * 2;
-        auto head_pass = [&](auto mask_tag) {
-          // pass 1: y and (keys) its sum of squares; y replaces x in this
-          // row's slot (rows after it have read x already: same wave,
-          // earlier instruction; the next band reads its own halo copy)
-          float ss0 = 0.f, ss1 = 0.f;
-          __builtin_amdgcn_s_waitcnt(0xc07f);
-#pragma unroll 4
-          for (int c = c0; c < c0 + CW; c += 4) {
-            const nf32x4 y = conv4(c, mask_tag);
-            ss0 = fmaf(y[0], y[0], fmaf(y[1], y[1], ss0));
-            ss1 = fmaf(y[2], y[2], fmaf(y[3], y[3], ss1));
-            *reinterpret_cast<__attribute__((address_space(3))) nf32x4*>(erow + c) = y;
-          }
-          float ss = ss0 + ss1;
-          if constexpr (D > 64) {
-            // the other 64 columns of the head are in lane l ^ 32
-            ss += __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __builtin_bit_cast(int, ss)));
-          }
-          const float inv = is_k ? 1.f / sqrtf(ss + a.eps) : 1.f;
-#pragma unroll 4
-          for (int q = 0; q < CW / 8; ++q) {
-            const nf32x4 y0 = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow + c0 + 8 * q);
-            const nf32x4 y1 = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(erow + c0 + 8 * q + 4);
-            uint4 o;
-            o.x = pack_bf16x2(y0[0] * inv, y0[1] * inv);
-            o.y = pack_bf16x2(y0[2] * inv, y0[3] * inv);
-            o.z = pack_bf16x2(y1[0] * inv, y1[1] * inv);
-            o.w = pack_bf16x2(y1[2] * inv, y1[3] * inv);
-            if (out) *reinterpret_cast<uint4*>(dst + q * 16) = o;
-          }
-        };
-        // the raw projection of the segment's last w-1 rows is the conv state
-        // (before the pass overwrites the row)
-        if (any_tail && tail_row) {
-          for (int e = 0; e < CW; ++e)
-            store_elem(a.tail, ((int64_t)ri.slot * a.c_tail + a.tail_kv_off + nb + e0 + e) * w1 + (w1 - ri.rem),
-                       erow[c0 + e] * col_scale<TB>(a, nb + e0 + e), tail_bf16);
-        }
-        if (need_mask) head_pass(std::true_type{});
-        else head_pass(std::false_type{});
-      } else {
-        // ---- gate columns: G = log2 alpha from a, beta from b (no conv)
-        for (int e = 0; e < CW; ++e) {
-          const int n = nb + e0 + e;
-          if (n >= a.N) break;
-          const float x = erow[c0 + e] * col_scale<TB>(a, n);
-          if (n < a.C_kv + a.H_v) {
-            const int hv = n - a.C_kv;
-            const float gl = -__expf(a.a_log[hv]) * softplus(x + a.dt_bias[hv]) * kLog2e;
-            if (out) a.Gbuf[(int64_t)hv * T + m] = gl;
-          } else {
-            const int hv = n - a.C_kv - a.H_v;
-            if (out) a.Bbuf[(int64_t)hv * T + m] = fast_sigmoid(x);
-          }
+      for (int k = 0; k < 8; ++k) {
+        const int u = 8 * b + k;
+        const uint32_t bit = 1u << u;
+        if (pr[k].x >= 1) m1 |= bit;
+        if (pr[k].x >= 2) m2 |= bit;
+        if (pr[k].x >= 3) m3 |= bit;
+        if (pr[k].x >= 0 && rbase + u >= HALO) {
+          outm |= bit;
+          if (pr[k].y <= w1) tailm |= bit;
         }
       }
     }
   }
+  if (a.tail == nullptr) tailm = 0u;
+  const bool tail_bf16 = a.tail_bf16 != 0;
+  // Wave-uniform row sets: cmask, the rows where some lane masks a conv
+  // term; ofull, the rows every lane outputs (rows 0-2 of the tile are not).
+  uint32_t cmask = 0u, ofull = wm == 0 ? ~7u : ~0u;
+  if (!wave_fast) {
+    cmask = wave_reduce<true>(~(m1 & m2 & m3));
+    ofull = wave_reduce<false>(outm);
+  }
+  const bool any_tail = __builtin_amdgcn_ballot_w64(tailm != 0u) != 0;
+
+  // conv taps (row t - d) with the fp8 column scale and -log2(e) folded in:
+  // the conv yields z = -log2(e) c, so e^-c = 2^z and SiLU(c) = -ln2 z / (1 + 2^z)
+  float tp[4][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      tp[j][d] = __builtin_bit_cast(float, tap_raw[j][d]) * bf16_bits_to_f32(sc_raw[j]) * -kLog2e;
+
+  // store of row u: unconditional where every lane outputs it
+  auto row_store = [&](auto* p, auto v, int u) {
+    if ((ofull >> u) & 1u) *p = v;
+    else if ((outm >> u) & 1u) *p = v;
+  };
+
+  constexpr int NH = 128 / D, JB = D / 32;   // heads per wave, 32-column blocks per head
+  static_for<NH>([&](auto hd_c) {
+    constexpr int hd = decltype(hd_c)::value;
+    const int nb = n0 + 128 * wn + hd * D;   // first column of the head (wave-uniform)
+    if (nb >= a.N) {
+    } else if (nb < a.C_kv) {
+      // ---- k or v head: conv, SiLU, (keys) L2 norm
+      const bool is_k = nb < a.C_k;
+      if (any_tail) {
+        // the raw projection of the segment's last w-1 rows is the conv state
+        static_for<JB>([&](auto jj_c) {
+          constexpr int j = hd * JB + decltype(jj_c)::value;
+          const float sc = bf16_bits_to_f32(sc_raw[j]);
+#pragma unroll
+          for (int u = 0; u < 32; ++u) {
+            if ((tailm >> u) & 1u) {
+              const RowInfo r = a.info[t0 + u];
+              if (r.slot >= 0)
+                store_elem(a.tail, ((int64_t)r.slot * a.c_tail + a.tail_kv_off + ncol + 32 * j) * w1 + (w1 - r.rem),
+                           XU(j, u) * sc, tail_bf16);
+            }
+          }
+        });
+      }
+      // Rows in descending order, so each x is overwritten only after the
+      // three rows after it have read it; one row of the head's blocks per
+      // group (the scheduler would otherwise hoist every row's exp and keep
+      // all conv results live at once).
+      float ss[32];
+      auto conv_row = [&](int u, auto mask_tag) {
+        constexpr bool MASK = decltype(mask_tag)::value;
+        ss[u] = 0.f;
+        static_for<JB>([&](auto jj_c) {
+          constexpr int j = hd * JB + decltype(jj_c)::value;
+          const float x1 = u >= 1 ? XU(j, u - 1) : xp[2][j];
+          const float x2 = u >= 2 ? XU(j, u - 2) : xp[u + 1][j];
+          const float x3 = u >= 3 ? XU(j, u - 3) : xp[u][j];
+          float z = tp[j][0] * XU(j, u);
+          z = fmaf(tp[j][1], MASK && !((m1 >> u) & 1u) ? 0.f : x1, z);
+          z = fmaf(tp[j][2], MASK && !((m2 >> u) & 1u) ? 0.f : x2, z);
+          z = fmaf(tp[j][3], MASK && !((m3 >> u) & 1u) ? 0.f : x3, z);
+          float y = z * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(z));   // -SiLU / ln2
+          asm volatile("" : "+v"(y));   // materialise y here (not z and 1/(1+2^z) until the stores)
+          XU(j, u) = y;
+          ss[u] = fmaf(y, y, ss[u]);
+        });
+      };
+#pragma unroll
+      for (int u = 31; u >= 0; --u) {
+        if ((cmask >> u) & 1u) conv_row(u, std::true_type{});
+        else conv_row(u, std::false_type{});
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (is_k) {
+        // sum of squares of each row over the head's D columns: over the
+        // lane's blocks above, then across the 32 lanes of the half-wave
+        // (reduce-scatter: lane lc ends with the total of row bitrev5(lc))
+        bfly_step<32, 0, 0xB1>(ss, lc);    // quad_perm 1,0,3,2: lane ^ 1
+        bfly_step<16, 1, 0x4E>(ss, lc);    // quad_perm 2,3,0,1: lane ^ 2
+        bfly_step<8, 2, 0x124>(ss, lc);    // row_ror 4: bit 2 flipped
+        bfly_step<4, 3, 0x128>(ss, lc);    // row_ror 8: lane ^ 8
+        bfly_step<2, 4, -1>(ss, lc);       // swizzle: lane ^ 16
+        const int tau = (int)(__builtin_bitreverse32((uint32_t)lc) >> 27);
+        INV[((wid * 2 + hf) * NH + hd) * 32 + tau] = -kLn2 * __builtin_amdgcn_rsqf(kLn2 * kLn2 * ss[0] + a.eps);
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+      }
+      // scale (1/|k| for keys), round to bf16, store two rows per pack
+      const int hh = is_k ? nb / D : (nb - a.C_k) / D;
+      uint16_t* dst = static_cast<uint16_t*>(is_k ? a.Kbuf : a.Vbuf) + ((int64_t)hh * T + t0) * D + lc;
+      const lfloat* ivp = INV + ((wid * 2 + hf) * NH + hd) * 32;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        nf32x4 iv = nf32x4{-kLn2, -kLn2, -kLn2, -kLn2};
+        if (is_k) iv = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(ivp + 4 * q);
+        static_for<JB>([&](auto jj_c) {
+          constexpr int jj = decltype(jj_c)::value, j = hd * JB + jj;
+#pragma unroll
+          for (int v = 0; v < 4; v += 2) {
+            const int u = 4 * q + v;
+            const uint32_t p = pack_bf16x2(XU(j, u) * iv[v], XU(j, u + 1) * iv[v + 1]);
+            row_store(dst + (int64_t)u * D + 32 * jj, (uint16_t)(p & 0xffffu), u);
+            row_store(dst + (int64_t)(u + 1) * D + 32 * jj, (uint16_t)(p >> 16), u + 1);
+          }
+        });
+      }
+    } else {
+      // ---- gate columns: G = log2 alpha from a, beta from b (no conv)
+      static_for<JB>([&](auto jj_c) {
+        constexpr int j = hd * JB + decltype(jj_c)::value;
+        const int n = ncol + 32 * j;
+        const float sc = bf16_bits_to_f32(sc_raw[j]);
+        if (n < a.C_kv + a.H_v) {
+          const int hv = n - a.C_kv;
+          const float al = -__expf(a.a_log[hv]) * kLog2e, db = a.dt_bias[hv];
+          float* g = a.Gbuf + (int64_t)hv * T + t0;
+#pragma unroll
+          for (int u = 0; u < 32; ++u) row_store(g + u, al * softplus(XU(j, u) * sc + db), u);
+        } else if (n < a.N) {
+          const int hv = n - a.C_kv - a.H_v;
+          float* bp = a.Bbuf + (int64_t)hv * T + t0;
+#pragma unroll
+          for (int u = 0; u < 32; ++u) row_store(bp + u, fast_sigmoid(XU(j, u) * sc), u);
+        }
+      });
+    }
+  });
+#undef XU
 }
 
 template <typename TB, int D>
