@@ -237,23 +237,40 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     pos0 = pr.x;
     rem0 = pr.y;
   }
-  uint32_t tap_raw[4][4], sc_raw[4];
+  // Raw conv taps, decoded in the epilogue (touching them here would make the
+  // prologue wait for the loads): with w = 4 and an aligned table, one 8-byte
+  // (bf16) or 16-byte (fp32) load per column, [row t-3, t-2, t-1, t]; else
+  // one element per tap, tr[j][d] holding the tap of row t - d.
+  const int tap_mode = (a.w == 4 && (reinterpret_cast<uintptr_t>(a.conv_w) & 15) == 0) ? (a.conv_bf16 ? 1 : 2) : 0;
+  uint32_t tr[4][4], sc_raw[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int n = ncol + 32 * j;
     sc_raw[j] = 0x3f80u;   // bf16 bits of 1
 #pragma unroll
-    for (int d = 0; d < 4; ++d) tap_raw[j][d] = 0u;
+    for (int d = 0; d < 4; ++d) tr[j][d] = 0u;
     if (n < a.N) {
       if constexpr (std::is_same<TB, fp8_t>::value) sc_raw[j] = *col_scale_ptr(a, n);
     }
     if (n < a.C_kv) {
+      if (tap_mode == 1) {
+        const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.conv_w) + (int64_t)n * 4);
+        tr[j][0] = v.x;
+        tr[j][1] = v.y;
+      } else if (tap_mode == 2) {
+        const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const float*>(a.conv_w) + (int64_t)n * 4);
+        tr[j][0] = v.x;
+        tr[j][1] = v.y;
+        tr[j][2] = v.z;
+        tr[j][3] = v.w;
+      } else {
 #pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        if (d < a.w) {
-          const int64_t i = (int64_t)n * a.w + a.w - 1 - d;   // tap of row t - d
-          tap_raw[j][d] = a.conv_bf16 ? (uint32_t) static_cast<const uint16_t*>(a.conv_w)[i] << 16
-                                      : static_cast<const uint32_t*>(a.conv_w)[i];
+        for (int d = 0; d < 4; ++d) {
+          if (d < a.w) {
+            const int64_t i = (int64_t)n * a.w + a.w - 1 - d;   // tap of row t - d
+            tr[j][d] = a.conv_bf16 ? (uint32_t) static_cast<const uint16_t*>(a.conv_w)[i]
+                                   : static_cast<const uint32_t*>(a.conv_w)[i];
+          }
         }
       }
     }
@@ -490,10 +507,16 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   // the conv yields z = -log2(e) c, so e^-c = 2^z and SiLU(c) = -ln2 z / (1 + 2^z)
   float tp[4][4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < 4; ++j) {
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
-      tp[j][d] = __builtin_bit_cast(float, tap_raw[j][d]) * bf16_bits_to_f32(sc_raw[j]) * -kLog2e;
+    for (int d = 0; d < 4; ++d) {
+      uint32_t bits;
+      if (tap_mode == 1) bits = (d & 1) ? tr[j][(3 - d) >> 1] << 16 : tr[j][(3 - d) >> 1] & 0xffff0000u;
+      else if (tap_mode == 2) bits = tr[j][3 - d];
+      else bits = a.conv_bf16 ? tr[j][d] << 16 : tr[j][d];
+      tp[j][d] = __builtin_bit_cast(float, bits) * bf16_bits_to_f32(sc_raw[j]) * -kLog2e;
+    }
+  }
 
   // store of row u: unconditional where every lane outputs it
   auto row_store = [&](auto* p, auto v, int u) {
@@ -571,21 +594,32 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
       const int hh = is_k ? nb / D : (nb - a.C_k) / D;
       uint16_t* dst = static_cast<uint16_t*>(is_k ? a.Kbuf : a.Vbuf) + ((int64_t)hh * T + t0) * D + lc;
       const lfloat* ivp = INV + ((wid * 2 + hf) * NH + hd) * 32;
+      // SIMPLE: every lane outputs rows 3..31, so only rows 0-2 need a
+      // per-lane predicate
+      auto out_pass = [&](auto simple_tag) {
+        constexpr bool SIMPLE = decltype(simple_tag)::value;
+        auto st = [&](uint16_t* p, uint16_t v, int u) {
+          if (SIMPLE && u >= HALO) *p = v;
+          else row_store(p, v, u);
+        };
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        nf32x4 iv = nf32x4{-kLn2, -kLn2, -kLn2, -kLn2};
-        if (is_k) iv = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(ivp + 4 * q);
-        static_for<JB>([&](auto jj_c) {
-          constexpr int jj = decltype(jj_c)::value, j = hd * JB + jj;
+        for (int q = 0; q < 8; ++q) {
+          nf32x4 iv = nf32x4{-kLn2, -kLn2, -kLn2, -kLn2};
+          if (is_k) iv = *reinterpret_cast<const __attribute__((address_space(3))) nf32x4*>(ivp + 4 * q);
+          static_for<JB>([&](auto jj_c) {
+            constexpr int jj = decltype(jj_c)::value, j = hd * JB + jj;
 #pragma unroll
-          for (int v = 0; v < 4; v += 2) {
-            const int u = 4 * q + v;
-            const uint32_t p = pack_bf16x2(XU(j, u) * iv[v], XU(j, u + 1) * iv[v + 1]);
-            row_store(dst + (int64_t)u * D + 32 * jj, (uint16_t)(p & 0xffffu), u);
-            row_store(dst + (int64_t)(u + 1) * D + 32 * jj, (uint16_t)(p >> 16), u + 1);
-          }
-        });
-      }
+            for (int v = 0; v < 4; v += 2) {
+              const int u = 4 * q + v;
+              const uint32_t p = pack_bf16x2(XU(j, u) * iv[v], XU(j, u + 1) * iv[v + 1]);
+              st(dst + (int64_t)u * D + 32 * jj, (uint16_t)(p & 0xffffu), u);
+              st(dst + (int64_t)(u + 1) * D + 32 * jj, (uint16_t)(p >> 16), u + 1);
+            }
+          });
+        }
+      };
+      if ((ofull | 7u) == ~0u) out_pass(std::true_type{});
+      else out_pass(std::false_type{});
     } else {
       // ---- gate columns: G = log2 alpha from a, beta from b (no conv)
       static_for<JB>([&](auto jj_c) {
