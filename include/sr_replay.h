@@ -189,6 +189,13 @@ typedef enum sr_kernel_kind {
 sr_status sr_kernel_timing_enable(int32_t enable);
 sr_status sr_kernel_timing_read(double* ms, int64_t* launches);
 
+/* Diagnostics for SR_ERR_HIP: the HIP error code (hipError_t) and the
+ * sr_kernel_kind of the calling thread's most recent failed launch inside
+ * sr_replay_state(), and hipGetErrorString() of that code (static storage).
+ * *hip_error is 0 and *kernel_kind -1 if no launch has failed on this thread.
+ * Any output pointer may be NULL.  Always returns SR_OK. */
+sr_status sr_last_hip_error(int32_t* hip_error, int32_t* kernel_kind, const char** message);
+
 /* Static, NUL-terminated description of a status code. */
 const char* sr_status_str(sr_status status);
 

@@ -44,11 +44,30 @@ class SrLayer(ctypes.Structure):
     _fields_ = [(name, ctypes.c_void_p) for name in _LAYER_FIELDS]
 
 
+def _hip_runtimes_mapped() -> set:
+    """Paths of every libamdhip64 mapped into this process."""
+    try:
+        with open("/proc/self/maps") as f:
+            return {line.split()[-1] for line in f if "libamdhip64" in line}
+    except OSError:  # pragma: no cover
+        return set()
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_33477_amd.build` "
                           "(or __graft_entry__.build())")
+    # The library's kernels run on memory and streams that torch owns, so it
+    # must use torch's HIP runtime.  torch ships its own libamdhip64 with the
+    # same SONAME; loading torch first lets the dynamic linker resolve the
+    # library's dependency to that copy.  Loaded the other way round, the
+    # process holds two HIP runtimes, and the second one may find no device.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
+    runtimes = _hip_runtimes_mapped()
+    if len(runtimes) > 1:
+        raise ImportError(f"two HIP runtimes are mapped into this process ({sorted(runtimes)}); "
+                          "libsr_replay.so must share torch's")
     P = ctypes.POINTER
     lib.sr_state_bytes.argtypes = [P(SrShape)]
     lib.sr_state_bytes.restype = ctypes.c_size_t
@@ -64,6 +83,8 @@ def _load() -> ctypes.CDLL:
     lib.sr_kernel_timing_enable.restype = ctypes.c_int
     lib.sr_kernel_timing_read.argtypes = [P(ctypes.c_double), P(ctypes.c_int64)]
     lib.sr_kernel_timing_read.restype = ctypes.c_int
+    lib.sr_last_hip_error.argtypes = [P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_char_p)]
+    lib.sr_last_hip_error.restype = ctypes.c_int
     lib.sr_status_str.argtypes = [ctypes.c_int]
     lib.sr_status_str.restype = ctypes.c_char_p
     return lib
@@ -72,7 +93,8 @@ def _load() -> ctypes.CDLL:
 LIB = _load()
 
 EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
-                    "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_status_str")
+                    "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_last_hip_error",
+                    "sr_status_str")
 
 KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan", "proj_conv", "row_info")
 
@@ -90,9 +112,22 @@ def status_str(status: int) -> str:
     return LIB.sr_status_str(int(status)).decode()
 
 
+def last_hip_error():
+    """(hip error code, kernel kind name or None, HIP's message) of this
+    thread's most recent failed launch inside replay_state()."""
+    code, kind, msg = ctypes.c_int32(0), ctypes.c_int32(-1), ctypes.c_char_p()
+    LIB.sr_last_hip_error(ctypes.byref(code), ctypes.byref(kind), ctypes.byref(msg))
+    name = KERNEL_KINDS[kind.value] if 0 <= kind.value < len(KERNEL_KINDS) else None
+    return int(code.value), name, (msg.value or b"").decode()
+
+
 def _check(status: int):
     if status != 0:
-        raise SrError(status, status_str(status))
+        detail = status_str(status)
+        if status == 6:                          # SR_ERR_HIP
+            code, kind, msg = last_hip_error()
+            detail += f" (kernel {kind}: hipError {code}, {msg})"
+        raise SrError(status, detail)
 
 
 def state_bytes(shape) -> int:

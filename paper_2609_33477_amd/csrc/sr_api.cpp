@@ -106,17 +106,34 @@ hipEvent_t take_event() {
   return e;
 }
 
+// The HIP error and kernel of this thread's last failed launch.
+thread_local hipError_t g_last_hip = hipSuccess;
+thread_local int g_last_kind = -1;
+
+hipError_t note(int kind, hipError_t e) {
+  if (e != hipSuccess) {
+    g_last_hip = e;
+    g_last_kind = kind;
+  }
+  return e;
+}
+
 // Runs `launch` on stream s, bracketed by events when timing is enabled.
+// The launchers report hipGetLastError(), which is per thread and sticky, so
+// an error left by an earlier unrelated HIP call is cleared first.
 template <typename F>
 hipError_t timed(int kind, hipStream_t s, F&& launch) {
-  if (!g_timing) return launch();
+  (void)hipGetLastError();
+  if (!g_timing) return note(kind, launch());
   TimedLaunch t{kind, take_event(), take_event()};
-  if (!t.start || !t.stop) return hipErrorOutOfMemory;
-  if (hipEventRecord(t.start, s) != hipSuccess) return hipErrorUnknown;
-  const hipError_t e = launch();
-  if (hipEventRecord(t.stop, s) != hipSuccess) return hipErrorUnknown;
+  if (!t.start || !t.stop) return note(kind, hipErrorOutOfMemory);
+  hipError_t e = hipEventRecord(t.start, s);
+  if (e != hipSuccess) return note(kind, e);
+  e = launch();
+  const hipError_t e2 = hipEventRecord(t.stop, s);
+  if (e == hipSuccess && e2 != hipSuccess) return note(kind, e2);
   g_records.push_back(t);
-  return e;
+  return note(kind, e);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -339,6 +356,13 @@ sr_status sr_kernel_timing_read(double* ms, int64_t* launches) {
   }
   g_records.clear();
   return st;
+}
+
+sr_status sr_last_hip_error(int32_t* hip_error, int32_t* kernel_kind, const char** message) {
+  if (hip_error) *hip_error = (int32_t)g_last_hip;
+  if (kernel_kind) *kernel_kind = g_last_kind;
+  if (message) *message = hipGetErrorString(g_last_hip);
+  return SR_OK;
 }
 
 const char* sr_status_str(sr_status status) {

@@ -28,11 +28,16 @@ def test_header_declares_and_library_exports_every_function():
     names = declared_functions()
     assert set(names) == {"sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
                           "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read",
-                          "sr_status_str"}
+                          "sr_last_hip_error", "sr_status_str"}
     lib = ctypes.CDLL(sr.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(sr.EXPORTED_SYMBOLS)
+
+
+def test_last_hip_error_is_clear_without_a_failed_launch():
+    code, kind, msg = sr.last_hip_error()
+    assert code == 0 and kind is None and isinstance(msg, str)
 
 
 def test_size_helpers_match_paper_table():
