@@ -10,17 +10,21 @@
 // Only the last two lines touch the state.  The workgroup runs a pipeline
 // with one barrier per sub-chunk step:
 //   4 prep waves: wave p builds everything but the state lines for the
-//     sub-chunks m = p (mod 4), spread over the 4 steps before the state
-//     needs them -- gates, Gram block and A (step m-4), a 32-step forward
-//     substitution in fp32, lane = column of T (steps m-3 and m-2), then
-//     Tu = T diag(beta) and W^T = K^T (T diag(beta 2^G))^T, which leaves W
-//     row-major (step m-1);
+//     sub-chunk pairs (m, m+1), m = 2p (mod 8), over the 8 steps before the
+//     state needs them, lanes 0-31 serving sub-chunk m and lanes 32-63
+//     sub-chunk m+1 wherever the work is one lane per row or column:
+//     K rows for the Gram blocks straight from global memory (issued two
+//     steps ahead); log2-alpha prefix and Gram blocks on MFMA (step m-7); A
+//     (m-6); T = (I + A)^{-1} by a 32-step forward substitution in fp32,
+//     lane = column of T, spread over steps m-5 .. m-3; Tu = T diag(beta)
+//     in two bf16 parts and Tw = T diag(beta 2^G) (m-2); then
+//     W^T = K^T Tw^T, which leaves W row-major (m-1 for sub-chunk m, m for
+//     m+1);
 //   d/32 state waves, wave s owning state columns [32s, 32s+32) as 2 d/16
-//     16x16 fp32 accumulator tiles for the whole segment: at step m they
-//     form U for their columns and run the state lines of sub-chunk m, and
-//     they stage K five sub-chunks ahead and V one ahead from registers
-//     loaded a step earlier.
-// K lives in a ring of 6 sub-chunk slots, V, W and Tu in rings of 2.
+//     16x16 fp32 accumulator tiles for the whole segment: at step n they
+//     run the state lines of sub-chunk n, and they request K(n+3) and V(n+2)
+//     by global -> LDS DMA, waited for one step later.
+// Rings (sub-chunk slots): K 4, V 3, W 2, Tu 4, gate vectors 16.
 //
 // Every product is v_mfma_f32_16x16x32_bf16.  A 32-wide reduction over
 // sub-chunk rows uses the k-slot order {4g..4g+3, 16+4g..16+4g+3} for lane
@@ -31,11 +35,12 @@
 // 16-lane group rows kbase..kbase+3 of column n0 + i when lane j of the group
 // addresses row kbase + j/4, columns n0 + 4 (j%4) .. +3.
 //
-// LDS (d = 128): K ring 54 KB, V and W rings 37 KB, Tu ring 6 KB, per prep
-// wave A^T (reused for Tw^T) and gate scratch 19 KB: ~117 KB, one workgroup
-// (8 waves) per CU.  Pitches are the measured conflict-free ones: row pitch
-// = 8 mod 64 dwords for 16-byte row and transposed reads, 2 mod 8 dwords for
-// 8-byte row reads and writes.
+// LDS (d = 128): K and V rings 56 KB, W ring 19 KB, Tu ring 24 KB, gate
+// vectors 4 KB, per prep wave A^T of a pair (reused for Tw^T) and gate
+// scratch 38 KB: ~141 KB, one workgroup (8 waves) per CU.  K and V rows are
+// unpadded and XOR-swizzled (kv_off) so the DMA writes whole 1 KB blocks;
+// the other pitches are the measured conflict-free ones: 8 mod 64 dwords for
+// transposed reads, 2 mod 8 dwords for 8-byte row reads and writes.
 #include "sr_device.hpp"
 
 #include <cstddef>
@@ -127,30 +132,50 @@ struct Cfg {
   static constexpr int NP = 4;                        // prep waves
   static constexpr int THREADS = 64 * (NSW + NP);
   static constexpr int NT = D / 16;                   // 16-row tiles along d
-  static constexpr int KP = D + 16;                   // K / V row pitch (bf16)
+  // K and V sub-chunks: unpadded rows of 2D bytes, 32-byte chunk pairs
+  // XOR-swizzled by row (see kv_off), staged by global -> LDS DMA
+  static constexpr int RPL = 128 / D;                 // rows per 256-byte bank line
+  static constexpr int NCP = D / 16;                  // 32-byte chunk pairs per row
+  static constexpr int DMA_ROWS = 512 / D;            // rows per 1 KB DMA block
+  static constexpr int DMA_PER = kS * 2 * D / 1024 / NSW;   // DMA blocks per state wave and matrix
   static constexpr int WP = D + 20;                   // W row pitch (bf16)
-  static constexpr int NK = 6;                        // K ring slots
-  static constexpr int SZ_KV = kS * KP * 2;           // one sub-chunk of K or V
+  static constexpr int NK = 4;                        // K ring: K(n) DMA issued at step n-3
+  static constexpr int NV = 3;                        // V ring: V(n) DMA issued at step n-2
+  static constexpr int NTU = 4;                       // Tu ring: a pair is packed two steps ahead
+  static constexpr int NVEC = 16;                     // gate-vector ring: written nine steps ahead
+  static constexpr int SZ_KV = kS * D * 2;            // one sub-chunk of K or V
   static constexpr int SZ_W = kS * WP * 2;
   static constexpr int SZ_TT = kS * kTP * 2;          // one T^T block (bf16)
-  static constexpr int SZ_A = kS * kAP * 4;           // A^T of one sub-chunk (prep-wave private; later Tw^T)
-  static constexpr int SZ_VEC = 2 * kS * 4;           // eG | eD of one sub-chunk
-  static constexpr int SZ_SCR = 2 * kS * 4;           // G prefix | beta (prep-wave private)
+  static constexpr int SZ_A = kS * kAP * 4;           // A^T of one sub-chunk (fp32)
+  static constexpr int SZ_VEC = 2 * kS * 4;           // eD[32] | 2^{G_31}
+  static constexpr int SZ_GB = 2 * kS * 4;            // G prefix[32] | beta[32] of one sub-chunk
+  // private area of a prep wave: A^T of its two sub-chunks (later Tw^T of
+  // both), then their G prefix and beta
+  static constexpr int SZ_PRIV = 2 * SZ_A + 2 * SZ_GB;
   static constexpr int OFF_K = 0;
   static constexpr int OFF_V = OFF_K + NK * SZ_KV;
-  static constexpr int OFF_W = OFF_V + 2 * SZ_KV;
-  static constexpr int OFF_TU = OFF_W + 2 * SZ_W;
-  static constexpr int OFF_A = OFF_TU + 4 * SZ_TT;     // two (Tu_hi^T | Tu_lo^T) slots
-  static constexpr int OFF_VEC = OFF_A + NP * SZ_A;
-  static constexpr int OFF_SCR = OFF_VEC + NK * SZ_VEC;
-  static constexpr int LDS = OFF_SCR + NP * SZ_SCR;
-  static constexpr int PPR = D / 8;                   // 16-byte pieces per row
-  static constexpr int PER_S = kS * PPR / (64 * NSW); // pieces per state thread per matrix
-  static constexpr int QS = 10;                       // solve steps in the first solve segment
-  static_assert(kS * PPR % (64 * NSW) == 0, "staging split");
+  static constexpr int OFF_W = OFF_V + NV * SZ_KV;
+  static constexpr int OFF_TU = OFF_W + 2 * SZ_W;     // slot: Tu_hi^T | Tu_lo^T
+  static constexpr int OFF_VEC = OFF_TU + NTU * 2 * SZ_TT;
+  static constexpr int OFF_PRIV = OFF_VEC + NVEC * SZ_VEC;
+  static constexpr int LDS = OFF_PRIV + NP * SZ_PRIV;
+  static constexpr int QG = D / 32;                   // 32-wide d blocks (Gram k-steps)
+  static_assert(DMA_PER * NSW * 1024 == kS * 2 * D, "staging split");
   static_assert(NT % 2 == 0, "state tiles pair up along d");
-  static_assert(SZ_TT <= SZ_A, "Tw^T reuses the A^T area");
+  static_assert(2 * SZ_TT <= 2 * SZ_A, "Tw^T of both sub-chunks reuses the A^T area");
+  static_assert(LDS <= 160 * 1024, "LDS");
 };
+
+// Byte offset of the 8 bytes at row r, columns 16 cb + 4 h .. + 3 (h = 0..3)
+// of a K or V sub-chunk.  Rows are unpadded (2D bytes) and the 32-byte
+// column pair cb of row r is stored at pair cb ^ ((r / RPL) mod NCP): the 8
+// consecutive rows that the 16-lane groups of a transposed read cover then
+// fall on 8 distinct groups of 8 banks, as with a row pitch of 8 mod 64 dwords.
+template <int D>
+__device__ __forceinline__ int kv_off(int r, int cb, int h) {
+  constexpr int RPL = Cfg<D>::RPL, NCP = Cfg<D>::NCP;
+  return r * 2 * D + 32 * (cb ^ ((r / RPL) % NCP)) + 8 * h;
+}
 
 __device__ int rank_to_segment(const ScanArgs& a, int rank, int* shared_sel) {
   if (a.n_seg > kSortMax) return rank;
@@ -174,7 +199,7 @@ __device__ int rank_to_segment(const ScanArgs& a, int rank, int* shared_sel) {
 template <int D>
 __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(ScanArgs a) {
   using CF = Cfg<D>;
-  constexpr int NSW = CF::NSW, NP = CF::NP, NT = CF::NT, KP = CF::KP, WP = CF::WP, NK = CF::NK;
+  constexpr int NSW = CF::NSW, NP = CF::NP, NT = CF::NT, WP = CF::WP, NK = CF::NK, NV = CF::NV, QG = CF::QG;
   __shared__ __attribute__((aligned(16))) char smem[CF::LDS];
   __shared__ int sel;
 
@@ -183,9 +208,9 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, li = lane & 15;
   // per-lane byte offsets; everything else is a compile-time immediate
-  const int kv_row = (li * KP + 8 * g) * 2;                           // 16-byte row reads of K
   const int w_row = (li * WP + 4 * g) * 2;                            // 8-byte row reads / writes of W
-  const int tr_kv = ((li >> 2) * KP + 4 * (li & 3) + 4 * g * KP) * 2; // transposed reads of K / V, rows 4g + ..
+  const int tr_row = 4 * g + (li >> 2);                              // transposed reads of K / V: row, 8-byte piece
+  const int tr_h = li & 3;
   const int tr_t = ((li >> 2) * kTP + 4 * (li & 3) + 4 * g * kTP) * 2; // transposed reads of T^T, rows 4g + ..
 
   const int u = blockIdx.x;
@@ -210,96 +235,147 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   float* st_out = *reinterpret_cast<float* const*>(kargs + offsetof(ScanArgs, state_out) + sizeof(void*) * layer);
   const size_t state_base = ((size_t)slot * a.H_v + head) * D * D;
 
-  auto kbuf = [&](int m) { return L + CF::OFF_K + (m % NK) * CF::SZ_KV; };
-  auto vbuf = [&](int m) { return L + CF::OFF_V + (m & 1) * CF::SZ_KV; };
+  auto kbuf = [&](int m) { return L + CF::OFF_K + (m & (NK - 1)) * CF::SZ_KV; };
+  auto vbuf = [&](int m) { return L + CF::OFF_V + (m % NV) * CF::SZ_KV; };
   auto wbuf = [&](int m) { return L + CF::OFF_W + (m & 1) * CF::SZ_W; };
-  auto tubuf = [&](int m) { return L + CF::OFF_TU + (m & 1) * 2 * CF::SZ_TT; };   // Tu_hi^T, then Tu_lo^T
-  auto vecbuf = [&](int m) { return (SR_LDS float*)(L + CF::OFF_VEC + (m % NK) * CF::SZ_VEC); };  // eG[32] | eD[32]
+  auto tubuf = [&](int m) { return L + CF::OFF_TU + (m & (CF::NTU - 1)) * 2 * CF::SZ_TT; };   // Tu_hi^T, then Tu_lo^T
+  auto vecbuf = [&](int m) { return (SR_LDS float*)(L + CF::OFF_VEC + (m & (CF::NVEC - 1)) * CF::SZ_VEC); };
 
   // A 32-wide reduction operand from a transposed-read matrix: rows
   // kbase + {4g..4g+3} and kbase + 16 + {4g..4g+3} of the lane's column.
   auto tr_pair = [&](const lchar* p, int pitch_bytes, bool negate) {
     return join(tr4(p), tr4(p + 16 * pitch_bytes), negate);
   };
+  // the same for column block cb (16 columns) of a K or V sub-chunk
+  auto tr_kv = [&](const lchar* base, int cb) { return tr_pair(base + kv_off<D>(tr_row, cb, tr_h), 2 * D, false); };
 
   if (wid < NP) {
     // ================================================================ prep
+    // Wave p prepares the sub-chunk pairs (m, m + 1), m = 2p (mod 8), each
+    // over the eight steps m-8 .. m-1 (phase s at step m-8+s) plus W(m+1)
+    // at step m.  Lanes 0-31 work on sub-chunk m, lanes 32-63 on m + 1 where
+    // the work is one lane per row or column (prefix, solve, packing).
     const int p = wid;
-    SR_LDS float* At = (SR_LDS float*)(L + CF::OFF_A + p * CF::SZ_A);   // A^T, later Tw^T (private)
-    lchar* Tw = (lchar*)At;
-    SR_LDS float* gsc = (SR_LDS float*)(L + CF::OFF_SCR + p * CF::SZ_SCR);   // G prefix [32] | beta [32]
-    const int col = lane & 31;                           // column of T this lane solves
+    lchar* priv = L + CF::OFF_PRIV + p * CF::SZ_PRIV;
+    const int hc = lane >> 5;                            // sub-chunk of the pair this lane serves
+    const int col = lane & 31;                           // its row (gates) / column of T (solve)
+    SR_LDS float* gsc_l = (SR_LDS float*)(priv + 2 * CF::SZ_A + hc * CF::SZ_GB);   // G prefix | beta
+    const SR_LDS float* At_l = (const SR_LDS float*)(priv + hc * CF::SZ_A);         // this lane's A^T
 
-    // log2 alpha and beta of sub-chunk m's 32 rows (lanes 0..31; rows past
-    // the segment end carry 0 and 0, which makes them inert)
-    auto load_gb = [&](int m, float& gv, float& bv) {
-      const int64_t t = s0 + (int64_t)m * kS + col;
-      const bool ok = lane < 32 && m < nsc && t < s1;
-      gv = ok ? Gp[t] : 0.f;
-      bv = ok ? Bp[t] : 0.f;
+    bf16x8 kf[2][QG][2];   // Gram operands of the pair: [sub-chunk][d block][row half]
+    float gv = 0.f, bv = 0.f;
+    f32x4 gr[2][3];        // Gram tiles (0,0), (1,0), (1,1) of each sub-chunk
+    float x[kS];           // column `col` of T, carried over the solve phases
+
+    // phase 7 of the previous pair: the pair's K rows straight from global memory
+    // as Gram fragments, and this lane's log2 alpha and beta (rows past the
+    // segment end carry 0 and 0, which makes them inert)
+    auto issue_loads = [&](int m) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int64_t t = s0 + (int64_t)(m + c) * kS + 16 * h + li;
+#pragma unroll
+          for (int q = 0; q < QG; ++q)
+            kf[c][q][h] = t < s1 ? *reinterpret_cast<const bf16x8*>(Kplane + (t * D + 32 * q + 8 * g) * 2)
+                                 : as_bf16x8(make_uint4(0, 0, 0, 0));
+        }
+      const int64_t t = s0 + (int64_t)(m + hc) * kS + col;
+      gv = t < s1 ? Gp[t] : 0.f;
+      bv = t < s1 ? Bp[t] : 0.f;
     };
-
-    float x[kS];                                         // column `col` of T, carried across segments
-    // S1: prefix, gate vectors, Gram block, A^T
-    auto seg_a = [&](int m, float gv, float bv) {
-      const lchar* Kc = kbuf(m);
+    // phase 1: prefix of log2 alpha inside each half, gate vectors, Gram
+    auto gram = [&](int m) {
       float gp = gv;
       gp += dpp_row_shr<1>(gp);
       gp += dpp_row_shr<2>(gp);
       gp += dpp_row_shr<4>(gp);
       gp += dpp_row_shr<8>(gp);
       const float g15 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gp), 15));
-      if (lane >= 16) gp += g15;
+      const float g47 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gp), 47));
+      if (col >= 16) gp += hc ? g47 : g15;
       const float g31 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gp), 31));
-      SR_LDS float* vec = vecbuf(m);
-      if (lane < 32) {
-        gsc[col] = gp;
-        gsc[kS + col] = bv;
-        vec[col] = exp2f(gp);                 // 2^{G_i}
-        vec[kS + col] = exp2f(g31 - gp);      // 2^{G_31 - G_i}
-      }
-      f32x4 g00 = zero4(), g10 = zero4(), g11 = zero4();
+      const float g63 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gp), 63));
+      const float glast = hc ? g63 : g31;
+      SR_LDS float* vec = vecbuf(m + hc);
+      gsc_l[col] = gp;
+      gsc_l[kS + col] = bv;
+      vec[col] = exp2f(glast - gp);           // 2^{G_31 - G_i}
+      if (col == kS - 1) vec[kS] = exp2f(gp); // 2^{G_31}
 #pragma unroll
-      for (int q = 0; q < D / 32; ++q) {
-        const bf16x8 k0 = as_bf16x8(lds_ld16(Kc + kv_row + 32 * q * 2));
-        const bf16x8 k1 = as_bf16x8(lds_ld16(Kc + kv_row + (16 * KP + 32 * q) * 2));
-        g00 = mma_k32(g00, k0, k0);
-        g10 = mma_k32(g10, k1, k0);
-        g11 = mma_k32(g11, k1, k1);
-      }
-      __builtin_amdgcn_s_waitcnt(0xc07f);          // this wave's writes of gsc have landed
-      const float gj0 = gsc[li], gj1 = gsc[16 + li];
-      float a00[4], a10[4], a11[4];
+      for (int c = 0; c < 2; ++c) {
+        f32x4 g00 = zero4(), g10 = zero4(), g11 = zero4();
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i0 = 4 * g + r, i1 = 16 + 4 * g + r;
-        const float b0 = gsc[kS + i0], b1 = gsc[kS + i1], gi0 = gsc[i0], gi1 = gsc[i1];
-        a00[r] = (i0 > li) ? b0 * exp2f(fminf(gi0 - gj0, 0.f)) * g00[r] : 0.f;
-        a10[r] = b1 * exp2f(fminf(gi1 - gj0, 0.f)) * g10[r];
-        a11[r] = (i1 > 16 + li) ? b1 * exp2f(fminf(gi1 - gj1, 0.f)) * g11[r] : 0.f;
+        for (int q = 0; q < QG; ++q) {
+          g00 = mma_k32(g00, kf[c][q][0], kf[c][q][0]);
+          g10 = mma_k32(g10, kf[c][q][1], kf[c][q][0]);
+          g11 = mma_k32(g11, kf[c][q][1], kf[c][q][1]);
+        }
+        gr[c][0] = g00;
+        gr[c][1] = g10;
+        gr[c][2] = g11;
       }
-      // stored transposed, At[j][i] = A_ij: one 16-byte store per block
-      lds_stf4((lchar*)(At + li * kAP + 4 * g), a00);
-      lds_stf4((lchar*)(At + li * kAP + 16 + 4 * g), a10);
-      lds_stf4((lchar*)(At + (16 + li) * kAP + 16 + 4 * g), a11);
     };
-    // S2 / S3: T = (I + A)^{-1}, lane = column, column-oriented: once
+    // phase 2: A_ij = beta_i 2^{G_i - G_j} Gram_ij (i > j), stored
+    // transposed, At[j][i] = A_ij: one 16-byte store per 16x16 block
+    auto make_a = [&]() {
+      // both sub-chunks' gate values first (the compiler cannot move these
+      // reads above the A stores, which it cannot tell apart)
+      float gj[2][2];
+      float4 gi[2][2], bi[2][2];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const SR_LDS float* gs = (const SR_LDS float*)(priv + 2 * CF::SZ_A + c * CF::SZ_GB);
+        gj[c][0] = gs[li];
+        gj[c][1] = gs[16 + li];
+        gi[c][0] = lds_ldf4((const lchar*)(gs + 4 * g));
+        gi[c][1] = lds_ldf4((const lchar*)(gs + 16 + 4 * g));
+        bi[c][0] = lds_ldf4((const lchar*)(gs + kS + 4 * g));
+        bi[c][1] = lds_ldf4((const lchar*)(gs + kS + 16 + 4 * g));
+      }
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        SR_LDS float* At = (SR_LDS float*)(priv + c * CF::SZ_A);
+        const float gj0 = gj[c][0], gj1 = gj[c][1];
+        const float gi0v[4] = {gi[c][0].x, gi[c][0].y, gi[c][0].z, gi[c][0].w};
+        const float gi1v[4] = {gi[c][1].x, gi[c][1].y, gi[c][1].z, gi[c][1].w};
+        const float bi0v[4] = {bi[c][0].x, bi[c][0].y, bi[c][0].z, bi[c][0].w};
+        const float bi1v[4] = {bi[c][1].x, bi[c][1].y, bi[c][1].z, bi[c][1].w};
+        float a00[4], a10[4], a11[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i0 = 4 * g + r, i1 = 16 + 4 * g + r;
+          a00[r] = (i0 > li) ? bi0v[r] * exp2f(fminf(gi0v[r] - gj0, 0.f)) * gr[c][0][r] : 0.f;
+          a10[r] = bi1v[r] * exp2f(fminf(gi1v[r] - gj0, 0.f)) * gr[c][1][r];
+          a11[r] = (i1 > 16 + li) ? bi1v[r] * exp2f(fminf(gi1v[r] - gj1, 0.f)) * gr[c][2][r] : 0.f;
+        }
+        lds_stf4((lchar*)(At + li * kAP + 4 * g), a00);
+        lds_stf4((lchar*)(At + li * kAP + 16 + 4 * g), a10);
+        lds_stf4((lchar*)(At + (16 + li) * kAP + 16 + 4 * g), a11);
+      }
+    };
+    // phases 3-5: T = (I + A)^{-1}, lane = column, column-oriented: once
     // x_q = T[q][col] is final it is eliminated from every later row.  Each
-    // step needs one column of A (a row of A^T), read two steps ahead; the
-    // empty asm keeps each step's updates in place (later loads may not be
-    // hoisted above them, nor the updates sunk below).
-    auto solve = [&](auto q0_tag, auto q1_tag) {
-      constexpr int Q0 = decltype(q0_tag)::value, Q1 = decltype(q1_tag)::value;
-      float4 cb[3][kS / 4];
-      auto load_col = [&](int q, float4* dst) {
+    // step needs one column of A (a row of A^T), read two steps ahead, so
+    // the pipeline runs on across the phase barriers (the first two columns
+    // are read at the end of phase 2).  The empty asm keeps each step's
+    // updates in place (later loads may not be hoisted above them, nor the
+    // updates sunk below).
+    float4 cb[3][kS / 4];
+    auto load_col = [&](int q, float4* dst) {
 #pragma unroll
-        for (int v = (q + 1) / 4; v < kS / 4; ++v) dst[v] = lds_ldf4((const lchar*)(At + q * kAP + 4 * v));
-      };
-      load_col(Q0, cb[Q0 % 3]);
-      if (Q0 + 1 < Q1) load_col(Q0 + 1, cb[(Q0 + 1) % 3]);
+      for (int v = (q + 1) / 4; v < kS / 4; ++v) dst[v] = lds_ldf4((const lchar*)(At_l + q * kAP + 4 * v));
+    };
+    auto solve = [&]() {
+      int cl = col;
+      asm volatile("" : "+v"(cl));
 #pragma unroll
-      for (int q = Q0; q < Q1; ++q) {
-        if (q + 2 < Q1) load_col(q + 2, cb[(q + 2) % 3]);
+      for (int i = 0; i < kS; ++i) x[i] = (i == cl) ? 1.f : 0.f;
+#pragma unroll
+      for (int q = 0; q < kS; ++q) {
+        if (q == 6 || q == 14) lds_barrier();          // phases 4 and 5 start here
+        if (q + 2 < kS) load_col(q + 2, cb[(q + 2) % 3]);
         const float xq = x[q];
         const float4* cv = cb[q % 3];
 #pragma unroll
@@ -313,76 +389,94 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
         __builtin_amdgcn_sched_barrier(0);
       }
     };
-    // S4: Tu^T and Tw^T rows (columns of T diag(beta) and T diag(beta 2^G),
-    // each rounded once; lane `col` writes row `col`), then W^T = K^T Tw^T:
-    // lane (li, g) of tile (td, bi) ends with W[16 bi + li][16 td + 4g ..],
-    // stored negated (the state subtracts W M0) as an 8-byte row-major store
-    auto seg_d = [&](int m) {
-      const float bc = gsc[kS + col];
-      const float wc = bc * exp2f(gsc[col]);
-      lchar* Tu = tubuf(m);
-      if (lane < 32) {
+    // phase 6: Tu^T and Tw^T rows (columns of T diag(beta) and
+    // T diag(beta 2^G), each rounded once; lane `col` writes row `col`), Tu
+    // into the shared ring, Tw into the private area (A is no longer read)
+    auto pack = [&](int m) {
+      const float bc = gsc_l[kS + col];
+      const float wc = bc * exp2f(gsc_l[col]);
+      lchar* Tu = tubuf(m + hc);
+      lchar* Tw = priv + hc * CF::SZ_TT;
 #pragma unroll
-        for (int q = 0; q < kS / 8; ++q) {
-          // Tu in two bf16 parts (hi + lo): U = Tu V is the state's only
-          // product whose rounding does not average over the segment
-          uint32_t th[4], tl[4];
+      for (int q = 0; q < kS / 8; ++q) {
+        // Tu in two bf16 parts (hi + lo): U = Tu V is the state's only
+        // product whose rounding does not average over the segment
+        uint32_t th[4], tl[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float u0 = x[8 * q + 2 * e] * bc, u1 = x[8 * q + 2 * e + 1] * bc;
-            th[e] = pack_bf16x2(u0, u1);
-            tl[e] = pack_bf16x2(u0 - bf16_bits_to_f32((uint16_t)th[e]), u1 - bf16_bits_to_f32((uint16_t)(th[e] >> 16)));
-          }
-          uint4 tw;
-          tw.x = pack_bf16x2(x[8 * q + 0] * wc, x[8 * q + 1] * wc);
-          tw.y = pack_bf16x2(x[8 * q + 2] * wc, x[8 * q + 3] * wc);
-          tw.z = pack_bf16x2(x[8 * q + 4] * wc, x[8 * q + 5] * wc);
-          tw.w = pack_bf16x2(x[8 * q + 6] * wc, x[8 * q + 7] * wc);
-          lds_st16(Tu + (col * kTP + 8 * q) * 2, make_uint4(th[0], th[1], th[2], th[3]));
-          lds_st16(Tu + CF::SZ_TT + (col * kTP + 8 * q) * 2, make_uint4(tl[0], tl[1], tl[2], tl[3]));
-          lds_st16(Tw + (col * kTP + 8 * q) * 2, tw);
+        for (int e = 0; e < 4; ++e) {
+          const float u0 = x[8 * q + 2 * e] * bc, u1 = x[8 * q + 2 * e + 1] * bc;
+          th[e] = pack_bf16x2(u0, u1);
+          tl[e] = pack_bf16x2(u0 - bf16_bits_to_f32((uint16_t)th[e]), u1 - __uint_as_float(th[e] & 0xffff0000u));
         }
+        uint4 tw;
+        tw.x = pack_bf16x2(x[8 * q + 0] * wc, x[8 * q + 1] * wc);
+        tw.y = pack_bf16x2(x[8 * q + 2] * wc, x[8 * q + 3] * wc);
+        tw.z = pack_bf16x2(x[8 * q + 4] * wc, x[8 * q + 5] * wc);
+        tw.w = pack_bf16x2(x[8 * q + 6] * wc, x[8 * q + 7] * wc);
+        lds_st16(Tu + (col * kTP + 8 * q) * 2, make_uint4(th[0], th[1], th[2], th[3]));
+        lds_st16(Tu + CF::SZ_TT + (col * kTP + 8 * q) * 2, make_uint4(tl[0], tl[1], tl[2], tl[3]));
+        lds_st16(Tw + (col * kTP + 8 * q) * 2, tw);
       }
-      __builtin_amdgcn_s_waitcnt(0xc07f);
-      const lchar* Kc = kbuf(m);
-      lchar* Wc = wbuf(m);
+    };
+    // phases 7 and 0: W^T = K^T Tw^T for sub-chunk m + c: lane (li, g) of
+    // tile (td, bi) ends with W[16 bi + li][16 td + 4g ..], stored negated
+    // (the state subtracts W M0) as an 8-byte row-major store
+    auto make_w = [&](int mc, int c) {
+      const lchar* Tw = priv + c * CF::SZ_TT;
+      const lchar* Kc = kbuf(mc);
+      lchar* Wc = wbuf(mc);
+      // every read first: the compiler cannot move them above the W stores
       const bf16x8 tw0 = tr_pair(Tw + tr_t, kTP * 2, false);
       const bf16x8 tw1 = tr_pair(Tw + tr_t + 16 * 2, kTP * 2, false);
+      bf16x8 kt[NT];
 #pragma unroll
-      for (int td = 0; td < NT; ++td) {
-        const bf16x8 kt = tr_pair(Kc + tr_kv + 16 * td * 2, KP * 2, false);
-        const f32x4 w0 = mma_k32(zero4(), kt, tw0);
-        const f32x4 w1 = mma_k32(zero4(), kt, tw1);
-        lds_st8(Wc + w_row + 16 * td * 2, make_uint2(pack_bf16x2(-w0[0], -w0[1]), pack_bf16x2(-w0[2], -w0[3])));
-        lds_st8(Wc + w_row + (16 * WP + 16 * td) * 2, make_uint2(pack_bf16x2(-w1[0], -w1[1]), pack_bf16x2(-w1[2], -w1[3])));
+      for (int td = 0; td < NT; ++td) kt[td] = tr_kv(Kc, td);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int h = 0; h < NT; h += 4) {
+        f32x4 w0[4], w1[4];
+#pragma unroll
+        for (int e = 0; e < 4 && h + e < NT; ++e) {
+          w0[e] = mma_k32(zero4(), kt[h + e], tw0);
+          w1[e] = mma_k32(zero4(), kt[h + e], tw1);
+        }
+#pragma unroll
+        for (int e = 0; e < 4 && h + e < NT; ++e) {
+          const int td = h + e;
+          lds_st8(Wc + w_row + 16 * td * 2, make_uint2(pack_bf16x2(-w0[e][0], -w0[e][1]), pack_bf16x2(-w0[e][2], -w0[e][3])));
+          lds_st8(Wc + w_row + (16 * WP + 16 * td) * 2, make_uint2(pack_bf16x2(-w1[e][0], -w1[e][1]), pack_bf16x2(-w1[e][2], -w1[e][3])));
+        }
       }
     };
 
-    // after the barrier that publishes K(0): steps -4 .. nsc-1, one barrier
-    // each; this wave runs sub-chunks
-    // m = p, p + 4, ... in steps m-4 .. m-1
-    lds_barrier();                                       // K(0) is in place
-    int n = -4;
-    for (; n < p - 4; ++n) lds_barrier();
-    float gv, bv, gv_nx, bv_nx;
-    load_gb(p, gv, bv);
-    for (int m = p; m < nsc; m += 4) {
-      load_gb(m + 4, gv_nx, bv_nx);
-      seg_a(m, gv, bv);
+    // steps -8 .. nsc-1, one barrier each: pair m runs phase s at step
+    // m - 8 + s, and phase 0 also finishes the previous pair
+    int n = -8;
+    for (; n < 2 * p - 8 && n < nsc; ++n) lds_barrier();
+    int m = 2 * p;
+    if (m < nsc) issue_loads(m);
+    for (; m < nsc; m += 8) {
+      if (m >= 8) make_w(m - 7, 1);            // m - 7 < nsc: the previous pair's second sub-chunk
       lds_barrier();
-      int cl = col;
-      asm volatile("" : "+v"(cl));
-#pragma unroll
-      for (int i = 0; i < kS; ++i) x[i] = (i == cl) ? 1.f : 0.f;
-      solve(std::integral_constant<int, 0>{}, std::integral_constant<int, CF::QS>{});
+      gram(m);
       lds_barrier();
-      solve(std::integral_constant<int, CF::QS>{}, std::integral_constant<int, kS>{});
+      make_a();
+      load_col(0, cb[0]);                      // the solve's first columns (same wave: after the A stores)
+      load_col(1, cb[1]);
       lds_barrier();
-      seg_d(m);
+      solve();                                 // phases 3, 4 and 5 (two barriers inside)
       lds_barrier();
-      gv = gv_nx;
-      bv = bv_nx;
-      n += 4;
+      pack(m);
+      lds_barrier();
+      make_w(m, 0);
+      if (m + 8 < nsc) issue_loads(m + 8);     // two steps before its Gram
+      lds_barrier();
+      n += 8;
+    }
+    if (m >= 8 && m - 7 < nsc) {                 // the last pair's second sub-chunk, at step m - 8
+      make_w(m - 7, 1);
+      lds_barrier();
+      ++n;
     }
     for (; n < nsc; ++n) lds_barrier();
     return;
@@ -393,26 +487,28 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int sw = wid - NP;
   const int stid = tid - 64 * NP;
   f32x4 M[NT][2];
-  uint4 pk[CF::PER_S], pv[CF::PER_S];
 
-  // rows of sub-chunk m as 16-byte pieces (zero past the segment end)
-  auto load_rows = [&](const char* plane, int m, uint4* dst) {
+  // DMA staging of K and V: this wave moves blocks DMA_PER sw .. + DMA_PER - 1
+  // (1 KB each) of a sub-chunk; lane l carries the 16 bytes at byte 16 l of
+  // its block, i.e. row dma_row[i] and logical columns dma_col[i] .. + 7 of
+  // the swizzled layout.  Rows past the segment end are read from its last
+  // row: their beta and log decay are 0, so T has unit rows and zero columns
+  // there and any finite values are multiplied by exact zeros.
+  int dma_row[CF::DMA_PER], dma_col[CF::DMA_PER];
+#pragma unroll
+  for (int i = 0; i < CF::DMA_PER; ++i) {
+    const int byte = (CF::DMA_PER * sw + i) * 1024 + 16 * lane;
+    const int r = byte / (2 * D), pos = byte % (2 * D);
+    const int cb = (pos / 32) ^ ((r / CF::RPL) % CF::NCP);
+    dma_row[i] = r;
+    dma_col[i] = 16 * cb + 8 * ((pos / 16) & 1);
+  }
+  auto stage = [&](const char* plane, int m, lchar* buf) {
     const int64_t c0 = s0 + (int64_t)m * kS;
 #pragma unroll
-    for (int i = 0; i < CF::PER_S; ++i) {
-      const int q = stid + i * 64 * NSW;
-      const int row = q / CF::PPR, cc = q % CF::PPR;
-      const int64_t t = c0 + row;
-      dst[i] = (m >= 0 && m < nsc && t < s1) ? *reinterpret_cast<const uint4*>(plane + (t * D + cc * 8) * 2)
-                                             : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store_rows = [&](lchar* buf, const uint4* src) {
-#pragma unroll
-    for (int i = 0; i < CF::PER_S; ++i) {
-      const int q = stid + i * 64 * NSW;
-      const int row = q / CF::PPR, cc = q % CF::PPR;
-      lds_st16(buf + (row * KP + cc * 8) * 2, src[i]);
+    for (int i = 0; i < CF::DMA_PER; ++i) {
+      const int64_t t = c0 + dma_row[i] < s1 ? c0 + dma_row[i] : s1 - 1;
+      dma16(plane + (t * D + dma_col[i]) * 2, (uint32_t)(uintptr_t)buf + (CF::DMA_PER * sw + i) * 1024);
     }
   };
 
@@ -431,7 +527,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     const bf16x8 t1l = tr_pair(Tu + CF::SZ_TT + tr_t + 16 * 2, kTP * 2, false);
     bf16x8 vf[2], wf[NT / 2][2], kt[NT];
 #pragma unroll
-    for (int cc = 0; cc < 2; ++cc) vf[cc] = tr_pair(Vc + tr_kv + (32 * sw + 16 * cc) * 2, KP * 2, false);
+    for (int cc = 0; cc < 2; ++cc) vf[cc] = tr_kv(Vc, 2 * sw + cc);
 #pragma unroll
     for (int q = 0; q < NT / 2; ++q)
 #pragma unroll
@@ -439,11 +535,11 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
         const lchar* wr = Wc + w_row + (16 * bi * WP + 32 * q) * 2;
         wf[q][bi] = join(lds_ld8(wr), lds_ld8(wr + 16 * 2), false);
       }
-    const float4 e0 = lds_ldf4((const lchar*)(vec + kS + 4 * g));
-    const float4 e1 = lds_ldf4((const lchar*)(vec + kS + 16 + 4 * g));
-    const float decay = vec[kS - 1];
+    const float4 e0 = lds_ldf4((const lchar*)(vec + 4 * g));
+    const float4 e1 = lds_ldf4((const lchar*)(vec + 16 + 4 * g));
+    const float decay = vec[kS];
 #pragma unroll
-    for (int td = 0; td < NT; ++td) kt[td] = tr_pair(Kc + tr_kv + 16 * td * 2, KP * 2, false);
+    for (int td = 0; td < NT; ++td) kt[td] = tr_kv(Kc, td);
     __builtin_amdgcn_sched_barrier(0);
     // U = Tu V for row halves bi and column tiles cc; Delta = U + (-W) M0,
     // W rows read in the state's k order
@@ -481,10 +577,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       }
   };
 
-  // ---- prologue: K(0) resident, K(1) and the state in registers
-  load_rows(Kplane, 0, pk);
-  store_rows(kbuf(0), pk);
-  load_rows(Kplane, 1, pk);
+  // ---- prologue: the state in registers
 #pragma unroll
   for (int td = 0; td < NT; ++td)
 #pragma unroll
@@ -497,17 +590,18 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       }
     }
 
-  lds_barrier();                    // publishes K(0) to the prep waves
-
-  // ---- steps -4 .. nsc-1: the state lines of sub-chunk n; K(n+5) and
-  // V(n+1) go to their slots from registers loaded a step earlier
-  // (the staging goes first so its LDS writes and loads overlap the step)
-  for (int n = -4; n < nsc; ++n) {
-    if (n + 5 < nsc) store_rows(kbuf(n + 5), pk);
-    load_rows(Kplane, n + 6, pk);
-    if (n + 1 >= 0 && n + 1 < nsc) store_rows(vbuf(n + 1), pv);
-    load_rows(Vplane, n + 2, pv);
+  // ---- steps -8 .. nsc-1: the state lines of sub-chunk n.  K(n+3) and
+  // V(n+2) are requested here and waited for at the end of the next step,
+  // before the barrier that publishes them (K(j) is read from step j-1 on,
+  // V(j) at step j)
+  for (int n = -8; n < nsc; ++n) {
+    const bool k_dma = n + 3 >= 0 && n + 3 < nsc, v_dma = n + 2 >= 0 && n + 2 < nsc;
+    if (k_dma) stage(Kplane, n + 3, kbuf(n + 3));
+    if (v_dma) stage(Vplane, n + 2, vbuf(n + 2));
     if (n >= 0) state_step(n);
+    if (k_dma && v_dma) wait_vm<2 * CF::DMA_PER>();
+    else if (k_dma || v_dma) wait_vm<CF::DMA_PER>();
+    else wait_vm<0>();
     lds_barrier();
   }
 

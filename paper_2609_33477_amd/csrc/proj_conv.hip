@@ -81,22 +81,6 @@ template <typename TB> struct BT;
 template <> struct BT<bf16_t> { static constexpr int ROW = 64, BLKS = 2, NS = 5; };
 template <> struct BT<fp8_t> { static constexpr int ROW = 32, BLKS = 1, NS = 6; };
 
-// 16 bytes per lane, global -> LDS at lds_base + 16 * lane (wave-uniform
-// base).  Inline asm: the compiler would otherwise wait for every such load
-// before any later LDS read; completion is tracked by hand (wait_vm) before
-// the barrier that publishes a stage.
-// `lds_off` must be wave-uniform (it is an SGPR operand).
-__device__ __forceinline__ void dma16(const void* src, uint32_t lds_off) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_off), "v"(src) : "memory", "m0");
-}
-
-// s_waitcnt vmcnt(N) with lgkmcnt and expcnt left at their maxima
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N < 64, "vmcnt");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 // 16-byte chunk swizzles inside a 64-byte LDS row.  A fragment read is
 // serviced 16 lanes at a time; rows r and r + 4 share a bank quarter, so the
 // 4 rows of each quarter a 16-lane group reads must sit in distinct chunks
