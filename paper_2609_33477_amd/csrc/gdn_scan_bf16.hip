@@ -213,7 +213,13 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int tr_h = li & 3;
   const int tr_t = ((li >> 2) * kTP + 4 * (li & 3) + 4 * g * kTP) * 2; // transposed reads of T^T, rows 4g + ..
 
-  const int u = blockIdx.x;
+  // Blocks are dealt to the 8 XCDs round-robin; within each full group of
+  // 16 blocks, blocks r and r + 8 (same XCD, dispatched together) take
+  // consecutive units, i.e. value heads 2k and 2k + 1, which share a key
+  // head when H_v = 2 H_k, so its K rows are fetched into one L2.
+  const int units = a.n_seg * a.n_layers * a.H_v;
+  int u = blockIdx.x;
+  if ((u | 15) < units) u = (u & ~15) + 2 * (u & 7) + ((u >> 3) & 1);
   const int head = u % a.H_v;
   const int layer = (u / a.H_v) % a.n_layers;
   const int rank = u / (a.H_v * a.n_layers);
