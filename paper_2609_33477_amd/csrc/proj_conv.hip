@@ -26,8 +26,10 @@
 // Anchors are the MFMA's first operand and their rows are fed in the order
 // that leaves each lane's accumulators holding 32 consecutive rows of one
 // column (tok_row).
-// Tiles are dealt in contiguous runs per XCD and walked in groups of 8
-// M-tiles so concurrently running tiles share A and B panels in L2.  In a
+// Tiles are dealt in contiguous runs per XCD and walked in pairs of M-tiles
+// (N-tiles fastest), so the 32 tiles an XCD runs at once span about 2
+// anchor panels and 16 weight panels, each fetched into its L2 once for
+// many tiles (of group sizes 1 to 32, 2 measured fastest).  In a
 // narrow last N-tile (the 2 H_v gate columns) waves skip the MFMAs and
 // fragment reads of columns past N.
 //
@@ -140,13 +142,13 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 // hardware block id -> (m tile, n tile): contiguous runs per XCD (blocks are
-// dealt round-robin to the 8 XCDs), then groups of 8 m-tiles walked n-major
+// dealt round-robin to the 8 XCDs), then pairs of m-tiles walked n-major
 __device__ __forceinline__ void tile_of(int b, int tm, int tn, int& mt, int& nt) {
   const int nb = tm * tn;
   const int per = nb / 8, rem = nb % 8;
   const int x = b % 8, loc = b / 8;
   const int t = x * per + (x < rem ? x : rem) + loc;
-  constexpr int GM = 8;
+  constexpr int GM = 2;
   const int grp = t / (GM * tn);
   const int first = grp * GM;
   const int gs = (tm - first) < GM ? (tm - first) : GM;
