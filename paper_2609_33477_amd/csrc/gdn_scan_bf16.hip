@@ -10,20 +10,21 @@
 // Only the last two lines touch the state.  The workgroup runs a pipeline
 // with one barrier per sub-chunk step:
 //   4 prep waves: wave p builds everything but the state lines for the
-//     sub-chunk pairs (m, m+1), m = 2p (mod 8), over the 8 steps before the
-//     state needs them, lanes 0-31 serving sub-chunk m and lanes 32-63
-//     sub-chunk m+1 wherever the work is one lane per row or column:
-//     K rows for the Gram blocks straight from global memory (issued two
-//     steps ahead); log2-alpha prefix and Gram blocks on MFMA (step m-7); A
-//     (m-6); T = (I + A)^{-1} by a 32-step forward substitution in fp32,
-//     lane = column of T, spread over steps m-5 .. m-3; Tu = T diag(beta)
-//     in two bf16 parts and Tw = T diag(beta 2^G) (m-2); then
-//     W^T = K^T Tw^T, which leaves W row-major (m-1 for sub-chunk m, m for
-//     m+1);
+//     sub-chunk pairs (m, m+1), m = 2p (mod 8), over the 8 steps m-9 .. m-2,
+//     lanes 0-31 serving sub-chunk m and lanes 32-63 sub-chunk m+1 wherever
+//     the work is one lane per row or column: K rows for the Gram blocks
+//     straight from global memory (issued two steps ahead); log2-alpha
+//     prefix and Gram blocks on MFMA (step m-8); A (m-7); T = (I + A)^{-1}
+//     by a 32-step forward substitution in fp32, lane = column of T, spread
+//     over steps m-6 .. m-4; Tu = T diag(beta) in two bf16 parts and
+//     Tw = T diag(beta 2^G) (m-3); then W^T = K^T Tw^T, which leaves W
+//     row-major (m-2 for sub-chunk m, m-1 for m+1);
 //   d/32 state waves, wave s owning state columns [32s, 32s+32) as 2 d/16
 //     16x16 fp32 accumulator tiles for the whole segment: at step n they
-//     run the state lines of sub-chunk n, and they request K(n+3) and V(n+2)
-//     by global -> LDS DMA, waited for one step later.
+//     run the state lines of sub-chunk n from registers, then read the
+//     operands of sub-chunk n+1, so the reads' latency overlaps the MFMAs
+//     and the barrier; they request K(n+4) and V(n+3) by global -> LDS
+//     DMA, waited for one step later.
 // Rings (sub-chunk slots): K 4, V 3, W 2, Tu 4, gate vectors 16.
 //
 // Every product is v_mfma_f32_16x16x32_bf16.  A 32-wide reduction over
@@ -35,12 +36,13 @@
 // 16-lane group rows kbase..kbase+3 of column n0 + i when lane j of the group
 // addresses row kbase + j/4, columns n0 + 4 (j%4) .. +3.
 //
-// LDS (d = 128): K and V rings 56 KB, W ring 19 KB, Tu ring 24 KB, gate
+// LDS (d = 128): K and V rings 56 KB, W ring 18 KB, Tu ring 24 KB, gate
 // vectors 4 KB, per prep wave A^T of a pair (reused for Tw^T) and gate
 // scratch 38 KB: ~141 KB, one workgroup (8 waves) per CU.  K and V rows are
 // unpadded and XOR-swizzled (kv_off) so the DMA writes whole 1 KB blocks;
-// the other pitches are the measured conflict-free ones: 8 mod 64 dwords for
-// transposed reads, 2 mod 8 dwords for 8-byte row reads and writes.
+// W rows hold their columns in the state's k order (32q + 4g .. + 3, then
+// 32q + 16 + 4g .. + 3, at 32q + 8g) so each fragment is one 16-byte read,
+// with the row pitch 8 mod 64 dwords measured conflict free for those.
 #include "sr_device.hpp"
 
 #include <cstddef>
@@ -138,9 +140,9 @@ struct Cfg {
   static constexpr int NCP = D / 16;                  // 32-byte chunk pairs per row
   static constexpr int DMA_ROWS = 512 / D;            // rows per 1 KB DMA block
   static constexpr int DMA_PER = kS * 2 * D / 1024 / NSW;   // DMA blocks per state wave and matrix
-  static constexpr int WP = D + 20;                   // W row pitch (bf16)
-  static constexpr int NK = 4;                        // K ring: K(n) DMA issued at step n-3
-  static constexpr int NV = 3;                        // V ring: V(n) DMA issued at step n-2
+  static constexpr int WP = D + 16;                   // W row pitch (bf16): 16-byte row reads
+  static constexpr int NK = 4;                        // K ring: K(n) DMA issued at step n-4
+  static constexpr int NV = 3;                        // V ring: V(n) DMA issued at step n-3
   static constexpr int NTU = 4;                       // Tu ring: a pair is packed two steps ahead
   static constexpr int NVEC = 16;                     // gate-vector ring: written nine steps ahead
   static constexpr int SZ_KV = kS * D * 2;            // one sub-chunk of K or V
@@ -208,7 +210,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, li = lane & 15;
   // per-lane byte offsets; everything else is a compile-time immediate
-  const int w_row = (li * WP + 4 * g) * 2;                            // 8-byte row reads / writes of W
+  const int w_row = (li * WP + 8 * g) * 2;                            // W rows: 8-byte writes, 16-byte reads
   const int tr_row = 4 * g + (li >> 2);                              // transposed reads of K / V: row, 8-byte piece
   const int tr_h = li & 3;
   const int tr_t = ((li >> 2) * kTP + 4 * (li & 3) + 4 * g * kTP) * 2; // transposed reads of T^T, rows 4g + ..
@@ -273,26 +275,34 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     f32x4 gr[2][3];        // Gram tiles (0,0), (1,0), (1,1) of each sub-chunk
     float x[kS];           // column `col` of T, carried over the solve phases
 
-    // phase 7 of the previous pair: the pair's K rows straight from global memory
-    // as Gram fragments, and this lane's log2 alpha and beta (rows past the
-    // segment end carry 0 and 0, which makes them inert)
+    // phase 7 of the previous pair: the pair's K rows straight from global
+    // memory as Gram fragments, and this lane's log2 alpha and beta.  Rows
+    // past the segment end carry log2 alpha 0 and beta 0, which makes them
+    // inert: their K rows are read from the segment's last row (any finite
+    // values do, they only meet beta = 0), so every load is unconditional.
     auto issue_loads = [&](int m) {
 #pragma unroll
       for (int c = 0; c < 2; ++c)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int64_t t = s0 + (int64_t)(m + c) * kS + 16 * h + li;
+          const char* rp = Kplane + ((t < s1 ? t : s1 - 1) * D + 8 * g) * 2;
 #pragma unroll
-          for (int q = 0; q < QG; ++q)
-            kf[c][q][h] = t < s1 ? *reinterpret_cast<const bf16x8*>(Kplane + (t * D + 32 * q + 8 * g) * 2)
-                                 : as_bf16x8(make_uint4(0, 0, 0, 0));
+          for (int q = 0; q < QG; ++q) kf[c][q][h] = *reinterpret_cast<const bf16x8*>(rp + 64 * q);
         }
+      // raw values of the row (clamped); zeroed past the end in the Gram
+      // phase, where they are first used, so nothing here waits for them
       const int64_t t = s0 + (int64_t)(m + hc) * kS + col;
-      gv = t < s1 ? Gp[t] : 0.f;
-      bv = t < s1 ? Bp[t] : 0.f;
+      const int64_t tc = t < s1 ? t : s1 - 1;
+      gv = Gp[tc];
+      bv = Bp[tc];
     };
     // phase 1: prefix of log2 alpha inside each half, gate vectors, Gram
     auto gram = [&](int m) {
+      if (s0 + (int64_t)(m + hc) * kS + col >= s1) {
+        gv = 0.f;
+        bv = 0.f;
+      }
       float gp = gv;
       gp += dpp_row_shr<1>(gp);
       gp += dpp_row_shr<2>(gp);
@@ -449,16 +459,17 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
 #pragma unroll
         for (int e = 0; e < 4 && h + e < NT; ++e) {
           const int td = h + e;
-          lds_st8(Wc + w_row + 16 * td * 2, make_uint2(pack_bf16x2(-w0[e][0], -w0[e][1]), pack_bf16x2(-w0[e][2], -w0[e][3])));
-          lds_st8(Wc + w_row + (16 * WP + 16 * td) * 2, make_uint2(pack_bf16x2(-w1[e][0], -w1[e][1]), pack_bf16x2(-w1[e][2], -w1[e][3])));
+          const int pos = 32 * (td >> 1) + 4 * (td & 1);   // column 16 td + 4g .. stored at 32 (td/2) + 8g + 4 (td%2)
+          lds_st8(Wc + w_row + pos * 2, make_uint2(pack_bf16x2(-w0[e][0], -w0[e][1]), pack_bf16x2(-w0[e][2], -w0[e][3])));
+          lds_st8(Wc + w_row + (16 * WP + pos) * 2, make_uint2(pack_bf16x2(-w1[e][0], -w1[e][1]), pack_bf16x2(-w1[e][2], -w1[e][3])));
         }
       }
     };
 
-    // steps -8 .. nsc-1, one barrier each: pair m runs phase s at step
-    // m - 8 + s, and phase 0 also finishes the previous pair
-    int n = -8;
-    for (; n < 2 * p - 8 && n < nsc; ++n) lds_barrier();
+    // steps -9 .. nsc-1, one barrier each: pair m runs phase s at step
+    // m - 9 + s, and phase 0 also finishes the previous pair
+    int n = -9;
+    for (; n < 2 * p - 9 && n < nsc; ++n) lds_barrier();
     int m = 2 * p;
     if (m < nsc) issue_loads(m);
     for (; m < nsc; m += 8) {
@@ -479,7 +490,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       lds_barrier();
       n += 8;
     }
-    if (m >= 8 && m - 7 < nsc) {                 // the last pair's second sub-chunk, at step m - 8
+    if (m >= 8 && m - 7 < nsc) {                 // the last pair's second sub-chunk, at step m - 9
       make_w(m - 7, 1);
       lds_barrier();
       ++n;
@@ -518,37 +529,39 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     }
   };
 
-  // the state lines of sub-chunk m for this wave's 32 columns.  Every LDS
-  // read of the step is issued first, so their latencies overlap instead of
-  // each one stalling the MFMA that needs it.
-  auto state_step = [&](int m) {
+  // The operands of a state step, read one step ahead: during step n the
+  // wave issues the MFMAs of sub-chunk n from registers, then reads
+  // sub-chunk n+1's operands, whose latency overlaps those MFMAs and the
+  // barrier.
+  bf16x8 t0, t1, t0l, t1l, vf[2], wf[NT / 2][2], kt[NT];
+  float4 e0, e1;
+  float decay;
+  auto load_ops = [&](int m) {
     const lchar* Kc = kbuf(m);
     const lchar* Vc = vbuf(m);
     const lchar* Wc = wbuf(m);
     const lchar* Tu = tubuf(m);
     const SR_LDS float* vec = vecbuf(m);
-    const bf16x8 t0 = tr_pair(Tu + tr_t, kTP * 2, false);
-    const bf16x8 t1 = tr_pair(Tu + tr_t + 16 * 2, kTP * 2, false);
-    const bf16x8 t0l = tr_pair(Tu + CF::SZ_TT + tr_t, kTP * 2, false);
-    const bf16x8 t1l = tr_pair(Tu + CF::SZ_TT + tr_t + 16 * 2, kTP * 2, false);
-    bf16x8 vf[2], wf[NT / 2][2], kt[NT];
+    t0 = tr_pair(Tu + tr_t, kTP * 2, false);
+    t1 = tr_pair(Tu + tr_t + 16 * 2, kTP * 2, false);
+    t0l = tr_pair(Tu + CF::SZ_TT + tr_t, kTP * 2, false);
+    t1l = tr_pair(Tu + CF::SZ_TT + tr_t + 16 * 2, kTP * 2, false);
 #pragma unroll
     for (int cc = 0; cc < 2; ++cc) vf[cc] = tr_kv(Vc, 2 * sw + cc);
+    // W rows 16 bi + li in the state's k order (stored that way)
 #pragma unroll
     for (int q = 0; q < NT / 2; ++q)
 #pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-        const lchar* wr = Wc + w_row + (16 * bi * WP + 32 * q) * 2;
-        wf[q][bi] = join(lds_ld8(wr), lds_ld8(wr + 16 * 2), false);
-      }
-    const float4 e0 = lds_ldf4((const lchar*)(vec + 4 * g));
-    const float4 e1 = lds_ldf4((const lchar*)(vec + 16 + 4 * g));
-    const float decay = vec[kS];
+      for (int bi = 0; bi < 2; ++bi) wf[q][bi] = as_bf16x8(lds_ld16(Wc + w_row + (16 * bi * WP + 32 * q) * 2));
+    e0 = lds_ldf4((const lchar*)(vec + 4 * g));
+    e1 = lds_ldf4((const lchar*)(vec + 16 + 4 * g));
+    decay = vec[kS];
 #pragma unroll
     for (int td = 0; td < NT; ++td) kt[td] = tr_kv(Kc, td);
-    __builtin_amdgcn_sched_barrier(0);
-    // U = Tu V for row halves bi and column tiles cc; Delta = U + (-W) M0,
-    // W rows read in the state's k order
+  };
+  // the state lines of a sub-chunk for this wave's 32 columns
+  auto state_step = [&]() {
+    // U = Tu V for row halves bi and column tiles cc; Delta = U + (-W) M0
     f32x4 dl[2][2];
 #pragma unroll
     for (int cc = 0; cc < 2; ++cc) {
@@ -595,16 +608,21 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
           M[td][cc][r] = st_in[state_base + (size_t)(16 * td + 4 * g + r) * D + 32 * sw + 16 * cc + li];
       }
     }
+  // The initial state has landed before the first DMA is issued: the
+  // compiler does not count the DMAs, so a wait for these loads placed inside
+  // the loop would be vmcnt(0) and stall every step on the DMAs in flight.
+  wait_vm<0>();
 
-  // ---- steps -8 .. nsc-1: the state lines of sub-chunk n.  K(n+3) and
-  // V(n+2) are requested here and waited for at the end of the next step,
-  // before the barrier that publishes them (K(j) is read from step j-1 on,
-  // V(j) at step j)
-  for (int n = -8; n < nsc; ++n) {
-    const bool k_dma = n + 3 >= 0 && n + 3 < nsc, v_dma = n + 2 >= 0 && n + 2 < nsc;
-    if (k_dma) stage(Kplane, n + 3, kbuf(n + 3));
-    if (v_dma) stage(Vplane, n + 2, vbuf(n + 2));
-    if (n >= 0) state_step(n);
+  // ---- steps -9 .. nsc-1: the state lines of sub-chunk n, then the reads
+  // of sub-chunk n+1's operands.  K(n+4) and V(n+3) are requested here and
+  // waited for at the end of the next step, before the barrier that
+  // publishes them (K(j) is read from step j-2 on, V(j) at step j-1)
+  for (int n = -9; n < nsc; ++n) {
+    const bool k_dma = n + 4 >= 0 && n + 4 < nsc, v_dma = n + 3 >= 0 && n + 3 < nsc;
+    if (k_dma) stage(Kplane, n + 4, kbuf(n + 4));
+    if (v_dma) stage(Vplane, n + 3, vbuf(n + 3));
+    if (n >= 0) state_step();
+    if (n + 1 >= 0 && n + 1 < nsc) load_ops(n + 1);
     if (k_dma && v_dma) wait_vm<2 * CF::DMA_PER>();
     else if (k_dma || v_dma) wait_vm<CF::DMA_PER>();
     else wait_vm<0>();
