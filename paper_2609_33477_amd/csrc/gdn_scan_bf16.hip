@@ -260,8 +260,8 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   if (wid < NP) {
     // ================================================================ prep
     // Wave p prepares the sub-chunk pairs (m, m + 1), m = 2p (mod 8), each
-    // over the eight steps m-8 .. m-1 (phase s at step m-8+s) plus W(m+1)
-    // at step m.  Lanes 0-31 work on sub-chunk m, lanes 32-63 on m + 1 where
+    // over the eight steps m-9 .. m-2 (phase s at step m-9+s) plus W(m+1)
+    // at step m-1.  Lanes 0-31 work on sub-chunk m, lanes 32-63 on m + 1 where
     // the work is one lane per row or column (prefix, solve, packing).
     const int p = wid;
     lchar* priv = L + CF::OFF_PRIV + p * CF::SZ_PRIV;
