@@ -520,12 +520,25 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     dma_row[i] = r;
     dma_col[i] = 16 * cb + 8 * ((pos / 16) & 1);
   }
+  // the sub-chunk's first row is a wave-uniform base; each lane adds its
+  // fixed byte offset, clamped to the last row only in a partial sub-chunk
+  uint32_t dma_off[CF::DMA_PER];
+#pragma unroll
+  for (int i = 0; i < CF::DMA_PER; ++i) dma_off[i] = (uint32_t)((dma_row[i] * D + dma_col[i]) * 2);
   auto stage = [&](const char* plane, int m, lchar* buf) {
     const int64_t c0 = s0 + (int64_t)m * kS;
+    const char* base = plane + c0 * D * 2;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)buf + CF::DMA_PER * sw * 1024;
+    if (c0 + kS <= s1) {
 #pragma unroll
-    for (int i = 0; i < CF::DMA_PER; ++i) {
-      const int64_t t = c0 + dma_row[i] < s1 ? c0 + dma_row[i] : s1 - 1;
-      dma16(plane + (t * D + dma_col[i]) * 2, (uint32_t)(uintptr_t)buf + (CF::DMA_PER * sw + i) * 1024);
+      for (int i = 0; i < CF::DMA_PER; ++i) dma16_s(base, dma_off[i], lds0 + i * 1024);
+    } else {
+      const int last = (int)(s1 - 1 - c0);
+#pragma unroll
+      for (int i = 0; i < CF::DMA_PER; ++i) {
+        const int r = dma_row[i] < last ? dma_row[i] : last;
+        dma16_s(base, (uint32_t)((r * D + dma_col[i]) * 2), lds0 + i * 1024);
+      }
     }
   };
 

@@ -132,6 +132,14 @@ __device__ __forceinline__ void dma16(const void* src, uint32_t lds_off) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_off), "v"(src) : "memory", "m0");
 }
 
+// The same with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane
+// byte offset (the instruction's saddr form): no 64-bit address arithmetic
+// per lane.
+__device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_off), "v"(voff), "s"(sbase)
+               : "memory", "m0");
+}
+
 // s_waitcnt vmcnt(N) with lgkmcnt and expcnt left at their maxima
 template <int N>
 __device__ __forceinline__ void wait_vm() {
