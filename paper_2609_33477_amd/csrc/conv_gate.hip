@@ -19,7 +19,8 @@
 // k and v.
 //   tail_q_mfma_kernel (bf16 anchors): one small GEMM over the gathered tail
 //     rows of all segments x the q channels, on v_mfma_f32_32x32x16_bf16
-//     (32 x 32 outputs per block, reduction split over its 4 waves).
+//     (32 x 32 outputs per block, reduction split over its 8 waves, whose
+//     loads are all independent: the kernel is bound by memory latency).
 //   tail_kernel (fp32 anchors): per (segment, 64 channels) dot products.
 #include "sr_device.hpp"
 
@@ -297,9 +298,11 @@ __device__ __forceinline__ int64_t tail_row(const TailArgs& a, int r, int* slot,
 
 // Block: 32 tail rows x 32 q channels; the 4 waves split the reduction over
 // d_model in quarters and combine their accumulators through LDS.
+constexpr int kTailQWaves = 8;
+
 template <typename TW, typename TT>
-__global__ __launch_bounds__(256) void tail_q_mfma_kernel(TailArgs a) {
-  __shared__ float part[3][16][64];
+__global__ __launch_bounds__(64 * kTailQWaves) void tail_q_mfma_kernel(TailArgs a) {
+  __shared__ float part[kTailQWaves - 1][16][64];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int R = a.n_seg * (a.w - 1);
   const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
@@ -309,10 +312,13 @@ __global__ __launch_bounds__(256) void tail_q_mfma_kernel(TailArgs a) {
   const int c = min(c0 + (lane & 31), a.c_q - 1);
   const uint16_t* xa = static_cast<const uint16_t*>(a.anchors) + (t >= 0 ? t : 0) * a.D;
   const int64_t wrow = (int64_t)c * a.D;
-  const int kq = a.D / 4;                       // d_model is a multiple of 64
+  // 16-wide k-steps (d_model is a multiple of 64), split evenly over the waves
+  const int ksteps = a.D / 16;
+  const int k_lo = wid * ksteps / kTailQWaves, k_hi = (wid + 1) * ksteps / kTailQWaves;
   f32x16 acc = zero16();
-#pragma unroll 8
-  for (int k = wid * kq + 8 * (lane >> 5); k < (wid + 1) * kq; k += 16) {
+#pragma unroll 10
+  for (int ks = k_lo; ks < k_hi; ++ks) {
+    const int k = 16 * ks + 8 * (lane >> 5);
     const bf16x8 av = as_bf16x8(*reinterpret_cast<const uint4*>(xa + k));
     const bf16x8 bv = load_w8<TW>(a.w_q, wrow + k);
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
@@ -324,7 +330,9 @@ __global__ __launch_bounds__(256) void tail_q_mfma_kernel(TailArgs a) {
   __syncthreads();
   if (wid > 0) return;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] += part[0][i][lane] + part[1][i][lane] + part[2][i][lane];
+  for (int w = 0; w < kTailQWaves - 1; ++w)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] += part[w][i][lane];
   const int col = c0 + (lane & 31);
   if (col >= a.c_q) return;
   const float scale = std::is_same<TW, fp8_t>::value ? Elem<bf16_t>::load(a.s_q, col) : 1.f;
@@ -363,7 +371,7 @@ hipError_t run_tail(const TailArgs& a, hipStream_t s) {
     if (a.c_q == 0) return hipSuccess;
     const int R = a.n_seg * (a.w - 1);
     dim3 grid((a.c_q + 31) / 32, (R + 31) / 32);
-    hipLaunchKernelGGL((tail_q_mfma_kernel<TW, TT>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((tail_q_mfma_kernel<TW, TT>), grid, dim3(64 * kTailQWaves), 0, s, a);
     return hipGetLastError();
   } else {
     dim3 grid(a.n_seg, (a.c_tail + kTailChannels - 1) / kTailChannels);
