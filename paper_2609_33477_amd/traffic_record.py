@@ -42,9 +42,8 @@ def per_dispatch_kib(path, fragment):
     return sum(vals) / len(vals), len(vals)
 
 
-def main():
-    fetch, write, cfetch, cwrite = sys.argv[1:5]
-    workload = sys.argv[5] if len(sys.argv) > 5 else "varlen16"
+def make_record(fetch, write, cfetch, cwrite, workload="varlen16"):
+    """The traffic record from the four counter CSV files."""
     cf, _ = per_dispatch_kib(cfetch, "elementwise")
     cw, _ = per_dispatch_kib(cwrite, "elementwise")
     fscale, wscale = COPY_BYTES / (cf * 1024), COPY_BYTES / (cw * 1024)
@@ -59,6 +58,13 @@ def main():
         rec["kernels"][key] = {"dispatches": n, "fetch_kib_raw": fk, "write_kib_raw": wk, "fetch_bytes": int(fb),
                                "write_bytes": int(wb), "traffic_bytes": int(fb + wb),
                                "source_sha256": source_sha256(files)}
+    return rec
+
+
+def main():
+    fetch, write, cfetch, cwrite = sys.argv[1:5]
+    workload = sys.argv[5] if len(sys.argv) > 5 else "varlen16"
+    rec = make_record(fetch, write, cfetch, cwrite, workload)
     out = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     with open(out, "w") as f:
         json.dump(rec, f, indent=1)
