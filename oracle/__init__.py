@@ -32,7 +32,9 @@ prints none of their algebra):
     channels ordered q | k | v, layout [C_tail][w-1] oldest -> newest, zero
     where the segment is shorter than w-1.
 
-Parity pins for every function live in tests/test_oracle_pins.py.
+Parity pins for every function live in tests/test_oracle_pins.py.  The
+anchor sidecar's write and read paths (Sections 4.2, 5.1, 5.2) are in
+``oracle.paged``, pinned in tests/test_paged_oracle.py.
 """
 from __future__ import annotations
 
