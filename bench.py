@@ -11,6 +11,12 @@ Prints ONE JSON line on stdout; progress goes to stderr.
 
     python bench.py [--gpus 1] [--steps 100] [--warmup 50] [--workload varlen16]
     python bench.py --copy-probe      # plain copy of known size, for HBM counter scaling
+    python bench.py --workload sidecar_gather   # anchor sidecar read path (Section 5.2)
+    python bench.py --workload sidecar_write    # anchor sidecar write path (Section 5.1)
+
+The two sidecar workloads time the sidecar's own calls instead of the replay
+and report anchor rows (x anchored layers) per second, with the HBM roofline
+of their dominant kernel.
 
 `roofline.traffic` is the dominant kernel's measured HBM bytes per launch,
 read from profiles/traffic_<workload>.json (rocprofv3 FETCH_SIZE / WRITE_SIZE
@@ -71,6 +77,8 @@ KERNEL_SOURCES = {
     "proj_conv": ("proj_conv.hip", "sr_device.hpp", "sr_internal.hpp"),
     "gdn_scan": ("gdn_scan_bf16.hip", "sr_device.hpp", "sr_internal.hpp"),
     "proj_gemm": ("proj_gemm.hip", "sr_device.hpp", "sr_internal.hpp"),
+    "anchor_gather": ("sidecar.hip", "sr_internal.hpp"),
+    "anchor_write": ("sidecar.hip", "sr_internal.hpp"),
 }
 
 
@@ -141,6 +149,141 @@ def cpu_baseline(wl, budget_s=15.0):
                       f"recurrence single-threaded"}
 
 
+SIDECAR_LAYERS = 7      # anchored layers of Qwen3.5-4B (Appendix A: A = G - 1 = 7)
+SIDECAR_D = 2560
+SIDECAR_PREFILL = (16, 4096)   # write path: a prefill step of 16 requests x 4096 tokens
+
+
+def bench_sidecar(args):
+    """Times the sidecar's gather (the last k anchors of the 16 varlen16
+    requests, all 7 anchored layers, into the packed replay batch) or its
+    write (compaction + indexed copy of a 64K-token prefill step)."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from workloads import sidecar as wsc
+    import paper_2609_33477_amd as sr
+
+    def dev(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).cuda()
+
+    A, d, eb = SIDECAR_LAYERS, SIDECAR_D, 2
+    row_bytes = d * eb
+    stream = torch.cuda.current_stream()
+    if args.workload == "sidecar_gather":
+        ks = W.make_config("varlen16").seg_lens
+        log(f"generating the pool for {len(ks)} requests, {sum(ks)} replay anchors x {A} layers")
+        g = wsc.gather_case(0, ks, A, d, eb)
+        pool = dev(g.pool)
+        sc = sr.make_sidecar(pool, A, wsc.PER_PAGE, d)
+        T = int(sum(ks))
+        outs = [torch.empty((T, d), dtype=torch.int16, device="cuda") for _ in range(A)]
+        cu = torch.empty(len(ks) + 1, dtype=torch.int32, device="cuda")
+        tabs = [dev(x) for x in (g.block_table, g.block_cu, g.anchor_first, g.n_anchors)]
+        rows = T * A
+
+        def step():
+            sr.anchor_gather(sc, *tabs, list(range(A)), outs, cu, stream)
+
+        bytes_of = {"anchor_gather": 2 * rows * row_bytes, "anchor_seqlens": (2 * len(ks) + 1) * 4}
+        config = {"workload": args.workload, "requests": len(ks), "anchor_rows": T, "layers": A, "d": d,
+                  "elem": "bf16", "per_page": wsc.PER_PAGE, "pool_blocks": g.n_blocks}
+
+        def cpu_leg(budget_s):
+            # the oracle's gather over whole requests until the budget is spent
+            t0, done, r = time.perf_counter(), 0, 0
+            tables = g.block_tables()
+            while r < len(ks) and time.perf_counter() - t0 < budget_s:
+                from oracle import paged
+                paged.anchor_gather(g.pool, A, wsc.PER_PAGE, [tables[r]], [int(g.anchor_first[r])],
+                                    [int(ks[r])], list(range(A)))
+                done += int(ks[r]) * A
+                r += 1
+            el = time.perf_counter() - t0
+            return {"value": round(done / el, 1), "unit": "anchor rows/s", "cores": 1, "kind": "oracle",
+                    "sample": f"oracle.paged.anchor_gather over the first {r} of {len(ks)} requests "
+                              f"({done} rows x layers) in {el:.1f} s"}
+    elif args.workload == "sidecar_write":
+        n_req, L = SIDECAR_PREFILL
+        log(f"generating a prefill step of {n_req} x {L} tokens x {A} layers")
+        c = wsc.write_case(0, [(0, L)] * n_req, A, d, eb)
+        dest_h = sr.anchor_dest_table(c.positions, c.token_req, c.page_table, c.page_cu, wsc.PAGE, wsc.PER_PAGE)
+        pool = dev(c.pool)
+        sc = sr.make_sidecar(pool, A, wsc.PER_PAGE, d)
+        hidden = [dev(h) for h in c.hidden]
+        dest = dev(dest_h)
+        n = len(dest_h)
+        sel = torch.empty(n, dtype=torch.int32, device="cuda")
+        n_sel = torch.empty(1, dtype=torch.int32, device="cuda")
+        n_rows = int((dest_h >= 0).sum())
+        rows = n_rows * A
+
+        def step():
+            sr.anchor_compact(dest, sel, n_sel, stream)
+            sr.anchor_write(sc, hidden, dest, sel, n_sel, stream)
+
+        bytes_of = {"anchor_compact": n * 4 + n_rows * 4,
+                    "anchor_write": 2 * rows * row_bytes + n_rows * 8}
+        config = {"workload": args.workload, "requests": n_req, "tokens": n, "anchor_rows": n_rows, "layers": A,
+                  "d": d, "elem": "bf16", "per_page": wsc.PER_PAGE}
+
+        def cpu_leg(budget_s):
+            from oracle import paged
+            t0, done, r = time.perf_counter(), 0, 0
+            pool_h = c.pool
+            while r < n_req and time.perf_counter() - t0 < budget_s:
+                m = c.token_req == r
+                sub = paged.compact(np.where(m, dest_h, -1))
+                pool_h = paged.anchor_write(pool_h, [h[sub] for h in c.hidden], dest_h[sub], wsc.PER_PAGE)
+                done += len(sub) * A
+                r += 1
+            el = time.perf_counter() - t0
+            return {"value": round(done / el, 1), "unit": "anchor rows/s", "cores": 1, "kind": "oracle",
+                    "sample": f"oracle.paged compact + anchor_write over the first {r} of {n_req} requests "
+                              f"({done} rows x layers) in {el:.1f} s"}
+    else:
+        raise SystemExit(f"unknown sidecar workload {args.workload}")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    sr.kernel_timing_enable(True)
+    sr.kernel_timing_read()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    kt = sr.kernel_timing_read()
+    sr.kernel_timing_enable(False)
+    kernels = {}
+    for k, (tot, cnt) in kt.items():
+        if cnt == 0:
+            continue
+        avg_ms = tot / cnt
+        ach = bytes_of[k] / (avg_ms * 1e-3) / 1e9
+        kernels[k] = {"avg_ms": round(avg_ms, 5), "launches_per_step": cnt / args.steps,
+                      "share": round(tot / max(sum(v[0] for v in kt.values()), 1e-12), 4), "bound": "hbm",
+                      "bytes": bytes_of[k], "achieved": round(ach, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                      "frac": round(ach / PEAK_HBM_GBS, 4)}
+    dom = max(kernels, key=lambda k: kernels[k]["share"])
+    dk = kernels[dom]
+    roofline = {"bound": "hbm", "achieved": dk["achieved"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": dk["frac"], "traffic": measured_traffic(args.workload, dom), "kernel": dom}
+    value = rows / (ms_per_step / 1e3)
+    log(f"{ms_per_step:.4f} ms/step, {value / 1e6:.2f} M rows/s; {dom} {dk['achieved']:.0f} GB/s")
+    cpu = None if args.no_cpu_baseline else cpu_leg(min(args.cpu_budget_s, 15.0))
+    out = {"metric": f"anchor rows x layers/sec ({args.workload.replace('_', ' ')})", "value": round(value, 1),
+           "unit": "rows/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "bf16", "data": "synthetic", "config": config, "latency_ms": round(ms_per_step, 5),
+           "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -162,6 +305,9 @@ def main():
 
     if args.copy_probe:
         copy_probe()
+        return
+    if args.workload.startswith("sidecar_"):
+        bench_sidecar(args)
         return
 
     import torch

@@ -166,7 +166,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
                           const int32_t* slot_ids, void* workspace, size_t workspace_bytes,
                           void* stream);
 
-/* Kernels the replay launches, as indexed by sr_kernel_timing_read(). */
+/* Kernels the library launches, as indexed by sr_kernel_timing_read(). */
 typedef enum sr_kernel_kind {
   SR_KERNEL_PROJ_GEMM = 0,   /* anchor projection (MFMA), fp32 path           */
   SR_KERNEL_CONV_GATE = 1,   /* conv + SiLU + key norm + gates + k|v tail,
@@ -176,12 +176,17 @@ typedef enum sr_kernel_kind {
   SR_KERNEL_PROJ_CONV = 4,   /* projection fused with conv, SiLU, key norm,
                                 gates and the k|v tail (bf16 / fp8 path)      */
   SR_KERNEL_ROW_INFO = 5,    /* per-row segment position and slot (bf16 path) */
-  SR_KERNEL_KINDS = 6
+  SR_KERNEL_ANCHOR_COMPACT = 6,  /* sidecar: prefill compaction (sr_sidecar.h)  */
+  SR_KERNEL_ANCHOR_WRITE = 7,    /* sidecar: indexed copy into the blocks       */
+  SR_KERNEL_ANCHOR_SEQLENS = 8,  /* sidecar: segment offsets of a gather        */
+  SR_KERNEL_ANCHOR_GATHER = 9,   /* sidecar: gather of the replay anchors       */
+  SR_KERNEL_KINDS = 10
 } sr_kernel_kind;
 
 /* Benchmark instrumentation (not needed by the replay itself).  While
- * enabled, sr_replay_state() records a HIP event pair around every kernel
- * launch on the caller's stream (creating events on first use).
+ * enabled, sr_replay_state() and the sidecar calls of sr_sidecar.h record a
+ * HIP event pair around every kernel launch on the caller's stream (creating
+ * events on first use).
  * sr_kernel_timing_read() waits for the recorded events, adds each pair's
  * elapsed time to ms[kind] and its count to launches[kind] (arrays of
  * SR_KERNEL_KINDS, zeroed by the call), then discards the records.
@@ -190,8 +195,8 @@ sr_status sr_kernel_timing_enable(int32_t enable);
 sr_status sr_kernel_timing_read(double* ms, int64_t* launches);
 
 /* Diagnostics for SR_ERR_HIP: the HIP error code (hipError_t) and the
- * sr_kernel_kind of the calling thread's most recent failed launch inside
- * sr_replay_state(), and hipGetErrorString() of that code (static storage).
+ * sr_kernel_kind of the calling thread's most recent failed launch inside a
+ * library call, and hipGetErrorString() of that code (static storage).
  * *hip_error is 0 and *kernel_kind -1 if no launch has failed on this thread.
  * Any output pointer may be NULL.  Always returns SR_OK. */
 sr_status sr_last_hip_error(int32_t* hip_error, int32_t* kernel_kind, const char** message);

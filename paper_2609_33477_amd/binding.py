@@ -53,6 +53,12 @@ def _hip_runtimes_mapped() -> set:
         return set()
 
 
+class SrSidecar(ctypes.Structure):
+    """sr_sidecar: the anchor block pool [n_blocks][n_layers][per_page][d]."""
+    _fields_ = [("pool", ctypes.c_void_p), ("n_blocks", ctypes.c_int64), ("n_layers", ctypes.c_int32),
+                ("per_page", ctypes.c_int32), ("d", ctypes.c_int32), ("elem_bytes", ctypes.c_int32)]
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_33477_amd.build` "
@@ -87,6 +93,19 @@ def _load() -> ctypes.CDLL:
     lib.sr_last_hip_error.restype = ctypes.c_int
     lib.sr_status_str.argtypes = [ctypes.c_int]
     lib.sr_status_str.restype = ctypes.c_char_p
+    I32P = ctypes.c_void_p
+    lib.sr_anchor_dest_table.argtypes = [I32P, I32P, ctypes.c_int32, I32P, I32P, ctypes.c_int32,
+                                         ctypes.c_int32, ctypes.c_int32, I32P]
+    lib.sr_anchor_dest_table.restype = ctypes.c_int
+    lib.sr_anchor_compact.argtypes = [I32P, ctypes.c_int32, I32P, I32P, ctypes.c_void_p]
+    lib.sr_anchor_compact.restype = ctypes.c_int
+    lib.sr_anchor_write.argtypes = [P(SrSidecar), P(ctypes.c_void_p), ctypes.c_int32, I32P, I32P, I32P,
+                                    ctypes.c_void_p]
+    lib.sr_anchor_write.restype = ctypes.c_int
+    lib.sr_anchor_gather.argtypes = [P(SrSidecar), ctypes.c_int32, I32P, I32P, I32P, I32P,
+                                     P(ctypes.c_int32), ctypes.c_int32, P(ctypes.c_void_p), ctypes.c_int64,
+                                     I32P, ctypes.c_void_p]
+    lib.sr_anchor_gather.restype = ctypes.c_int
     return lib
 
 
@@ -94,9 +113,11 @@ LIB = _load()
 
 EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
                     "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_last_hip_error",
-                    "sr_status_str")
+                    "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact", "sr_anchor_write",
+                    "sr_anchor_gather")
 
-KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan", "proj_conv", "row_info")
+KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan", "proj_conv", "row_info", "anchor_compact",
+                "anchor_write", "anchor_seqlens", "anchor_gather")
 
 
 def make_shape(shape) -> SrShape:
@@ -217,3 +238,61 @@ def replay_state(shape, layers: Sequence[LayerTensors], n_segments: int, t_total
                                  _ptr(cu_seqlens), _ptr(slot_ids), _ptr(workspace), int(workspace_bytes),
                                  stream_ptr)
     _check(status)
+
+
+# ------------------------------------------------------------ anchor sidecar
+def _stream_ptr(stream):
+    import torch  # plumbing: device memory and streams
+
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def make_sidecar(pool, n_layers: int, per_page: int, d: int) -> SrSidecar:
+    """sr_sidecar over a device tensor holding [n_blocks][n_layers][per_page][d]."""
+    eb = pool.element_size()
+    n_blocks = pool.numel() // (n_layers * per_page * d)
+    return SrSidecar(pool.data_ptr(), n_blocks, n_layers, per_page, d, eb)
+
+
+def anchor_dest_table(positions, token_req, page_table, page_cu, page_size: int, per_page: int):
+    """sr_anchor_dest_table on host int32 numpy arrays; returns dest (int32)."""
+    import numpy as np
+
+    pos = np.ascontiguousarray(positions, dtype=np.int32)
+    req = np.ascontiguousarray(token_req, dtype=np.int32)
+    tab = np.ascontiguousarray(page_table, dtype=np.int32)
+    cu = np.ascontiguousarray(page_cu, dtype=np.int32)
+    dest = np.empty(len(pos), dtype=np.int32)
+    _check(LIB.sr_anchor_dest_table(pos.ctypes.data, req.ctypes.data, len(pos), tab.ctypes.data if tab.size else None,
+                                    cu.ctypes.data, len(cu) - 1, int(page_size), int(per_page), dest.ctypes.data))
+    return dest
+
+
+def anchor_compact(dest, sel, n_sel, stream=None):
+    """sr_anchor_compact: device int32 tensors dest [n], sel [n], n_sel [1]."""
+    _check(LIB.sr_anchor_compact(_ptr(dest), int(dest.numel()), _ptr(sel), _ptr(n_sel), _stream_ptr(stream)))
+
+
+def anchor_write(sidecar: SrSidecar, hidden: Sequence, dest, sel=None, n_sel=None, stream=None):
+    """sr_anchor_write: hidden[l] are device tensors [n_tokens][d]."""
+    ptrs = (ctypes.c_void_p * len(hidden))(*[_ptr(h) for h in hidden])
+    n_tokens = int(dest.numel())
+    _check(LIB.sr_anchor_write(ctypes.byref(sidecar), ptrs, n_tokens, _ptr(dest), _ptr(sel), _ptr(n_sel),
+                               _stream_ptr(stream)))
+
+
+def anchor_gather(sidecar: SrSidecar, block_table, block_cu, anchor_first, n_anchors, layers: Sequence[int],
+                  out: Sequence, cu_seqlens, stream=None):
+    """sr_anchor_gather: device int32 tensors for the tables, out[o] device
+    tensors [t_cap][d] receiving layer layers[o]; cu_seqlens [n_req + 1]."""
+    lay = (ctypes.c_int32 * len(layers))(*[int(x) for x in layers])
+    ptrs = (ctypes.c_void_p * len(out))(*[_ptr(o) for o in out])
+    t_cap = min(int(o.shape[0]) for o in out)
+    n_req = int(n_anchors.numel())
+    _check(LIB.sr_anchor_gather(ctypes.byref(sidecar), n_req, _ptr(block_table), _ptr(block_cu),
+                                _ptr(anchor_first), _ptr(n_anchors), lay, len(layers), ptrs, t_cap,
+                                _ptr(cu_seqlens), _stream_ptr(stream)))

@@ -138,6 +138,14 @@ hipError_t timed(int kind, hipStream_t s, F&& launch) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+}  // namespace
+
+hipError_t sr::timed_launch(int kind, hipStream_t s, hipError_t (*launch)(void*), void* ctx) {
+  return timed(kind, s, [&] { return launch(ctx); });
+}
+
+namespace {
+
 sr_status check_layer(const sr_shape* s, const sr_layer& L, int64_t t_total) {
   if (t_total > 0 && !L.anchors) return SR_ERR_NULL_ARG;
   if (!L.w_k || !L.w_v || !L.w_a || !L.w_b || !L.conv_w || !L.a_log || !L.dt_bias || !L.state_out)

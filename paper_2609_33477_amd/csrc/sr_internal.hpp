@@ -133,4 +133,14 @@ struct ScanArgs {
 hipError_t launch_scan(int op_dtype, int d_head, const ScanArgs& a, hipStream_t s);
 hipError_t launch_scan_bf16(int d_head, const ScanArgs& a, hipStream_t s);
 
+// ----------------------------------------------------------- launch timing
+// Runs launch(ctx) on stream s under the library's per-kind timing and
+// failed-launch bookkeeping (sr_kernel_timing_*, sr_last_hip_error).
+hipError_t timed_launch(int kind, hipStream_t s, hipError_t (*launch)(void*), void* ctx);
+
+template <typename F>
+hipError_t timed_call(int kind, hipStream_t s, F&& f) {
+  return timed_launch(kind, s, [](void* c) { return (*static_cast<F*>(c))(); }, &f);
+}
+
 }  // namespace sr

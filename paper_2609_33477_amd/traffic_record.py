@@ -23,6 +23,8 @@ CSRC = os.path.join(PKG, "csrc")
 KERNELS = {
     "proj_conv": ("proj_conv_kernel", ("proj_conv.hip", "sr_device.hpp", "sr_internal.hpp")),
     "gdn_scan": ("gdn_scan_bf16_kernel", ("gdn_scan_bf16.hip", "sr_device.hpp", "sr_internal.hpp")),
+    "anchor_gather": ("gather_kernel", ("sidecar.hip", "sr_internal.hpp")),
+    "anchor_write": ("write_kernel", ("sidecar.hip", "sr_internal.hpp")),
 }
 COPY_BYTES = 1 << 30
 
@@ -52,6 +54,8 @@ def make_record(fetch, write, cfetch, cwrite, workload="varlen16"):
                           "fetch_scale": fscale, "write_scale": wscale},
            "kernels": {}}
     for key, (frag, files) in KERNELS.items():
+        if not any(frag in r["Kernel_Name"] for r in csv.DictReader(open(fetch))):
+            continue   # not launched by this workload
         fk, n = per_dispatch_kib(fetch, frag)
         wk, _ = per_dispatch_kib(write, frag)
         fb, wb = fk * 1024 * fscale, wk * 1024 * wscale

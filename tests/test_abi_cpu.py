@@ -1,5 +1,5 @@
 """CPU-side checks of the C-ABI library: it loads without a GPU, exports every
-function include/sr_replay.h declares, reproduces the paper's state and
+function include/sr_replay.h and include/sr_sidecar.h declare, reproduces the paper's state and
 conv-state sizes (Appendix A), and rejects bad arguments on the host before
 any launch (no device work is started by these calls)."""
 import ctypes
@@ -10,7 +10,7 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "sr_replay.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("sr_replay.h", "sr_sidecar.h")]
 GOLDEN = os.path.join(ROOT, "tests", "golden", "storage_table6.json")
 
 sr = pytest.importorskip("paper_2609_33477_amd.binding",
@@ -19,7 +19,7 @@ from workloads import Shape, F32, BF16, FP8  # noqa: E402
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     # declarations: "<return type> sr_name(" at the start of a line
     return sorted(set(re.findall(r"^(?:size_t|sr_status|const char\s*\*)\s*(sr_\w+)\s*\(", text, re.M)))
 
@@ -28,7 +28,8 @@ def test_header_declares_and_library_exports_every_function():
     names = declared_functions()
     assert set(names) == {"sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
                           "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read",
-                          "sr_last_hip_error", "sr_status_str"}
+                          "sr_last_hip_error", "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact",
+                          "sr_anchor_write", "sr_anchor_gather"}
     lib = ctypes.CDLL(sr.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
