@@ -32,6 +32,10 @@ prints none of their algebra):
     channels ordered q | k | v, layout [C_tail][w-1] oldest -> newest, zero
     where the segment is shorter than w-1.
 
+``shape.recurrence`` selects the state update: "gdn" (the default, above) or
+"decay", the per-head decay without the erase that the paper names for
+Mamba2 (Section 2.1), kept with Gated DeltaNet's inputs and write.
+
 Parity pins for every function live in tests/test_oracle_pins.py.  The
 anchor sidecar's write and read paths (Sections 4.2, 5.1, 5.2) are in
 ``oracle.paged``, pinned in tests/test_paged_oracle.py.
@@ -44,7 +48,7 @@ import numpy as np
 
 __all__ = [
     "project", "causal_depthwise_conv", "silu", "sigmoid", "softplus",
-    "l2_normalize", "decay_erase_gates", "key_head_of", "gated_delta_recurrence",
+    "l2_normalize", "decay_erase_gates", "key_head_of", "gated_delta_recurrence", "decay_recurrence",
     "replay_segment", "replay_workload", "layer_features",
 ]
 
@@ -140,6 +144,30 @@ def gated_delta_recurrence(k: np.ndarray, v: np.ndarray, alpha: np.ndarray,
     return S
 
 
+def decay_recurrence(k: np.ndarray, v: np.ndarray, alpha: np.ndarray,
+                     beta: np.ndarray, S0: Optional[np.ndarray] = None) -> np.ndarray:
+    """Token-by-token per-head-decay recurrence, the Mamba2-style form the
+    paper names beside Gated DeltaNet (Section 2.1, Eq. recurrence: A_t is a
+    per-head decay, no erase), with the same write as Gated DeltaNet:
+
+        S_t = alpha_t S_{t-1} + beta_t v_t k_t^T
+
+    Arguments and result as gated_delta_recurrence."""
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    L, H, dk = k.shape
+    dv = v.shape[2]
+    S = np.zeros((H, dv, dk)) if S0 is None else np.array(S0, dtype=np.float64)
+    for t in range(L):
+        at = np.asarray(alpha[t], dtype=np.float64)[:, None, None]
+        bt = np.asarray(beta[t], dtype=np.float64)[:, None, None]
+        S = at * S + bt * v[t][:, :, None] * k[t][:, None, :]
+    return S
+
+
+RECURRENCES = {"gdn": gated_delta_recurrence, "decay": decay_recurrence}
+
+
 def layer_features(shape, layer, x: np.ndarray) -> Dict[str, np.ndarray]:
     """Projection, conv, SiLU, key norm and gates for one segment's rows x
     ([L, D]).  Returns k [L, H_k, d_k], v [L, H_v, d_v], alpha/beta [L, H_v]
@@ -179,7 +207,7 @@ def replay_segment(shape, layer, x: np.ndarray, S0: Optional[np.ndarray] = None,
     kv_head = [key_head_of(h, H_k, H_v) for h in range(H_v)]
     k_per_v = f["k"][:, kv_head, :]                                  # [L, H_v, dk]
     S0_s = None if S0 is None else np.transpose(np.asarray(S0, dtype=np.float64), (0, 2, 1))
-    S = gated_delta_recurrence(k_per_v, f["v"], f["alpha"], f["beta"], S0_s)
+    S = RECURRENCES[getattr(shape, "recurrence", "gdn")](k_per_v, f["v"], f["alpha"], f["beta"], S0_s)
     state = np.transpose(S, (0, 2, 1))                               # M = S^T
 
     n_tail = min(L, w - 1)

@@ -320,3 +320,40 @@ def test_state_and_conv_sizes_match_paper_table():
         assert m["L_lin"] * (m["B_rec"] + m["B_conv"]) == m["B_ckpt"], name
         assert m["B_ckpt"] / 8192 == m["B_native_8192"], name
         assert m["L_lin"] * m["d"] * 2 == m["B_naive"], name
+
+
+# ------------------------------------------------- per-head decay (Mamba2)
+def test_decay_recurrence_equals_gdn_for_orthogonal_keys():
+    """With mutually orthogonal unit keys the erase term S_{t-1} k_t vanishes
+    (every earlier write is along an orthogonal key), so Gated DeltaNet and
+    the decay-only recurrence give the same state.  Catches a decay applied
+    to the write, a missing beta, or a transposed outer product."""
+    rng = np.random.default_rng(21)
+    L, H, dk, dv = 6, 2, 8, 5
+    q, _ = np.linalg.qr(rng.standard_normal((dk, dk)))
+    k = np.stack([q[:L].copy() for _ in range(H)], axis=1)          # [L, H, dk], orthonormal rows
+    v = rng.standard_normal((L, H, dv))
+    alpha = rng.uniform(0.5, 1.0, (L, H))
+    beta = rng.uniform(0.1, 0.9, (L, H))
+    S0 = rng.standard_normal((H, dv, dk)) @ np.diag([0.0] * dk)     # zero start
+    assert np.allclose(oracle.decay_recurrence(k, v, alpha, beta, S0),
+                       oracle.gated_delta_recurrence(k, v, alpha, beta, S0), atol=1e-12)
+
+
+def test_decay_recurrence_matches_the_unrolled_sum():
+    """The paper's unrolled form (Section 2.1, Eq. unrolled) with a scalar
+    decay per head: S_n = prod(alpha) S_0 + sum_i (prod_{s>i} alpha_s) beta_i
+    v_i k_i^T, evaluated as one weighted matrix product.  Catches an
+    off-by-one in which decays a write receives."""
+    rng = np.random.default_rng(22)
+    L, H, dk, dv = 9, 3, 4, 6
+    k = rng.standard_normal((L, H, dk))
+    v = rng.standard_normal((L, H, dv))
+    alpha = rng.uniform(0.3, 1.0, (L, H))
+    beta = rng.uniform(0.1, 0.9, (L, H))
+    S0 = rng.standard_normal((H, dv, dk))
+    got = oracle.decay_recurrence(k, v, alpha, beta, S0)
+    for h in range(H):
+        w = np.array([np.prod(alpha[i + 1:, h]) * beta[i, h] for i in range(L)])
+        want = np.prod(alpha[:, h]) * S0[h] + v[:, h].T @ np.diag(w) @ k[:, h]
+        assert np.allclose(got[h], want, atol=1e-12)

@@ -88,6 +88,7 @@ class Shape:
     weight_dtype: str = BF16   # projection weights (q, k, v, a, b)
     conv_dtype: str = BF16     # depthwise conv taps
     tail_dtype: str = BF16     # conv-tail output
+    recurrence: str = "gdn"    # "gdn" (decay + erase) or "decay" (per-head decay only)
 
     @property
     def c_kv(self) -> int:     # conv channels the recurrence consumes (k | v)
