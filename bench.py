@@ -69,6 +69,8 @@ def algorithmic_work(wl, with_q=True):
         "row_info": ("hbm", T * 16),
         # one launch covers all layers (up to 32)
         "gdn_scan": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * d * d * 4)),
+        # the per-head-decay state reads the same operands and writes the same states
+        "decay_state": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * d * d * 4)),
     }
 
 
@@ -77,6 +79,7 @@ KERNEL_SOURCES = {
     "proj_conv": ("proj_conv.hip", "sr_device.hpp", "sr_internal.hpp"),
     "gdn_scan": ("gdn_scan_bf16.hip", "sr_device.hpp", "sr_internal.hpp"),
     "proj_gemm": ("proj_gemm.hip", "sr_device.hpp", "sr_internal.hpp"),
+    "decay_state": ("decay_state.hip", "sr_device.hpp", "sr_internal.hpp"),
     "anchor_gather": ("sidecar.hip", "sr_internal.hpp"),
     "anchor_write": ("sidecar.hip", "sr_internal.hpp"),
 }

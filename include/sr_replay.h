@@ -89,7 +89,19 @@ typedef struct sr_shape {
   int32_t weight_dtype;
   int32_t conv_dtype;
   int32_t tail_dtype;
+  int32_t recurrence;   /* sr_recurrence; 0 (the zero-initialised default) = Gated DeltaNet */
 } sr_shape;
+
+/* The state update (Section 2.1, Eq. recurrence; both share the layer's
+ * projections, conv, key norm and gates):
+ *  SR_RECURRENCE_GDN    S_t = alpha_t S_{t-1} (I - beta_t k_t k_t^T) + beta_t v_t k_t^T
+ *  SR_RECURRENCE_DECAY  S_t = alpha_t S_{t-1} + beta_t v_t k_t^T: the per-head decay
+ *                       without erase that the paper names for Mamba2; BF16
+ *                       anchors only (SR_ERR_UNSUPPORTED_DTYPE otherwise) */
+typedef enum sr_recurrence {
+  SR_RECURRENCE_GDN = 0,
+  SR_RECURRENCE_DECAY = 1
+} sr_recurrence;
 
 /* Tensors of one layer (all device pointers).  T = t_total, D = d_model.
  *  anchors    [T][D] anchor_dtype: the packed replay suffixes of all segments
@@ -180,7 +192,8 @@ typedef enum sr_kernel_kind {
   SR_KERNEL_ANCHOR_WRITE = 7,    /* sidecar: indexed copy into the blocks       */
   SR_KERNEL_ANCHOR_SEQLENS = 8,  /* sidecar: segment offsets of a gather        */
   SR_KERNEL_ANCHOR_GATHER = 9,   /* sidecar: gather of the replay anchors       */
-  SR_KERNEL_KINDS = 10
+  SR_KERNEL_DECAY_STATE = 10,    /* per-head-decay state (SR_RECURRENCE_DECAY)  */
+  SR_KERNEL_KINDS = 11
 } sr_kernel_kind;
 
 /* Benchmark instrumentation (not needed by the replay itself).  While

@@ -33,7 +33,7 @@ class SrShape(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int32), ("n_k_heads", ctypes.c_int32), ("n_v_heads", ctypes.c_int32),
                 ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("conv_width", ctypes.c_int32),
                 ("l2_eps", ctypes.c_float), ("anchor_dtype", ctypes.c_int32), ("weight_dtype", ctypes.c_int32),
-                ("conv_dtype", ctypes.c_int32), ("tail_dtype", ctypes.c_int32)]
+                ("conv_dtype", ctypes.c_int32), ("tail_dtype", ctypes.c_int32), ("recurrence", ctypes.c_int32)]
 
 
 _LAYER_FIELDS = ("anchors", "w_k", "w_v", "w_a", "w_b", "w_q", "s_k", "s_v", "s_a", "s_b", "s_q",
@@ -117,7 +117,10 @@ EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace
                     "sr_anchor_gather")
 
 KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan", "proj_conv", "row_info", "anchor_compact",
-                "anchor_write", "anchor_seqlens", "anchor_gather")
+                "anchor_write", "anchor_seqlens", "anchor_gather", "decay_state")
+
+
+_RECURRENCE_CODES = {"gdn": 0, "decay": 1, 0: 0, 1: 1}
 
 
 def make_shape(shape) -> SrShape:
@@ -126,7 +129,8 @@ def make_shape(shape) -> SrShape:
     return SrShape(int(shape.d_model), int(shape.n_k_heads), int(shape.n_v_heads), int(shape.d_k),
                    int(shape.d_v), int(shape.conv_width), float(shape.l2_eps),
                    _DTYPE_CODES[shape.anchor_dtype], _DTYPE_CODES[shape.weight_dtype],
-                   _DTYPE_CODES[shape.conv_dtype], _DTYPE_CODES[shape.tail_dtype])
+                   _DTYPE_CODES[shape.conv_dtype], _DTYPE_CODES[shape.tail_dtype],
+                   _RECURRENCE_CODES[getattr(shape, "recurrence", "gdn")])
 
 
 def status_str(status: int) -> str:

@@ -52,6 +52,8 @@ sr_status check_shape(const sr_shape* s) {
   if (!pair_ok) return SR_ERR_UNSUPPORTED_DTYPE;
   if (s->conv_dtype != SR_F32 && s->conv_dtype != SR_BF16) return SR_ERR_UNSUPPORTED_DTYPE;
   if (s->tail_dtype != SR_F32 && s->tail_dtype != SR_BF16) return SR_ERR_UNSUPPORTED_DTYPE;
+  if (s->recurrence != SR_RECURRENCE_GDN && s->recurrence != SR_RECURRENCE_DECAY) return SR_ERR_BAD_SHAPE;
+  if (s->recurrence == SR_RECURRENCE_DECAY && s->anchor_dtype != SR_BF16) return SR_ERR_UNSUPPORTED_DTYPE;
   return SR_OK;
 }
 
@@ -333,7 +335,10 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       a.state_in[i] = layers[l0 + i].state_in;
       a.state_out[i] = layers[l0 + i].state_out;
     }
-    if (timed(SR_KERNEL_GDN_SCAN, s, [&] { return sr::launch_scan(plan.op_dtype, d, a, s); }) != hipSuccess)
+    if (shape->recurrence == SR_RECURRENCE_DECAY) {
+      if (timed(SR_KERNEL_DECAY_STATE, s, [&] { return sr::launch_decay_state(d, a, s); }) != hipSuccess)
+        return SR_ERR_HIP;
+    } else if (timed(SR_KERNEL_GDN_SCAN, s, [&] { return sr::launch_scan(plan.op_dtype, d, a, s); }) != hipSuccess)
       return SR_ERR_HIP;
   }
   return SR_OK;

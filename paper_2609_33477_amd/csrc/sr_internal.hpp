@@ -132,6 +132,8 @@ struct ScanArgs {
 
 hipError_t launch_scan(int op_dtype, int d_head, const ScanArgs& a, hipStream_t s);
 hipError_t launch_scan_bf16(int d_head, const ScanArgs& a, hipStream_t s);
+// per-head-decay recurrence: M = 2^{G_L} M_0 + K^T diag(beta 2^{G_L - G}) V (bf16 path)
+hipError_t launch_decay_state(int d_head, const ScanArgs& a, hipStream_t s);
 
 // ----------------------------------------------------------- launch timing
 // Runs launch(ctx) on stream s under the library's per-kind timing and

@@ -23,6 +23,7 @@ CSRC = os.path.join(PKG, "csrc")
 KERNELS = {
     "proj_conv": ("proj_conv_kernel", ("proj_conv.hip", "sr_device.hpp", "sr_internal.hpp")),
     "gdn_scan": ("gdn_scan_bf16_kernel", ("gdn_scan_bf16.hip", "sr_device.hpp", "sr_internal.hpp")),
+    "decay_state": ("decay_state_kernel", ("decay_state.hip", "sr_device.hpp", "sr_internal.hpp")),
     "anchor_gather": ("gather_kernel", ("sidecar.hip", "sr_internal.hpp")),
     "anchor_write": ("write_kernel", ("sidecar.hip", "sr_internal.hpp")),
 }

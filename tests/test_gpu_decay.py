@@ -1,0 +1,86 @@
+"""The per-head-decay recurrence (SR_RECURRENCE_DECAY, the Mamba2 form of
+Section 2.1: S_t = alpha_t S_{t-1} + beta_t v_t k_t^T) through the C ABI
+against the oracle's decay_recurrence: ragged segments spanning several
+64-row chunks with partial chunks and an empty segment, all head sizes, GQA,
+sentinel slots, the initial-state carry, and varlen16's full inputs on
+sampled segments.  CPU part: the host rejects what the variant does not
+support before any launch."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+sr = pytest.importorskip("paper_2609_33477_amd.binding",
+                         reason="libsr_replay.so not built (run __graft_entry__.build())")
+
+RAGGED = [1, 3, 64, 65, 200, 0, 130, 127]
+
+
+def _ws_status(shape):
+    out = ctypes.c_size_t(0)
+    return sr.LIB.sr_replay_workspace_size(ctypes.byref(sr.make_shape(shape)), 1, 100, ctypes.byref(out))
+
+
+def test_host_checks_of_the_recurrence_field():
+    assert _ws_status(W.Shape(256, 2, 4, 128, 128, recurrence="decay")) == 0
+    f32 = W.Shape(128, 2, 2, 32, 32, anchor_dtype=W.F32, weight_dtype=W.F32, conv_dtype=W.F32,
+                  tail_dtype=W.F32, recurrence="decay")
+    assert _ws_status(f32) == 3          # SR_ERR_UNSUPPORTED_DTYPE: decay runs on bf16 anchors only
+    sh = sr.make_shape(W.Shape(256, 2, 4, 128, 128))
+    sh.recurrence = 2
+    out = ctypes.c_size_t(0)
+    assert sr.LIB.sr_replay_workspace_size(ctypes.byref(sh), 1, 100, ctypes.byref(out)) == 2   # SR_ERR_BAD_SHAPE
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_decay_ragged_segments(d):
+    import torch
+    from gpu_harness import TOL_BF16, check_pairs, log, run, upload
+    shape = W.Shape(256, 2, 4, d, d, recurrence="decay")
+    wl = W.make_workload(f"decay_d{d}", shape, RAGGED, seed=71 + d)
+    log(f"decay ragged d={d}: T={wl.t_total}")
+    dev = upload(wl)
+    run(dev)
+    check_pairs(dev, [(0, b) for b in range(len(RAGGED)) if RAGGED[b] > 0], TOL_BF16)
+    b0 = RAGGED.index(0)
+    assert torch.all(dev.layers[0].state_out[b0] == 0)
+
+
+@pytest.mark.gpu
+def test_decay_sentinels_and_initial_state():
+    import torch
+    import oracle
+    from gpu_harness import TOL_BF16, check_pairs, log, rel_frob, run, upload
+    shape = W.Shape(256, 2, 4, 128, 128, recurrence="decay")
+    seg = [40, 65, 7, 130]
+    wl = W.make_workload("decay_slots", shape, seg, seed=81, slot_ids=[3, -1, 0, -5], n_slots=5)
+    log("decay sentinels")
+    dev = upload(wl)
+    run(dev)
+    for s in (1, 2, 4):
+        assert torch.all(torch.isnan(dev.layers[0].state_out[s])), s
+    check_pairs(dev, [(0, 0), (0, 2)], TOL_BF16)
+    log("decay initial state")
+    wl2 = W.make_workload("decay_init", shape, [3, 90, 200], seed=82)
+    S0 = np.random.default_rng(1).standard_normal((3, 4, 128, 128)).astype(np.float32) * 0.5
+    dev2 = upload(wl2, state_in=[S0])
+    run(dev2)
+    cu, L = wl2.cu_seqlens, wl2.layers[0]
+    for b in range(3):
+        ref, _ = oracle.replay_segment(shape, L, L.anchors[cu[b]:cu[b + 1]], S0=S0[b].astype(np.float64))
+        assert rel_frob(dev2.layers[0].state_out[b].cpu().numpy(), ref) <= TOL_BF16, b
+
+
+@pytest.mark.gpu
+def test_varlen16_decay_sampled():
+    from gpu_harness import check_pairs, log, run, upload
+    wl = W.make_config("varlen16_decay")
+    log(f"varlen16_decay: T={wl.t_total}")
+    dev = upload(wl)
+    run(dev)
+    lens = wl.seg_lens
+    pick = sorted({int(np.argmin(lens)), int(np.argmax(lens)), 5})
+    check_pairs(dev, [(0, b) for b in pick])

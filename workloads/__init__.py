@@ -19,7 +19,7 @@ Replay lengths are whole 64-token pages (Section 4.2 aligns anchors to
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass, field, replace
 from typing import Dict, List, Optional
 
 import numpy as np
@@ -235,7 +235,15 @@ LONG_MEMORY_DT_BIAS_MEAN = -7.494
 CONFIG_NAMES = ("tiny", "gdn_single", "varlen16", "multilayer12", "stress64")
 
 
+# Variants of a named workload: same seed and tensors, another recurrence.
+VARIANTS = {"varlen16_decay": ("varlen16", "decay")}
+
+
 def _config_table(name: str):
+    if name in VARIANTS:
+        base, rec = VARIANTS[name]
+        seed, shape, seg, n_layers, mu = _config_table(base)
+        return seed, replace(shape, recurrence=rec), seg, n_layers, mu
     seed = CONFIG_NAMES.index(name) + 1
     rng = np.random.default_rng((seed, SEGMENT_STREAM))
     if name == "tiny":
@@ -271,6 +279,7 @@ def make_config(name: str) -> Workload:
                   fp8 E4M3 weights + per-channel bf16 scales, bf16 anchors
     stress64      64 requests, L ~ 64*U{16..128}, D=4096, H=32, bf16,
                   dt_bias shifted so mean alpha is 0.995
+    varlen16_decay  varlen16's inputs under the per-head-decay recurrence
     Weights ~ N(0, 0.02), anchors ~ N(0, 1), A_log ~ U(log 1, log 16),
     dt_bias ~ N(mu, 0.5), zero initial state.
     """
