@@ -249,3 +249,54 @@ def test_write_then_gather_returns_the_hidden_rows():
         for l in range(2):
             got = _host(outs[l], np.uint16)[cu_h[r]:cu_h[r + 1]]
             assert np.array_equal(got, c.hidden[l][want])
+
+
+@pytest.mark.gpu
+def test_write_and_gather_replay_under_hip_graph_capture():
+    """Section 5.1 moves the anchor writes into the captured graph of each
+    serving step.  The compaction, the indexed copy and the gather are
+    stream-ordered and allocate nothing, so one graph holds all three; every
+    replay (with eager work and synchronisation between replays, and the
+    outputs poisoned before each) reproduces the oracle bit for bit."""
+    import torch
+    _log("sidecar calls under graph capture")
+    c = wsc.write_case(13, [(0, 700), (128, 900), (60, 61)], 3, 64, 2, hole_frac=0.1)
+    dest = paged.dest_table(c.positions, c.token_req, c.page_tables(), wsc.PAGE, wsc.PER_PAGE)
+    want_pool = paged.anchor_write(c.pool, c.hidden, dest, wsc.PER_PAGE)
+    g = wsc.gather_case(14, [9, 0, 31], 3, 64, 2)
+    want_out, want_cu = paged.anchor_gather(g.pool, 3, wsc.PER_PAGE, g.block_tables(), g.anchor_first,
+                                            g.n_anchors, [2, 0])
+    pool0 = _dev(c.pool)
+    pool = pool0.clone()
+    hidden = [_dev(h) for h in c.hidden]
+    d_dest = _dev(dest)
+    sel = torch.empty(len(dest), dtype=torch.int32, device="cuda")
+    n_sel = torch.empty(1, dtype=torch.int32, device="cuda")
+    sc_w = sr.make_sidecar(pool, 3, wsc.PER_PAGE, 64)
+    gpool = _dev(g.pool)
+    sc_g = sr.make_sidecar(gpool, 3, wsc.PER_PAGE, 64)
+    tabs = [_dev(x) for x in (g.block_table, g.block_cu, g.anchor_first, g.n_anchors)]
+    T = int(want_cu[-1])
+    outs = [torch.empty((T, 64), dtype=torch.int16, device="cuda") for _ in range(2)]
+    cu = torch.empty(4, dtype=torch.int32, device="cuda")
+    s = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=s):
+        sr.anchor_compact(d_dest, sel, n_sel, s)
+        sr.anchor_write(sc_w, hidden, d_dest, sel, n_sel, s)
+        sr.anchor_gather(sc_g, *tabs, [2, 0], outs, cu, s)
+    for rep in range(3):
+        pool.copy_(pool0)
+        for o in outs:
+            o.fill_(-1)
+        cu.fill_(-7)
+        sel.fill_(-7)
+        n_sel.fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(_host(pool, np.uint16), want_pool), rep
+        assert np.array_equal(cu.cpu().numpy(), want_cu), rep
+        for o, w in zip(outs, want_out):
+            assert np.array_equal(_host(o, np.uint16), w), rep
