@@ -190,7 +190,7 @@ struct GatherArgs {
   int32_t layer[kMaxLayers];
 };
 
-constexpr int kRowsPerWave = 2;
+constexpr int kRowsPerWave = 1;
 
 // A wave copies kRowsPerWave consecutive output rows: it finds the first
 // row's request by binary search over cu_seqlens, then steps forward.
