@@ -84,3 +84,34 @@ def test_varlen16_decay_sampled():
     lens = wl.seg_lens
     pick = sorted({int(np.argmin(lens)), int(np.argmax(lens)), 5})
     check_pairs(dev, [(0, b) for b in pick])
+
+
+@pytest.mark.gpu
+def test_decay_deterministic_and_graph_capture_replays():
+    """No atomics and a fixed reduction order: two eager runs agree bit for
+    bit, and a captured graph reproduces the eager state on every replay
+    (outputs poisoned before each, eager work between replays)."""
+    import torch
+    from gpu_harness import log, run, upload
+    shape = W.Shape(256, 2, 4, 128, 128, recurrence="decay")
+    wl = W.make_workload("decay_graph", shape, [70, 5, 129, 300], seed=91)
+    log("decay determinism and graph capture")
+    dev = upload(wl)
+    ws = run(dev)
+    eager = dev.layers[0].state_out.clone()
+    eager_tail = dev.layers[0].tail_out.clone()
+    run(dev, workspace=ws)
+    assert torch.equal(dev.layers[0].state_out, eager)
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        run(dev, workspace=ws, stream=s, sync=False)
+    for _ in range(3):
+        dev.layers[0].state_out.fill_(float("nan"))
+        dev.layers[0].tail_out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dev.layers[0].state_out, eager)
+        assert torch.equal(dev.layers[0].tail_out, eager_tail)
