@@ -13,6 +13,7 @@ Prints ONE JSON line on stdout; progress goes to stderr.
     python bench.py --copy-probe      # plain copy of known size, for HBM counter scaling
     python bench.py --workload sidecar_gather   # anchor sidecar read path (Section 5.2)
     python bench.py --workload sidecar_write    # anchor sidecar write path (Section 5.1)
+    python bench.py --workload graph_small      # graph-bucketed replay of a small batch vs eager
 
 The two sidecar workloads time the sidecar's own calls instead of the replay
 and report anchor rows (x anchored layers) per second, with the HBM roofline
@@ -287,6 +288,82 @@ def bench_sidecar(args):
     print(json.dumps(out), flush=True)
 
 
+GRAPH_SEGMENTS = [128] * 8          # a small batch of hits: 8 requests x 128 replayed anchors
+GRAPH_LAYERS = 24                   # every linear-attention layer of Qwen3.5-4B (Appendix A)
+GRAPH_BUCKETS = [256, 1024, 4096]   # total-length buckets, up to the paper's T_max = 4096
+
+
+def bench_graph(args):
+    """Replay of a small batch of hits (8 x 128 anchors through all 24
+    Qwen3.5-4B linear layers) through the graph-bucketed path
+    (sr_replay_graph: the padding kernel and the replay in one captured
+    graph) against the eager sr_replay_state call on the same inputs."""
+    import torch
+    import workloads as W
+    from workloads.device import upload
+    import paper_2609_33477_amd as sr
+
+    shape = W.config_shape("varlen16")[0]
+    wl = W.make_workload("graph_small", shape, GRAPH_SEGMENTS, n_layers=GRAPH_LAYERS, seed=3)
+    dev = upload(wl)
+    layers = [sr.LayerTensors(**vars(ns)) for ns in dev.layers]
+    g = sr.ReplayGraph(shape, layers, max_segments=len(GRAPH_SEGMENTS), bucket_rows=GRAPH_BUCKETS)
+    for li in range(GRAPH_LAYERS):
+        g.anchors(li)[:wl.t_total].copy_(dev.layers[li].anchors.view(torch.int16))
+    ws_bytes = sr.replay_workspace_size(shape, GRAPH_LAYERS, wl.t_total)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    n = len(GRAPH_SEGMENTS)
+
+    def eager():
+        sr.replay_state(shape, layers, n, wl.t_total, dev.cu_seqlens, dev.slot_ids, ws, ws_bytes, stream)
+
+    def graph():
+        g.run(n, wl.t_total, dev.cu_seqlens, dev.slot_ids, stream)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps
+
+    ms_graph = timed(graph)
+    ms_eager = timed(eager)
+    # the kernels' own durations, from the eager path's per-kernel events
+    sr.kernel_timing_enable(True)
+    sr.kernel_timing_read()
+    for _ in range(args.steps):
+        eager()
+    kt = sr.kernel_timing_read()
+    sr.kernel_timing_enable(False)
+    work = algorithmic_work(wl, with_q=dev.with_q)
+    tot, cnt = kt["proj_conv"]
+    avg_ms = tot / cnt
+    ach = work["proj_conv"][1] / (avg_ms * 1e-3) / 1e12
+    g.close()
+    value = wl.replayed_tokens / (ms_graph / 1e3)
+    log(f"graph {ms_graph:.4f} ms, eager {ms_eager:.4f} ms per replay of {wl.t_total} anchors")
+    out = {"metric": METRIC + " (graph-bucketed small batch)", "value": round(value, 1), "unit": "tokens/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_graph, 5),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": "graph_small", "requests": n, "anchors_per_request": GRAPH_SEGMENTS[0],
+                      "layers": GRAPH_LAYERS,
+                      "t_total": wl.t_total, "bucket_rows": GRAPH_BUCKETS, "d_model": shape.d_model,
+                      "n_k_heads": shape.n_k_heads, "n_v_heads": shape.n_v_heads, "d_k": shape.d_k,
+                      "eager_ms_per_step": round(ms_eager, 5)},
+           "latency_ms": round(ms_graph, 5),
+           "roofline": {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
+                        "frac": round(ach / PEAK_TFLOPS["bf16"], 4), "traffic": None, "kernel": "proj_conv"},
+           "cpu_baseline": None}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -311,6 +388,9 @@ def main():
         return
     if args.workload.startswith("sidecar_"):
         bench_sidecar(args)
+        return
+    if args.workload == "graph_small":
+        bench_graph(args)
         return
 
     import torch

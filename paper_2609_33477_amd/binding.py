@@ -106,6 +106,18 @@ def _load() -> ctypes.CDLL:
                                      P(ctypes.c_int32), ctypes.c_int32, P(ctypes.c_void_p), ctypes.c_int64,
                                      I32P, ctypes.c_void_p]
     lib.sr_anchor_gather.restype = ctypes.c_int
+    lib.sr_replay_graph_create.argtypes = [P(SrShape), ctypes.c_int32, P(SrLayer), ctypes.c_int32,
+                                           P(ctypes.c_int64), ctypes.c_int32, P(ctypes.c_void_p)]
+    lib.sr_replay_graph_create.restype = ctypes.c_int
+    lib.sr_replay_graph_anchors.argtypes = [ctypes.c_void_p, ctypes.c_int32]
+    lib.sr_replay_graph_anchors.restype = ctypes.c_void_p
+    lib.sr_replay_graph_max_rows.argtypes = [ctypes.c_void_p]
+    lib.sr_replay_graph_max_rows.restype = ctypes.c_int64
+    lib.sr_replay_graph_run.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p, P(ctypes.c_int32)]
+    lib.sr_replay_graph_run.restype = ctypes.c_int
+    lib.sr_replay_graph_destroy.argtypes = [ctypes.c_void_p]
+    lib.sr_replay_graph_destroy.restype = ctypes.c_int
     return lib
 
 
@@ -114,7 +126,8 @@ LIB = _load()
 EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
                     "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_last_hip_error",
                     "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact", "sr_anchor_write",
-                    "sr_anchor_gather")
+                    "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
+                    "sr_replay_graph_max_rows", "sr_replay_graph_run", "sr_replay_graph_destroy")
 
 KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan", "proj_conv", "row_info", "anchor_compact",
                 "anchor_write", "anchor_seqlens", "anchor_gather", "decay_state")
@@ -300,3 +313,56 @@ def anchor_gather(sidecar: SrSidecar, block_table, block_cu, anchor_first, n_anc
     _check(LIB.sr_anchor_gather(ctypes.byref(sidecar), n_req, _ptr(block_table), _ptr(block_cu),
                                 _ptr(anchor_first), _ptr(n_anchors), lay, len(layers), ptrs, t_cap,
                                 _ptr(cu_seqlens), _stream_ptr(stream)))
+
+
+# ------------------------------------------------------ graph-bucketed replay
+class _DevArray:
+    """A device buffer the library owns, seen by torch without a copy."""
+
+    def __init__(self, ptr, shape, typestr):
+        self.__cuda_array_interface__ = {"shape": tuple(shape), "typestr": typestr, "data": (ptr, False),
+                                         "version": 3, "strides": None}
+
+
+class ReplayGraph:
+    """sr_replay_graph: graph-captured replay per total-length bucket."""
+
+    def __init__(self, shape, layers: Sequence[LayerTensors], max_segments: int, bucket_rows: Sequence[int]):
+        self.shape = shape
+        self._layers = make_layer_array(layers)   # kept alive: weights/state pointers are frozen in graphs
+        self._sh = make_shape(shape)
+        rows = (ctypes.c_int64 * len(bucket_rows))(*[int(r) for r in bucket_rows])
+        h = ctypes.c_void_p()
+        _check(LIB.sr_replay_graph_create(ctypes.byref(self._sh), len(layers), self._layers, int(max_segments),
+                                          rows, len(bucket_rows), ctypes.byref(h)))
+        self._h = h
+        self.n_layers = len(layers)
+        self.max_rows = int(LIB.sr_replay_graph_max_rows(h))
+
+    def anchors(self, layer: int):
+        """torch view [T_max][d_model] of layer `layer`'s anchor buffer."""
+        import torch  # plumbing: device memory
+
+        ptr = LIB.sr_replay_graph_anchors(self._h, int(layer))
+        if not ptr:
+            raise IndexError(layer)
+        typestr = "<f4" if _DTYPE_CODES[self.shape.anchor_dtype] == SR_F32 else "<i2"
+        return torch.as_tensor(_DevArray(ptr, (self.max_rows, int(self.shape.d_model)), typestr), device="cuda")
+
+    def run(self, n_segments: int, t_total: int, cu_seqlens, slot_ids=None, stream=None) -> int:
+        """Replays the batch; returns the bucket index used (-1: eager)."""
+        used = ctypes.c_int32(-2)
+        _check(LIB.sr_replay_graph_run(self._h, int(n_segments), int(t_total), _ptr(cu_seqlens), _ptr(slot_ids),
+                                       _stream_ptr(stream), ctypes.byref(used)))
+        return int(used.value)
+
+    def close(self):
+        if self._h:
+            _check(LIB.sr_replay_graph_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,5 +1,5 @@
 """CPU-side checks of the C-ABI library: it loads without a GPU, exports every
-function include/sr_replay.h and include/sr_sidecar.h declare, reproduces the paper's state and
+function include/*.h declares, reproduces the paper's state and
 conv-state sizes (Appendix A), and rejects bad arguments on the host before
 any launch (no device work is started by these calls)."""
 import ctypes
@@ -10,7 +10,7 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADERS = [os.path.join(ROOT, "include", h) for h in ("sr_replay.h", "sr_sidecar.h")]
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("sr_replay.h", "sr_sidecar.h", "sr_replay_graph.h")]
 GOLDEN = os.path.join(ROOT, "tests", "golden", "storage_table6.json")
 
 sr = pytest.importorskip("paper_2609_33477_amd.binding",
@@ -21,7 +21,7 @@ from workloads import Shape, F32, BF16, FP8  # noqa: E402
 def declared_functions():
     text = "".join(open(h).read() for h in HEADERS)
     # declarations: "<return type> sr_name(" at the start of a line
-    return sorted(set(re.findall(r"^(?:size_t|sr_status|const char\s*\*)\s*(sr_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^(?:size_t|sr_status|int64_t|void\s*\*|const char\s*\*)\s*(sr_\w+)\s*\(", text, re.M)))
 
 
 def test_header_declares_and_library_exports_every_function():
@@ -29,7 +29,8 @@ def test_header_declares_and_library_exports_every_function():
     assert set(names) == {"sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
                           "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read",
                           "sr_last_hip_error", "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact",
-                          "sr_anchor_write", "sr_anchor_gather"}
+                          "sr_anchor_write", "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
+                          "sr_replay_graph_max_rows", "sr_replay_graph_run", "sr_replay_graph_destroy"}
     lib = ctypes.CDLL(sr.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -133,3 +134,18 @@ def test_kernel_timing_read_without_launches():
     sr.kernel_timing_enable(False)
     assert set(out) == set(sr.KERNEL_KINDS)
     assert all(v == (0.0, 0) for v in out.values())
+
+
+def test_replay_graph_rejects_bad_arguments_before_allocating():
+    import workloads as W
+    sh = sr.make_shape(W.Shape(256, 2, 4, 128, 128))
+    lay = (sr.SrLayer * 1)()
+    h = ctypes.c_void_p()
+    rows = (ctypes.c_int64 * 3)(256, 128, 1024)            # not ascending
+    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, 8, rows, 3, ctypes.byref(h)) == 2
+    rows = (ctypes.c_int64 * 1)(256)
+    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, 0, rows, 1, ctypes.byref(h)) == 2
+    assert sr.LIB.sr_replay_graph_create(None, 1, lay, 8, rows, 1, ctypes.byref(h)) == 1
+    assert sr.LIB.sr_replay_graph_run(None, 1, 10, None, None, None, None) == 1
+    assert sr.LIB.sr_replay_graph_destroy(None) == 0
+    assert sr.LIB.sr_replay_graph_anchors(None, 0) is None and sr.LIB.sr_replay_graph_max_rows(None) == 0
