@@ -125,16 +125,33 @@ def copy_probe(n_bytes=1 << 30, launches=5):
                       "avg_ms": round(ms, 4), "GBps": round(2 * n_bytes / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return None
+
+
 def cpu_baseline(wl, budget_s=15.0):
     """The fp64 oracle on a bounded sample of the same workload: whole
-    segments, in order, until ~budget_s of CPU work."""
+    segments, shortest first, until ~budget_s of CPU work.  The projection
+    runs on the BLAS threads, the recurrence on the C twin with one host
+    thread per value head (up to the cores the process may use)."""
     import numpy as np
     import oracle
+    from oracle import crec
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        cores = 1
+        blas = 1
+    rec_threads = min(crec.threads(), wl.shape.n_v_heads) if crec.available() else 1
+    cores = max(blas, rec_threads)
     cu = wl.cu_seqlens
     lay = wl.layers[0]
     rows = 0
@@ -147,10 +164,12 @@ def cpu_baseline(wl, budget_s=15.0):
         rows += wl.seg_lens[b]
         segs.append(int(b))
     el = time.perf_counter() - t0
+    rec = (f"recurrence on the C twin over {rec_threads} threads" if crec.available()
+           else "recurrence in numpy, single-threaded")
     return {"value": rows / el, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"{len(segs)} of {len(wl.seg_lens)} segments of layer 0 ({rows} anchor rows, "
-                      f"segments {segs}), fp64 numpy, {el:.1f} s; projection on {cores} BLAS threads, "
-                      f"recurrence single-threaded"}
+                      f"segments {segs}), fp64, {el:.1f} s; projection on {blas} BLAS threads, {rec}"}
 
 
 SIDECAR_LAYERS = 7      # anchored layers of Qwen3.5-4B (Appendix A: A = G - 1 = 7)

@@ -42,14 +42,14 @@ anchor sidecar's write and read paths (Sections 4.2, 5.1, 5.2) are in
 """
 from __future__ import annotations
 
-from typing import Dict, Iterable, Optional, Tuple
+from typing import Dict, Optional, Tuple
 
 import numpy as np
 
 __all__ = [
     "project", "causal_depthwise_conv", "silu", "sigmoid", "softplus",
     "l2_normalize", "decay_erase_gates", "key_head_of", "gated_delta_recurrence", "decay_recurrence",
-    "replay_segment", "replay_workload", "layer_features",
+    "replay_segment", "layer_features", "recurrence",
 ]
 
 
@@ -80,9 +80,12 @@ def causal_depthwise_conv(p: np.ndarray, taps: np.ndarray) -> np.ndarray:
 
 
 def sigmoid(x: np.ndarray) -> np.ndarray:
+    """1 / (1 + e^-x) without overflow: with e = e^-|x|, 1 / (1 + e) for
+    x >= 0 and e / (1 + e) otherwise."""
     x = np.asarray(x, dtype=np.float64)
     e = np.exp(-np.abs(x))
-    return np.where(x >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+    r = 1.0 / (1.0 + e)
+    return np.where(x >= 0, r, e * r)
 
 
 def silu(y: np.ndarray) -> np.ndarray:
@@ -168,6 +171,20 @@ def decay_recurrence(k: np.ndarray, v: np.ndarray, alpha: np.ndarray,
 RECURRENCES = {"gdn": gated_delta_recurrence, "decay": decay_recurrence}
 
 
+def recurrence(kind: str, k, v, alpha, beta, S0=None, impl: str = "auto") -> np.ndarray:
+    """The recurrence ``kind`` ("gdn" or "decay") over expanded per-head inputs
+    (arguments as gated_delta_recurrence).  ``impl`` "numpy" runs the numpy
+    loops above, "c" the plain-C twin in oracle/recurrence.c (one host thread
+    per head), "auto" the C twin when it is built.  The two are pinned to each
+    other; the C twin only makes full-size workloads affordable."""
+    from . import crec
+    if impl == "c" or (impl == "auto" and crec.available()):
+        return crec.recurrence(kind, k, v, alpha, beta, S0)
+    if impl not in ("numpy", "auto"):
+        raise ValueError(impl)
+    return RECURRENCES[kind](k, v, alpha, beta, S0)
+
+
 def layer_features(shape, layer, x: np.ndarray) -> Dict[str, np.ndarray]:
     """Projection, conv, SiLU, key norm and gates for one segment's rows x
     ([L, D]).  Returns k [L, H_k, d_k], v [L, H_v, d_v], alpha/beta [L, H_v]
@@ -187,12 +204,13 @@ def layer_features(shape, layer, x: np.ndarray) -> Dict[str, np.ndarray]:
 
 
 def replay_segment(shape, layer, x: np.ndarray, S0: Optional[np.ndarray] = None,
-                   with_q_tail: bool = True) -> Tuple[np.ndarray, np.ndarray]:
+                   with_q_tail: bool = True, impl: str = "auto") -> Tuple[np.ndarray, np.ndarray]:
     """Replay one segment's anchors x [L, D] through one linear layer.
 
     Returns (state [H_v, d_k, d_v] = S_L^T, tail [C_tail, w-1]).  ``S0`` is an
     optional initial state in the same [H_v, d_k, d_v] layout (None = zero, the
-    method).  With ``with_q_tail`` False the tail holds only k | v channels."""
+    method).  With ``with_q_tail`` False the tail holds only k | v channels.
+    ``impl`` selects the recurrence implementation (see ``recurrence``)."""
     H_k, H_v, dk, dv = shape.n_k_heads, shape.n_v_heads, shape.d_k, shape.d_v
     w = shape.conv_width
     x = np.asarray(x, dtype=np.float64)
@@ -207,7 +225,7 @@ def replay_segment(shape, layer, x: np.ndarray, S0: Optional[np.ndarray] = None,
     kv_head = [key_head_of(h, H_k, H_v) for h in range(H_v)]
     k_per_v = f["k"][:, kv_head, :]                                  # [L, H_v, dk]
     S0_s = None if S0 is None else np.transpose(np.asarray(S0, dtype=np.float64), (0, 2, 1))
-    S = RECURRENCES[getattr(shape, "recurrence", "gdn")](k_per_v, f["v"], f["alpha"], f["beta"], S0_s)
+    S = recurrence(getattr(shape, "recurrence", "gdn"), k_per_v, f["v"], f["alpha"], f["beta"], S0_s, impl=impl)
     state = np.transpose(S, (0, 2, 1))                               # M = S^T
 
     n_tail = min(L, w - 1)
@@ -219,22 +237,3 @@ def replay_segment(shape, layer, x: np.ndarray, S0: Optional[np.ndarray] = None,
     parts += [f["p_k"][rows], f["p_v"][rows]]
     tail[:, w - 1 - n_tail:] = np.concatenate(parts, axis=1).T
     return state, tail
-
-
-def replay_workload(wl, layers: Optional[Iterable[int]] = None,
-                    segments: Optional[Iterable[int]] = None,
-                    with_q_tail: bool = True) -> Dict[Tuple[int, int], Tuple[np.ndarray, np.ndarray]]:
-    """Oracle output for (layer, segment) pairs of a workload; sentinel
-    segments (slot < 0) are skipped."""
-    cu = wl.cu_seqlens
-    layers = range(len(wl.layers)) if layers is None else layers
-    segments = range(len(wl.seg_lens)) if segments is None else segments
-    out = {}
-    for li in layers:
-        layer = wl.layers[li]
-        for b in segments:
-            if wl.slot_ids[b] < 0:
-                continue
-            x = layer.anchors[cu[b]:cu[b + 1]]
-            out[(li, b)] = replay_segment(wl.shape, layer, x, with_q_tail=with_q_tail)
-    return out

@@ -329,7 +329,10 @@ class ReplayGraph:
 
     def __init__(self, shape, layers: Sequence[LayerTensors], max_segments: int, bucket_rows: Sequence[int]):
         self.shape = shape
-        self._layers = make_layer_array(layers)   # kept alive: weights/state pointers are frozen in graphs
+        # The captured graphs hold the raw weight, state and tail pointers, so
+        # the tensors behind them must outlive this object: keep references.
+        self._tensors = list(layers)
+        self._layers = make_layer_array(layers)
         self._sh = make_shape(shape)
         rows = (ctypes.c_int64 * len(bucket_rows))(*[int(r) for r in bucket_rows])
         h = ctypes.c_void_p()

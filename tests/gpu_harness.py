@@ -15,6 +15,11 @@ from workloads.device import upload  # noqa: F401  (re-exported for tests)
 
 TOL_F32 = 1e-4
 TOL_BF16 = 5e-3
+# Per value head, a looser bound guards against one wrong head hiding in a
+# slab's average (H_v = 32..48 heads dilute one head's error by ~sqrt(H_v)):
+# rounding alone keeps every head within 2x the slab tolerance, while a head
+# computed wrongly (wrong gate row, key head or sign) is off by 1e-1 or more.
+HEAD_FACTOR = 2.0
 
 
 def log(msg: str):
@@ -48,31 +53,55 @@ def tolerance(wl) -> float:
     return TOL_F32 if wl.shape.anchor_dtype == "f32" else TOL_BF16
 
 
+def per_head_rel(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
+    """Relative Frobenius error of each value head of a [H_v][d_k][d_v] slab
+    (a zero reference head must come back exactly zero)."""
+    got = np.asarray(got, dtype=np.float64)
+    num = np.linalg.norm((got - ref).reshape(ref.shape[0], -1), axis=1)
+    den = np.linalg.norm(ref.reshape(ref.shape[0], -1), axis=1)
+    return np.where(den > 0, num / np.where(den > 0, den, 1.0), num)
+
+
+def check_slab(wl, li, b, got_state, got_tail, tol, with_q=True, check_tail=True, ref=None):
+    """Compares one (layer, segment) slab with the oracle; returns
+    (state error, worst head error, tail error) and asserts the bounds."""
+    cu = wl.cu_seqlens
+    L = wl.layers[li]
+    t0 = time.time()
+    if ref is None:
+        ref = oracle.replay_segment(wl.shape, L, L.anchors[cu[b]:cu[b + 1]], with_q_tail=with_q)
+    ref_state, ref_tail = ref
+    es = rel_frob(got_state, ref_state)
+    eh = per_head_rel(got_state, ref_state)
+    msg = (f"layer {li} seg {b} (L={wl.seg_lens[b]}, slot {wl.slot_ids[b]}): state rel err {es:.3e}, "
+           f"worst head {eh.max():.3e} (head {int(eh.argmax())})")
+    et = 0.0
+    if check_tail and wl.shape.conv_width > 1:
+        et = rel_frob(got_tail, ref_tail)
+        msg += f", tail rel err {et:.3e}"
+        assert np.all(np.isfinite(got_tail)), msg
+    log(msg + f"  [oracle {time.time() - t0:.1f}s]")
+    assert np.all(np.isfinite(got_state)), msg
+    assert es <= tol, msg
+    assert eh.max() <= HEAD_FACTOR * tol, msg
+    if check_tail and wl.shape.conv_width > 1:
+        # a bf16 tail is rounded once on output (relative error <= 2^-9 per
+        # element), so it cannot meet the fp32 bound even with fp32 inputs
+        assert et <= (tol if wl.shape.tail_dtype == "f32" else max(tol, TOL_BF16)), msg
+    return es, float(eh.max()), et
+
+
 def check_pairs(dev, pairs, tol=None, check_tail=True):
-    """Oracle vs GPU for (layer, segment) pairs; returns the worst errors."""
+    """Oracle vs GPU for (layer, segment) pairs; returns the worst state and
+    tail errors."""
     wl = dev.wl
     tol = tolerance(wl) if tol is None else tol
-    cu = wl.cu_seqlens
     worst_s = worst_t = 0.0
     for li, b in pairs:
         slot = wl.slot_ids[b]
         assert slot >= 0
-        L = wl.layers[li]
-        t0 = time.time()
-        ref_state, ref_tail = oracle.replay_segment(wl.shape, L, L.anchors[cu[b]:cu[b + 1]], with_q_tail=dev.with_q)
         got_state = dev.layers[li].state_out[slot].cpu().numpy()
-        es = rel_frob(got_state, ref_state)
-        worst_s = max(worst_s, es)
-        msg = f"layer {li} seg {b} (L={wl.seg_lens[b]}, slot {slot}): state rel err {es:.3e}"
-        if check_tail and wl.shape.conv_width > 1:
-            got_tail = dev.layers[li].tail_out[slot].float().cpu().numpy()
-            et = rel_frob(got_tail, ref_tail)
-            worst_t = max(worst_t, et)
-            msg += f", tail rel err {et:.3e}"
-            assert np.all(np.isfinite(got_tail)), msg
-        log(msg + f"  [oracle {time.time() - t0:.1f}s]")
-        assert np.all(np.isfinite(got_state)), msg
-        assert es <= tol, msg
-        if check_tail and wl.shape.conv_width > 1:
-            assert et <= tol, msg
+        got_tail = dev.layers[li].tail_out[slot].float().cpu().numpy() if check_tail else None
+        es, _, et = check_slab(wl, li, b, got_state, got_tail, tol, dev.with_q, check_tail)
+        worst_s, worst_t = max(worst_s, es), max(worst_t, et)
     return worst_s, worst_t

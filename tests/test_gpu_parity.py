@@ -201,3 +201,33 @@ def test_more_segments_than_the_device_sort():
     run(dev)
     live = [p for p in _live_pairs(wl)]
     check_pairs(dev, live[::17] + live[-3:], TOL_BF16)
+
+
+# Every (dtype, head size, conv width) combination the host accepts, on a
+# small ragged batch, so that no accepted combination goes untested.
+COMBOS = [
+    # (name, shape keyword arguments, d, conv width, with q tail)
+    ("f32_d64", dict(anchor_dtype=W.F32, weight_dtype=W.F32, conv_dtype=W.F32, tail_dtype=W.F32), 64, 4, True),
+    ("f32_bf16_conv_tail", dict(anchor_dtype=W.F32, weight_dtype=W.F32, conv_dtype=W.BF16, tail_dtype=W.BF16),
+     64, 4, True),
+    ("fp8_d32", dict(weight_dtype=W.FP8), 32, 4, True),
+    ("fp8_d64", dict(weight_dtype=W.FP8), 64, 4, True),
+    ("bf16_w1", dict(), 64, 1, True),
+    ("bf16_w3", dict(), 64, 3, True),
+    ("f32_w3", dict(anchor_dtype=W.F32, weight_dtype=W.F32, conv_dtype=W.F32, tail_dtype=W.F32), 32, 3, True),
+    ("f32_w1", dict(anchor_dtype=W.F32, weight_dtype=W.F32, conv_dtype=W.F32, tail_dtype=W.F32), 32, 1, False),
+    ("fp8_w2_noq", dict(weight_dtype=W.FP8, tail_dtype=W.F32), 128, 2, False),
+]
+
+
+@pytest.mark.parametrize("name,kw,d,w,with_q", COMBOS, ids=[c[0] for c in COMBOS])
+def test_accepted_combinations(name, kw, d, w, with_q):
+    shape = W.Shape(192, 2, 4, d, d, conv_width=w, **kw)
+    wl = W.make_workload(name, shape, [1, 2, 70, 0, 131], seed=200 + [c[0] for c in COMBOS].index(name))
+    log(f"combination {name}: T={wl.t_total}")
+    dev = upload(wl, with_q=with_q)
+    run(dev)
+    tol = TOL_F32 if shape.anchor_dtype == W.F32 else TOL_BF16
+    check_pairs(dev, _live_pairs(wl), tol, check_tail=w > 1)
+    b0 = 3
+    assert torch.all(dev.layers[0].state_out[b0] == 0)

@@ -13,6 +13,7 @@ import scipy.special
 import torch
 
 import oracle
+from oracle import crec
 from workloads import Shape, LayerInputs, F32
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -108,6 +109,39 @@ def test_key_head_grouping():
 
 
 # ----------------------------------------------------------------- recurrence
+# Every recurrence pin runs on both implementations: the numpy loops and the
+# plain-C twin (oracle/recurrence.c) that full-size parity tests use.
+IMPLS = ["numpy", "c"]
+if not crec.available():
+    crec.build()
+
+
+def _gdn(impl):
+    return lambda *a: oracle.recurrence("gdn", *a, impl=impl)
+
+
+def _decay(impl):
+    return lambda *a: oracle.recurrence("decay", *a, impl=impl)
+
+
+@pytest.mark.parametrize("kind", ["gdn", "decay"])
+def test_c_twin_matches_numpy_recurrence(kind):
+    """Implementation independence: the C twin and the numpy loops agree to
+    1e-12 relative on random inputs with d_k != d_v, a non-zero initial state,
+    unnormalised keys and several heads.  Catches a stride or orientation
+    mistake in either."""
+    for seed, (L, H, dk, dv) in enumerate([(1, 1, 3, 5), (37, 3, 8, 6), (130, 2, 32, 16)]):
+        r = np.random.default_rng(100 + seed)
+        k = r.standard_normal((L, H, dk)) * 0.4
+        v = r.standard_normal((L, H, dv))
+        alpha = r.uniform(0.2, 1.0, (L, H))
+        beta = r.uniform(0.0, 1.0, (L, H))
+        S0 = r.standard_normal((H, dv, dk))
+        a = oracle.recurrence(kind, k, v, alpha, beta, S0, impl="numpy")
+        b = oracle.recurrence(kind, k, v, alpha, beta, S0, impl="c")
+        assert np.linalg.norm(a - b) <= 1e-12 * np.linalg.norm(a)
+        assert np.array_equal(oracle.recurrence(kind, k[:0], v[:0], alpha[:0], beta[:0], S0, impl="c"), S0)
+
 def _rand_inputs(L, H=2, dk=5, dv=3, unit=True, seed=0):
     r = np.random.default_rng(seed)
     k = r.standard_normal((L, H, dk))
@@ -119,14 +153,15 @@ def _rand_inputs(L, H=2, dk=5, dv=3, unit=True, seed=0):
     return k, v, alpha, beta
 
 
-def test_recurrence_matches_paper_unrolled_form():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_recurrence_matches_paper_unrolled_form(impl):
     """Eq. (unrolled): S_n = sum_i Phi_{n,i}(B_i) with A_t(S) = S R_t,
     R_t = alpha_t (I - beta_t k_t k_t^T) and B_t = beta_t v_t k_t^T, evaluated as
     explicit matrix products.  Non-symmetric random data makes a transposed
     state, a wrong sign of the erase, or a missing decay fail."""
     L, H, dk, dv = 9, 2, 5, 3
     k, v, alpha, beta = _rand_inputs(L, H, dk, dv, unit=False)
-    S = oracle.gated_delta_recurrence(k, v, alpha, beta)
+    S = _gdn(impl)(k, v, alpha, beta)
     for h in range(H):
         R = [alpha[t, h] * (np.eye(dk) - beta[t, h] * np.outer(k[t, h], k[t, h])) for t in range(L)]
         total = np.zeros((dv, dk))
@@ -138,33 +173,37 @@ def test_recurrence_matches_paper_unrolled_form():
         np.testing.assert_allclose(S[h], total, rtol=1e-12, atol=1e-13)
 
 
-def test_recurrence_identity_gates_keep_state():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_recurrence_identity_gates_keep_state(impl):
     """I1: alpha = 1, beta = 0 leaves any initial state unchanged."""
     k, v, _, _ = _rand_inputs(20)
     S0 = np.random.default_rng(3).standard_normal((2, 3, 5))
-    S = oracle.gated_delta_recurrence(k, v, np.ones((20, 2)), np.zeros((20, 2)), S0)
+    S = _gdn(impl)(k, v, np.ones((20, 2)), np.zeros((20, 2)), S0)
     np.testing.assert_array_equal(S, S0)
 
 
-def test_recurrence_pure_decay():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_recurrence_pure_decay(impl):
     """I2: beta = 0 gives S_L = prod(alpha) S_0."""
     k, v, alpha, _ = _rand_inputs(12)
     S0 = np.random.default_rng(4).standard_normal((2, 3, 5))
-    S = oracle.gated_delta_recurrence(k, v, alpha, np.zeros((12, 2)), S0)
+    S = _gdn(impl)(k, v, alpha, np.zeros((12, 2)), S0)
     np.testing.assert_allclose(S, np.prod(alpha, axis=0)[:, None, None] * S0, rtol=1e-14)
 
 
-def test_recurrence_exact_delta_write():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_recurrence_exact_delta_write(impl):
     """I3: with beta_L = 1 and a unit key, S_L k_L = v_L whatever the history."""
     k, v, alpha, beta = _rand_inputs(15)
     beta[-1] = 1.0
     S0 = np.random.default_rng(5).standard_normal((2, 3, 5))
-    S = oracle.gated_delta_recurrence(k, v, alpha, beta, S0)
+    S = _gdn(impl)(k, v, alpha, beta, S0)
     for h in range(2):
         np.testing.assert_allclose(S[h] @ k[-1, h], v[-1, h], rtol=1e-12, atol=1e-13)
 
 
-def test_recurrence_orthonormal_keys_store_last_value():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_recurrence_orthonormal_keys_store_last_value(impl):
     """I4: alpha = beta = 1 and keys from an orthonormal basis: the state is
     sum_e v_last(e) e^T (each write erases the previous value at its key)."""
     dk, dv, L = 4, 3, 11
@@ -173,7 +212,7 @@ def test_recurrence_orthonormal_keys_store_last_value():
     idx = r.integers(0, dk, L)
     k = basis[idx][:, None, :]
     v = r.standard_normal((L, 1, dv))
-    S = oracle.gated_delta_recurrence(k, v, np.ones((L, 1)), np.ones((L, 1)))
+    S = _gdn(impl)(k, v, np.ones((L, 1)), np.ones((L, 1)))
     ref = np.zeros((dv, dk))
     for e in range(dk):
         hits = np.nonzero(idx == e)[0]
@@ -182,35 +221,38 @@ def test_recurrence_orthonormal_keys_store_last_value():
     np.testing.assert_allclose(S[0], ref, atol=1e-12)
 
 
-def test_recurrence_contraction_bound():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_recurrence_contraction_bound(impl):
     """I5 (the property suffix replay rests on, Section 1 and Section 2.1):
     ||S_L(S_0) - S_L(0)||_F <= ||S_0||_F prod(alpha) for unit keys, beta in [0,1]."""
     for seed in range(5):
         k, v, alpha, beta = _rand_inputs(40, H=3, dk=6, dv=4, seed=seed)
         S0 = np.random.default_rng(seed + 10).standard_normal((3, 4, 6)) * 5
-        full = oracle.gated_delta_recurrence(k, v, alpha, beta, S0)
-        replay = oracle.gated_delta_recurrence(k, v, alpha, beta)
+        full = _gdn(impl)(k, v, alpha, beta, S0)
+        replay = _gdn(impl)(k, v, alpha, beta)
         for h in range(3):
             lhs = np.linalg.norm(full[h] - replay[h])
             rhs = np.linalg.norm(S0[h]) * np.prod(alpha[:, h])
             assert lhs <= rhs * (1 + 1e-12) + 1e-300
 
 
-def test_recurrence_single_token_closed_form():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_recurrence_single_token_closed_form(impl):
     """I6: L = 1 from zero: S_1 = beta v k^T (catches an outer product in the
     wrong order)."""
     k, v, alpha, beta = _rand_inputs(1, unit=False)
-    S = oracle.gated_delta_recurrence(k, v, alpha, beta)
+    S = _gdn(impl)(k, v, alpha, beta)
     for h in range(2):
         np.testing.assert_allclose(S[h], beta[0, h] * np.outer(v[0, h], k[0, h]), rtol=1e-15)
 
 
-def test_recurrence_linear_in_values():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_recurrence_linear_in_values(impl):
     """I7: from zero, f(v + c v') = f(v) + c f(v') for fixed k, alpha, beta."""
     k, v, alpha, beta = _rand_inputs(17)
     v2 = np.random.default_rng(8).standard_normal(v.shape)
-    lhs = oracle.gated_delta_recurrence(k, v + 2.5 * v2, alpha, beta)
-    rhs = oracle.gated_delta_recurrence(k, v, alpha, beta) + 2.5 * oracle.gated_delta_recurrence(k, v2, alpha, beta)
+    lhs = _gdn(impl)(k, v + 2.5 * v2, alpha, beta)
+    rhs = _gdn(impl)(k, v, alpha, beta) + 2.5 * _gdn(impl)(k, v2, alpha, beta)
     np.testing.assert_allclose(lhs, rhs, rtol=1e-12, atol=1e-13)
 
 
@@ -323,7 +365,8 @@ def test_state_and_conv_sizes_match_paper_table():
 
 
 # ------------------------------------------------- per-head decay (Mamba2)
-def test_decay_recurrence_equals_gdn_for_orthogonal_keys():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_decay_recurrence_equals_gdn_for_orthogonal_keys(impl):
     """With mutually orthogonal unit keys the erase term S_{t-1} k_t vanishes
     (every earlier write is along an orthogonal key), so Gated DeltaNet and
     the decay-only recurrence give the same state.  Catches a decay applied
@@ -336,11 +379,12 @@ def test_decay_recurrence_equals_gdn_for_orthogonal_keys():
     alpha = rng.uniform(0.5, 1.0, (L, H))
     beta = rng.uniform(0.1, 0.9, (L, H))
     S0 = rng.standard_normal((H, dv, dk)) @ np.diag([0.0] * dk)     # zero start
-    assert np.allclose(oracle.decay_recurrence(k, v, alpha, beta, S0),
-                       oracle.gated_delta_recurrence(k, v, alpha, beta, S0), atol=1e-12)
+    assert np.allclose(_decay(impl)(k, v, alpha, beta, S0),
+                       _gdn(impl)(k, v, alpha, beta, S0), atol=1e-12)
 
 
-def test_decay_recurrence_matches_the_unrolled_sum():
+@pytest.mark.parametrize("impl", IMPLS)
+def test_decay_recurrence_matches_the_unrolled_sum(impl):
     """The paper's unrolled form (Section 2.1, Eq. unrolled) with a scalar
     decay per head: S_n = prod(alpha) S_0 + sum_i (prod_{s>i} alpha_s) beta_i
     v_i k_i^T, evaluated as one weighted matrix product.  Catches an
@@ -352,7 +396,7 @@ def test_decay_recurrence_matches_the_unrolled_sum():
     alpha = rng.uniform(0.3, 1.0, (L, H))
     beta = rng.uniform(0.1, 0.9, (L, H))
     S0 = rng.standard_normal((H, dv, dk))
-    got = oracle.decay_recurrence(k, v, alpha, beta, S0)
+    got = _decay(impl)(k, v, alpha, beta, S0)
     for h in range(H):
         w = np.array([np.prod(alpha[i + 1:, h]) * beta[i, h] for i in range(L)])
         want = np.prod(alpha[:, h]) * S0[h] + v[:, h].T @ np.diag(w) @ k[:, h]
