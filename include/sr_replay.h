@@ -178,6 +178,29 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
                           const int32_t* slot_ids, void* workspace, size_t workspace_bytes,
                           void* stream);
 
+/* Largest workspace sr_replay_state_noalloc() can serve (128 MiB: e.g. 4096
+ * packed rows of one Qwen3.5-4B or Qwen3.6-27B linear layer). */
+#define SR_NOALLOC_SCRATCH_BYTES (128u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the replay
+ * of sr_replay_state() with the same arguments minus the workspace, which
+ * comes from a library-owned device array of SR_NOALLOC_SCRATCH_BYTES per GPU
+ * (held until the process ends).  Calls no hipMalloc, hipFree or allocating
+ * library routine.
+ *  - SR_ERR_WORKSPACE_TOO_SMALL, with nothing written, when
+ *    sr_replay_workspace_size() for these arguments exceeds
+ *    SR_NOALLOC_SCRATCH_BYTES.
+ *  - Every call on a GPU shares that GPU's array: calls that overlap on one
+ *    GPU race, so calls on one device must be ordered (one stream, or
+ *    events).  The array keeps the last call's contents; a call never reads
+ *    scratch it has not written.
+ *  - The first call on a device resolves the array's device address
+ *    (SR_ERR_HIP if that fails); later calls reuse it. */
+sr_status sr_replay_state_noalloc(const sr_shape* shape, int32_t n_layers, const sr_layer* layers,
+                                  int32_t n_segments, int64_t t_total, const int32_t* cu_seqlens,
+                                  const int32_t* slot_ids, void* stream);
+
 /* Kernels the library launches, as indexed by sr_kernel_timing_read(). */
 typedef enum sr_kernel_kind {
   SR_KERNEL_PROJ_GEMM = 0,   /* anchor projection (MFMA), fp32 path           */

@@ -12,7 +12,8 @@ _BINDING_NAMES = {
     "LIB_PATH", "SR_BF16", "SR_F32", "SR_FP8_E4M3", "KERNEL_KINDS", "LayerTensors", "SrError",
     "conv_tail_bytes", "kernel_timing_enable", "kernel_timing_read", "replay_state",
     "replay_workspace_size", "state_bytes", "status_str", "SrSidecar", "make_sidecar", "anchor_dest_table",
-    "anchor_compact", "anchor_write", "anchor_gather", "ReplayGraph",
+    "anchor_compact", "anchor_write", "anchor_gather", "ReplayGraph", "replay_state_noalloc",
+    "NOALLOC_SCRATCH_BYTES",
 }
 
 

@@ -85,6 +85,9 @@ def _load() -> ctypes.CDLL:
                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                     ctypes.c_void_p]
     lib.sr_replay_state.restype = ctypes.c_int
+    lib.sr_replay_state_noalloc.argtypes = [P(SrShape), ctypes.c_int32, P(SrLayer), ctypes.c_int32,
+                                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.sr_replay_state_noalloc.restype = ctypes.c_int
     lib.sr_kernel_timing_enable.argtypes = [ctypes.c_int32]
     lib.sr_kernel_timing_enable.restype = ctypes.c_int
     lib.sr_kernel_timing_read.argtypes = [P(ctypes.c_double), P(ctypes.c_int64)]
@@ -124,7 +127,7 @@ def _load() -> ctypes.CDLL:
 LIB = _load()
 
 EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
-                    "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_last_hip_error",
+                    "sr_replay_state", "sr_replay_state_noalloc", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_last_hip_error",
                     "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact", "sr_anchor_write",
                     "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
                     "sr_replay_graph_max_rows", "sr_replay_graph_run", "sr_replay_graph_destroy")
@@ -255,6 +258,21 @@ def replay_state(shape, layers: Sequence[LayerTensors], n_segments: int, t_total
                                  _ptr(cu_seqlens), _ptr(slot_ids), _ptr(workspace), int(workspace_bytes),
                                  stream_ptr)
     _check(status)
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20      # SR_NOALLOC_SCRATCH_BYTES
+
+
+def replay_state_noalloc(shape, layers: Sequence[LayerTensors], n_segments: int, t_total: int, cu_seqlens,
+                         slot_ids=None, stream=None):
+    """sr_replay_state_noalloc: replay_state() on the library's own device
+    scratch (no workspace argument).  Raises SrError on a non-OK status
+    (SR_ERR_WORKSPACE_TOO_SMALL when the call needs more than
+    NOALLOC_SCRATCH_BYTES)."""
+    sh = make_shape(shape)
+    arr = make_layer_array(layers)
+    _check(LIB.sr_replay_state_noalloc(ctypes.byref(sh), len(layers), arr, int(n_segments), int(t_total),
+                                       _ptr(cu_seqlens), _ptr(slot_ids), _stream_ptr(stream)))
 
 
 # ------------------------------------------------------------ anchor sidecar

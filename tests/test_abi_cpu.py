@@ -27,7 +27,7 @@ def declared_functions():
 def test_header_declares_and_library_exports_every_function():
     names = declared_functions()
     assert set(names) == {"sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
-                          "sr_replay_state", "sr_kernel_timing_enable", "sr_kernel_timing_read",
+                          "sr_replay_state", "sr_replay_state_noalloc", "sr_kernel_timing_enable", "sr_kernel_timing_read",
                           "sr_last_hip_error", "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact",
                           "sr_anchor_write", "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
                           "sr_replay_graph_max_rows", "sr_replay_graph_run", "sr_replay_graph_destroy"}
@@ -149,3 +149,17 @@ def test_replay_graph_rejects_bad_arguments_before_allocating():
     assert sr.LIB.sr_replay_graph_run(None, 1, 10, None, None, None, None) == 1
     assert sr.LIB.sr_replay_graph_destroy(None) == 0
     assert sr.LIB.sr_replay_graph_anchors(None, 0) is None and sr.LIB.sr_replay_graph_max_rows(None) == 0
+
+
+def test_noalloc_refuses_oversized_batches_on_the_host():
+    """sr_replay_state_noalloc checks its workspace need against the scratch
+    before touching the device (this runs without a GPU)."""
+    shape = Shape(2560, 16, 32, 128, 128)
+    t_big = 16384
+    assert sr.replay_workspace_size(shape, 1, t_big) > sr.NOALLOC_SCRATCH_BYTES
+    lay = sr.SrLayer()
+    arr = (sr.SrLayer * 1)(lay)
+    st = sr.LIB.sr_replay_state_noalloc(ctypes.byref(sr.make_shape(shape)), 1, arr, 1, t_big, None, None, None)
+    assert st == 4      # SR_ERR_WORKSPACE_TOO_SMALL
+    st = sr.LIB.sr_replay_state_noalloc(None, 1, arr, 1, 8, None, None, None)
+    assert st == 1      # SR_ERR_NULL_ARG
