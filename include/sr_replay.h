@@ -35,9 +35,13 @@
  *    outputs are then undefined.  A caller treats any non-SR_OK status as a
  *    cache miss (the fail-closed rule of Section 5.2).  The library never
  *    aborts or prints.
- *  - Preconditions the host cannot check without a device read: cu_seqlens is
- *    non-decreasing with cu_seqlens[0] = 0 and cu_seqlens[n_segments] =
- *    t_total; live slot ids are distinct and < the slot count of state_out.
+ *  - The device tables are checked on the device, first thing in the call
+ *    (cu_seqlens[0] = 0, non-decreasing, cu_seqlens[n_segments] = t_total;
+ *    live slot ids < n_slots and distinct).  If the check fails, every later
+ *    kernel of the call exits without writing anything, and the reason (a
+ *    mask of sr_varlen_error bits) goes to the optional device word
+ *    varlen_status and to the first 4 bytes of the workspace; the caller
+ *    treats a non-zero mask as a cache miss.
  *  - Outputs must not alias inputs or the workspace.  Calls that share a
  *    workspace must be ordered on one stream.
  */
@@ -168,6 +172,11 @@ sr_status sr_replay_workspace_size(const sr_shape* shape, int32_t n_layers,
  *  slot_ids     device int32 [n_segments] or NULL (slot b for segment b);
  *               a negative id is the sentinel: that segment's state, tail and
  *               initial state are neither read nor written
+ *  n_slots      slots of every layer's state_out / tail_out / state_in
+ *               (0 <= n_slots <= SR_MAX_SLOTS); live slot ids must be below it
+ *  varlen_status  NULL or a device int32 that receives the table check's
+ *               result (0, or a mask of sr_varlen_error bits) when the call
+ *               runs
  *  workspace    device scratch of >= sr_replay_workspace_size() bytes,
  *               256-byte aligned
  *  stream       hipStream_t (NULL = default stream)
@@ -175,8 +184,35 @@ sr_status sr_replay_workspace_size(const sr_shape* shape, int32_t n_layers,
  * zero tail. */
 sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_layer* layers,
                           int32_t n_segments, int64_t t_total, const int32_t* cu_seqlens,
-                          const int32_t* slot_ids, void* workspace, size_t workspace_bytes,
-                          void* stream);
+                          const int32_t* slot_ids, int32_t n_slots, int32_t* varlen_status,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Reasons the device check of the varlen tables fails (Section 5.2: a bad
+ * input is a cache miss, never a corrupt write). */
+typedef enum sr_varlen_error {
+  SR_VARLEN_BAD_START = 1,       /* cu_seqlens[0] != 0                          */
+  SR_VARLEN_NOT_MONOTONE = 2,    /* cu_seqlens[b + 1] < cu_seqlens[b]           */
+  SR_VARLEN_BAD_TOTAL = 4,       /* cu_seqlens[n_segments] != t_total           */
+  SR_VARLEN_SLOT_RANGE = 8,      /* a live slot id >= n_slots                   */
+  SR_VARLEN_SLOT_DUPLICATE = 16  /* two live segments share a slot id           */
+} sr_varlen_error;
+
+/* Largest n_slots the device check accepts (its slot bitmap lives in LDS). */
+#define SR_MAX_SLOTS (1 << 19)
+
+/* The device check that sr_replay_state runs first, on its own: reads
+ * cu_seqlens [n_segments + 1] and slot_ids [n_segments] (or NULL: identity)
+ * and writes 0 or a mask of sr_varlen_error bits to the device int32
+ * *status, stream-ordered.  For debugging a serving system's tables.
+ * SR_ERR_BAD_SHAPE if n_segments < 1, t_total < 0 or n_slots is outside
+ * 0..SR_MAX_SLOTS; SR_ERR_NULL_ARG if cu_seqlens or status is NULL. */
+sr_status sr_validate_varlen(const int32_t* cu_seqlens, const int32_t* slot_ids, int32_t n_segments,
+                             int64_t t_total, int32_t n_slots, int32_t* status, void* stream);
+
+/* The same check on host arrays (host pointers, no device work): writes the
+ * mask to *mask.  Argument errors as sr_validate_varlen. */
+sr_status sr_validate_varlen_host(const int32_t* cu_seqlens, const int32_t* slot_ids, int32_t n_segments,
+                                  int64_t t_total, int32_t n_slots, int32_t* mask);
 
 /* Largest workspace sr_replay_state_noalloc() can serve (128 MiB: e.g. 4096
  * packed rows of one Qwen3.5-4B or Qwen3.6-27B linear layer). */
@@ -199,7 +235,8 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
  *    (SR_ERR_HIP if that fails); later calls reuse it. */
 sr_status sr_replay_state_noalloc(const sr_shape* shape, int32_t n_layers, const sr_layer* layers,
                                   int32_t n_segments, int64_t t_total, const int32_t* cu_seqlens,
-                                  const int32_t* slot_ids, void* stream);
+                                  const int32_t* slot_ids, int32_t n_slots, int32_t* varlen_status,
+                                  void* stream);
 
 /* Kernels the library launches, as indexed by sr_kernel_timing_read(). */
 typedef enum sr_kernel_kind {
@@ -216,7 +253,10 @@ typedef enum sr_kernel_kind {
   SR_KERNEL_ANCHOR_SEQLENS = 8,  /* sidecar: segment offsets of a gather        */
   SR_KERNEL_ANCHOR_GATHER = 9,   /* sidecar: gather of the replay anchors       */
   SR_KERNEL_DECAY_STATE = 10,    /* per-head-decay state (SR_RECURRENCE_DECAY)  */
-  SR_KERNEL_KINDS = 11
+  SR_KERNEL_GRAPH = 11,          /* graph replay: capture, launch, parameter
+                                    kernel, anchor fetch (sr_replay_graph.h)    */
+  SR_KERNEL_VALIDATE = 12,       /* device check of the varlen tables           */
+  SR_KERNEL_KINDS = 13
 } sr_kernel_kind;
 
 /* Benchmark instrumentation (not needed by the replay itself).  While

@@ -53,6 +53,12 @@ def _hip_runtimes_mapped() -> set:
         return set()
 
 
+class SrHostRange(ctypes.Structure):
+    """sr_host_range: `rows` anchor rows at host `src` -> layer `layer`, row `dst_row`."""
+    _fields_ = [("src", ctypes.c_void_p), ("layer", ctypes.c_int32), ("dst_row", ctypes.c_int64),
+                ("rows", ctypes.c_int64)]
+
+
 class SrSidecar(ctypes.Structure):
     """sr_sidecar: the anchor block pool [n_blocks][n_layers][per_page][d]."""
     _fields_ = [("pool", ctypes.c_void_p), ("n_blocks", ctypes.c_int64), ("n_layers", ctypes.c_int32),
@@ -82,11 +88,18 @@ def _load() -> ctypes.CDLL:
     lib.sr_replay_workspace_size.argtypes = [P(SrShape), ctypes.c_int32, ctypes.c_int64, P(ctypes.c_size_t)]
     lib.sr_replay_workspace_size.restype = ctypes.c_int
     lib.sr_replay_state.argtypes = [P(SrShape), ctypes.c_int32, P(SrLayer), ctypes.c_int32, ctypes.c_int64,
-                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
-                                    ctypes.c_void_p]
+                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
     lib.sr_replay_state.restype = ctypes.c_int
     lib.sr_replay_state_noalloc.argtypes = [P(SrShape), ctypes.c_int32, P(SrLayer), ctypes.c_int32,
-                                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+                                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                            ctypes.c_void_p, ctypes.c_void_p]
+    lib.sr_validate_varlen.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                       ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    lib.sr_validate_varlen.restype = ctypes.c_int
+    lib.sr_validate_varlen_host.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                            ctypes.c_int32, P(ctypes.c_int32)]
+    lib.sr_validate_varlen_host.restype = ctypes.c_int
     lib.sr_replay_state_noalloc.restype = ctypes.c_int
     lib.sr_kernel_timing_enable.argtypes = [ctypes.c_int32]
     lib.sr_kernel_timing_enable.restype = ctypes.c_int
@@ -110,15 +123,21 @@ def _load() -> ctypes.CDLL:
                                      I32P, ctypes.c_void_p]
     lib.sr_anchor_gather.restype = ctypes.c_int
     lib.sr_replay_graph_create.argtypes = [P(SrShape), ctypes.c_int32, P(SrLayer), ctypes.c_int32,
-                                           P(ctypes.c_int64), ctypes.c_int32, P(ctypes.c_void_p)]
+                                           ctypes.c_void_p, ctypes.c_int32, P(ctypes.c_int64), ctypes.c_int32,
+                                           ctypes.c_void_p, ctypes.c_size_t, P(ctypes.c_void_p)]
     lib.sr_replay_graph_create.restype = ctypes.c_int
     lib.sr_replay_graph_anchors.argtypes = [ctypes.c_void_p, ctypes.c_int32]
     lib.sr_replay_graph_anchors.restype = ctypes.c_void_p
     lib.sr_replay_graph_max_rows.argtypes = [ctypes.c_void_p]
     lib.sr_replay_graph_max_rows.restype = ctypes.c_int64
+    lib.sr_replay_graph_fetch.argtypes = [ctypes.c_void_p, P(SrHostRange), ctypes.c_int32, ctypes.c_void_p]
+    lib.sr_replay_graph_fetch.restype = ctypes.c_int
     lib.sr_replay_graph_run.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p,
-                                        ctypes.c_void_p, ctypes.c_void_p, P(ctypes.c_int32)]
+                                        ctypes.c_void_p, P(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_size_t,
+                                        ctypes.c_void_p, P(ctypes.c_int32)]
     lib.sr_replay_graph_run.restype = ctypes.c_int
+    lib.sr_replay_graph_wait.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    lib.sr_replay_graph_wait.restype = ctypes.c_int
     lib.sr_replay_graph_destroy.argtypes = [ctypes.c_void_p]
     lib.sr_replay_graph_destroy.restype = ctypes.c_int
     return lib
@@ -127,13 +146,15 @@ def _load() -> ctypes.CDLL:
 LIB = _load()
 
 EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
-                    "sr_replay_state", "sr_replay_state_noalloc", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_last_hip_error",
+                    "sr_replay_state", "sr_replay_state_noalloc", "sr_validate_varlen",
+                    "sr_validate_varlen_host", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_last_hip_error",
                     "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact", "sr_anchor_write",
                     "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
-                    "sr_replay_graph_max_rows", "sr_replay_graph_run", "sr_replay_graph_destroy")
+                    "sr_replay_graph_max_rows", "sr_replay_graph_fetch", "sr_replay_graph_run",
+                    "sr_replay_graph_wait", "sr_replay_graph_destroy")
 
 KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan", "proj_conv", "row_info", "anchor_compact",
-                "anchor_write", "anchor_seqlens", "anchor_gather", "decay_state")
+                "anchor_write", "anchor_seqlens", "anchor_gather", "decay_state", "graph", "validate")
 
 
 _RECURRENCE_CODES = {"gdn": 0, "decay": 1, 0: 0, 1: 1}
@@ -237,11 +258,20 @@ def kernel_timing_read():
     return {k: (ms[i], int(n[i])) for i, k in enumerate(KERNEL_KINDS)}
 
 
+def _n_slots(layers, n_slots):
+    """The slot count sr_replay_state checks slot ids against: given, or the
+    leading dimension of the first layer's state_out."""
+    return int(layers[0].state_out.shape[0]) if n_slots is None else int(n_slots)
+
+
 def replay_state(shape, layers: Sequence[LayerTensors], n_segments: int, t_total: int, cu_seqlens,
-                 slot_ids=None, workspace=None, workspace_bytes: Optional[int] = None, stream=None):
+                 slot_ids=None, workspace=None, workspace_bytes: Optional[int] = None, stream=None,
+                 n_slots: Optional[int] = None, varlen_status=None):
     """Enqueue sr_replay_state on `stream` (a torch.cuda.Stream, a raw
-    hipStream_t int, or None for torch's current stream).  Raises SrError on
-    a non-OK status."""
+    hipStream_t int, or None for torch's current stream).  ``n_slots``
+    defaults to state_out's leading dimension; ``varlen_status`` is an
+    optional device int32 tensor receiving the table check.  Raises SrError
+    on a non-OK status."""
     import torch  # plumbing: device memory and streams
 
     if stream is None:
@@ -255,8 +285,8 @@ def replay_state(shape, layers: Sequence[LayerTensors], n_segments: int, t_total
     sh = make_shape(shape)
     arr = make_layer_array(layers)
     status = LIB.sr_replay_state(ctypes.byref(sh), len(layers), arr, int(n_segments), int(t_total),
-                                 _ptr(cu_seqlens), _ptr(slot_ids), _ptr(workspace), int(workspace_bytes),
-                                 stream_ptr)
+                                 _ptr(cu_seqlens), _ptr(slot_ids), _n_slots(layers, n_slots), _ptr(varlen_status),
+                                 _ptr(workspace), int(workspace_bytes), stream_ptr)
     _check(status)
 
 
@@ -264,7 +294,7 @@ NOALLOC_SCRATCH_BYTES = 128 << 20      # SR_NOALLOC_SCRATCH_BYTES
 
 
 def replay_state_noalloc(shape, layers: Sequence[LayerTensors], n_segments: int, t_total: int, cu_seqlens,
-                         slot_ids=None, stream=None):
+                         slot_ids=None, stream=None, n_slots: Optional[int] = None, varlen_status=None):
     """sr_replay_state_noalloc: replay_state() on the library's own device
     scratch (no workspace argument).  Raises SrError on a non-OK status
     (SR_ERR_WORKSPACE_TOO_SMALL when the call needs more than
@@ -272,7 +302,30 @@ def replay_state_noalloc(shape, layers: Sequence[LayerTensors], n_segments: int,
     sh = make_shape(shape)
     arr = make_layer_array(layers)
     _check(LIB.sr_replay_state_noalloc(ctypes.byref(sh), len(layers), arr, int(n_segments), int(t_total),
-                                       _ptr(cu_seqlens), _ptr(slot_ids), _stream_ptr(stream)))
+                                       _ptr(cu_seqlens), _ptr(slot_ids), _n_slots(layers, n_slots),
+                                       _ptr(varlen_status), _stream_ptr(stream)))
+
+
+def validate_varlen(cu_seqlens, slot_ids, n_segments: int, t_total: int, n_slots: int, status, stream=None):
+    """sr_validate_varlen: the device check of the tables; writes 0 or a mask
+    of sr_varlen_error bits into the device int32 tensor ``status``."""
+    _check(LIB.sr_validate_varlen(_ptr(cu_seqlens), _ptr(slot_ids), int(n_segments), int(t_total), int(n_slots),
+                                  _ptr(status), _stream_ptr(stream)))
+
+
+def validate_varlen_host(cu_seqlens, slot_ids, t_total: int, n_slots: int) -> int:
+    """sr_validate_varlen_host on host int32 arrays; returns the mask."""
+    import numpy as np
+
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    sl = None if slot_ids is None else np.ascontiguousarray(slot_ids, dtype=np.int32)
+    out = ctypes.c_int32(-1)
+    _check(LIB.sr_validate_varlen_host(cu.ctypes.data, None if sl is None else sl.ctypes.data, len(cu) - 1,
+                                       int(t_total), int(n_slots), ctypes.byref(out)))
+    return int(out.value)
+
+
+VARLEN_BAD_START, VARLEN_NOT_MONOTONE, VARLEN_BAD_TOTAL, VARLEN_SLOT_RANGE, VARLEN_SLOT_DUPLICATE = 1, 2, 4, 8, 16
 
 
 # ------------------------------------------------------------ anchor sidecar
@@ -343,22 +396,30 @@ class _DevArray:
 
 
 class ReplayGraph:
-    """sr_replay_graph: graph-captured replay per total-length bucket."""
+    """sr_replay_graph: one group of layers replayed from graphs captured at
+    creation (one per total-length bucket), with host anchor fetch on a copy
+    stream and an eager path for batches no bucket holds."""
 
-    def __init__(self, shape, layers: Sequence[LayerTensors], max_segments: int, bucket_rows: Sequence[int]):
+    def __init__(self, shape, layers: Sequence[LayerTensors], max_segments: int, bucket_rows: Sequence[int],
+                 workspace=None, n_slots: Optional[int] = None, varlen_status=None):
         self.shape = shape
         # The captured graphs hold the raw weight, state and tail pointers, so
         # the tensors behind them must outlive this object: keep references.
         self._tensors = list(layers)
+        self._workspace = workspace
+        self._status = varlen_status
         self._layers = make_layer_array(layers)
         self._sh = make_shape(shape)
         rows = (ctypes.c_int64 * len(bucket_rows))(*[int(r) for r in bucket_rows])
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         h = ctypes.c_void_p()
-        _check(LIB.sr_replay_graph_create(ctypes.byref(self._sh), len(layers), self._layers, int(max_segments),
-                                          rows, len(bucket_rows), ctypes.byref(h)))
+        _check(LIB.sr_replay_graph_create(ctypes.byref(self._sh), len(layers), self._layers,
+                                          _n_slots(layers, n_slots), _ptr(varlen_status), int(max_segments),
+                                          rows, len(bucket_rows), _ptr(workspace), int(ws_bytes), ctypes.byref(h)))
         self._h = h
         self.n_layers = len(layers)
         self.max_rows = int(LIB.sr_replay_graph_max_rows(h))
+        self._pending_host = []
 
     def anchors(self, layer: int):
         """torch view [T_max][d_model] of layer `layer`'s anchor buffer."""
@@ -370,12 +431,32 @@ class ReplayGraph:
         typestr = "<f4" if _DTYPE_CODES[self.shape.anchor_dtype] == SR_F32 else "<i2"
         return torch.as_tensor(_DevArray(ptr, (self.max_rows, int(self.shape.d_model)), typestr), device="cuda")
 
-    def run(self, n_segments: int, t_total: int, cu_seqlens, slot_ids=None, stream=None) -> int:
+    def fetch(self, ranges, copy_stream):
+        """sr_replay_graph_fetch: ranges are (host tensor [rows][d_model] in
+        pinned memory, layer, dst_row).  The host tensors are kept referenced
+        until the next fetch of this object."""
+        arr = (SrHostRange * max(1, len(ranges)))()
+        for i, (src, layer, dst_row) in enumerate(ranges):
+            arr[i] = SrHostRange(src.data_ptr(), int(layer), int(dst_row), int(src.shape[0]))
+        self._pending_host = [r[0] for r in ranges]
+        _check(LIB.sr_replay_graph_fetch(self._h, arr, len(ranges), _stream_ptr(copy_stream)))
+
+    def run(self, n_segments: int, t_total: int, cu_seqlens, slot_ids=None, stream=None, eager_anchors=None,
+            eager_workspace=None) -> int:
         """Replays the batch; returns the bucket index used (-1: eager)."""
         used = ctypes.c_int32(-2)
+        ea = None
+        if eager_anchors is not None:
+            ea = (ctypes.c_void_p * len(eager_anchors))(*[_ptr(a) for a in eager_anchors])
+        ews = 0 if eager_workspace is None else eager_workspace.numel() * eager_workspace.element_size()
         _check(LIB.sr_replay_graph_run(self._h, int(n_segments), int(t_total), _ptr(cu_seqlens), _ptr(slot_ids),
-                                       _stream_ptr(stream), ctypes.byref(used)))
+                                       ea, _ptr(eager_workspace), int(ews), _stream_ptr(stream),
+                                       ctypes.byref(used)))
         return int(used.value)
+
+    def wait(self, stream=None):
+        """sr_replay_graph_wait: `stream` waits for this object's last run."""
+        _check(LIB.sr_replay_graph_wait(self._h, _stream_ptr(stream)))
 
     def close(self):
         if self._h:

@@ -48,6 +48,7 @@ __device__ __forceinline__ float sigmoid(float x) { return 1.f / (1.f + expf(-x)
 
 template <typename OUT, typename CW, typename TT, int DH>
 __global__ __launch_bounds__(kConvThreads) void conv_gate_kernel(ConvGateArgs a) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
   constexpr int CPL = DH >= 64 ? DH / 64 : 1;   // channels per lane
   constexpr int LPH = DH / CPL;                   // lanes per head
   constexpr int HPW = 64 / LPH;                   // heads per wave
@@ -215,6 +216,7 @@ __device__ __forceinline__ void load8<fp8_t>(const void* p, int64_t i, float* ou
 
 template <typename TA, typename TW, typename TT>
 __global__ __launch_bounds__(kTailThreads) void tail_kernel(TailArgs a) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
   constexpr int WMAX = 4;
   const int b = blockIdx.x;
   const int slot = a.slot_ids ? a.slot_ids[b] : b;
@@ -302,6 +304,7 @@ constexpr int kTailQWaves = 8;
 
 template <typename TW, typename TT>
 __global__ __launch_bounds__(64 * kTailQWaves) void tail_q_mfma_kernel(TailArgs a) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
   __shared__ float part[kTailQWaves - 1][16][64];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int R = a.n_seg * (a.w - 1);
@@ -350,6 +353,7 @@ __global__ __launch_bounds__(64 * kTailQWaves) void tail_q_mfma_kernel(TailArgs 
 // Zeros at tail positions before a segment's first row, every channel.
 template <typename TT>
 __global__ __launch_bounds__(256) void tail_zero_kernel(TailArgs a) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
   const int b = blockIdx.x;
   const int slot = a.slot_ids ? a.slot_ids[b] : b;
   const int w1 = a.w - 1;

@@ -75,6 +75,7 @@ __device__ int segment_of_rank(const ScanArgs& a, int rank, int* shared_sel) {
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void decay_state_kernel(ScanArgs a) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
   using C = DCfg<D>;
   constexpr int P = C::P, VPT = C::VPT, NI = C::NI, NJ = C::NJ, VPR = D / 8;
   __shared__ __attribute__((aligned(16))) char smem[4 * C::MAT];   // two buffers of K and cV

@@ -195,6 +195,7 @@ __device__ int segment_for_rank(const ScanArgs& a, int rank, int* shared_sel) {
 
 template <typename OP, int D>
 __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
   using CF = ScanCfg<OP, D>;
   using MF = Mfma<OP>;
   constexpr int NW = CF::NW, EB = CF::EB, KP = CF::KP, CP = CF::CP;

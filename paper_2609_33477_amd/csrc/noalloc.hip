@@ -9,9 +9,10 @@
 // resolves the array's address on that device with hipGetSymbolAddress (with
 // the device current) and keeps it per device; every later use goes through
 // that pointer.  The replay's kernels write every workspace byte they read
-// within a call (row info, k, v, log-decay and beta planes), so nothing needs
-// clearing between calls.  Calls that overlap on one GPU share the array and
-// race; calls on one GPU must be ordered (one stream, or explicit events).
+// within a call (the table check's flag word, row info, k, v, log-decay and
+// beta planes), so nothing needs clearing between calls.  Calls that overlap
+// on one GPU share the array and race; calls on one GPU must be ordered (one
+// stream, or explicit events).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -46,7 +47,8 @@ void* scratch_on_current_device() {
 
 extern "C" sr_status sr_replay_state_noalloc(const sr_shape* shape, int32_t n_layers, const sr_layer* layers,
                                              int32_t n_segments, int64_t t_total, const int32_t* cu_seqlens,
-                                             const int32_t* slot_ids, void* stream) {
+                                             const int32_t* slot_ids, int32_t n_slots, int32_t* varlen_status,
+                                             void* stream) {
   size_t need = 0;
   const sr_status st = sr_replay_workspace_size(shape, n_layers, t_total, &need);
   if (st != SR_OK) return st;
@@ -54,6 +56,6 @@ extern "C" sr_status sr_replay_state_noalloc(const sr_shape* shape, int32_t n_la
   if (!layers) return SR_ERR_NULL_ARG;
   void* ws = scratch_on_current_device();
   if (!ws) return SR_ERR_HIP;
-  return sr_replay_state(shape, n_layers, layers, n_segments, t_total, cu_seqlens, slot_ids, ws,
-                         (size_t)SR_NOALLOC_SCRATCH_BYTES, stream);
+  return sr_replay_state(shape, n_layers, layers, n_segments, t_total, cu_seqlens, slot_ids, n_slots, varlen_status,
+                         ws, (size_t)SR_NOALLOC_SCRATCH_BYTES, stream);
 }

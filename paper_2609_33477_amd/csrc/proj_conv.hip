@@ -190,6 +190,7 @@ __device__ __forceinline__ void store_elem(void* p, int64_t i, float v, bool is_
 
 template <typename TB, int D>
 __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, int tiles_m, int tiles_n) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
   constexpr int BROW = BT<TB>::ROW, BBLK = BT<TB>::BLKS, NS = BT<TB>::NS;
   constexpr int A_BYTES = BM * 64, B_BYTES = BN * BROW, STAGE = A_BYTES + B_BYTES;
   constexpr int LPK = 2 + BBLK;  // DMA instructions per wave per K-step
@@ -650,7 +651,8 @@ hipError_t by_head(int d, const ProjConvArgs& a, hipStream_t s) {
 }
 
 // One block per segment: position in the segment, rows left, slot.
-__global__ void row_info_kernel(const int32_t* cu, const int32_t* slot_ids, RowInfo* info) {
+__global__ void row_info_kernel(const int32_t* cu, const int32_t* slot_ids, RowInfo* info, const int32_t* err) {
+  if (err && *err) return;   // the call's table check failed: write nothing
   const int b = blockIdx.x;
   const int32_t s0 = cu[b], s1 = cu[b + 1];
   const int32_t slot = slot_ids ? slot_ids[b] : b;
@@ -667,9 +669,9 @@ __global__ void row_info_kernel(const int32_t* cu, const int32_t* slot_ids, RowI
 }  // namespace
 
 hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, RowInfo* info,
-                           hipStream_t s) {
+                           const int32_t* err, hipStream_t s) {
   if (n_seg == 0) return hipSuccess;
-  hipLaunchKernelGGL(row_info_kernel, dim3(n_seg), dim3(256), 0, s, cu, slot_ids, info);
+  hipLaunchKernelGGL(row_info_kernel, dim3(n_seg), dim3(256), 0, s, cu, slot_ids, info, err);
   return hipGetLastError();
 }
 

@@ -1,6 +1,8 @@
 // C ABI of the replay library: argument validation, workspace plan and the
 // launch sequence per call.
 //
+// Every call first runs validate (one workgroup) on the device tables; every
+// later kernel exits without writing if that check failed.
 // bf16 / fp8 path (stream-ordered):
 //   row_info       once per call: position in segment, rows left, slot per row
 //   per layer:
@@ -59,7 +61,7 @@ sr_status check_shape(const sr_shape* s) {
 
 struct Plan {
   int64_t ldp;                       // row pitch of P (floats)
-  int64_t off_p, off_info, off_k, off_v, off_g, off_b, total;
+  int64_t off_flag, off_p, off_info, off_k, off_v, off_g, off_b, total;
   int64_t k_stride, v_stride, g_stride;   // per-layer strides (elements)
   int op_dtype, op_bytes;
 };
@@ -75,6 +77,7 @@ Plan make_plan(const sr_shape* s, int32_t n_layers, int64_t T) {
   p.v_stride = hv * T * d;
   p.g_stride = hv * T;
   int64_t off = 0;
+  p.off_flag = off; off = align_up(off + 4, kAlign);   // the table check's result word
   if (p.op_dtype == SR_F32) {        // only the unfused fp32 path stores the projection
     p.off_p = off; off = align_up(off + T * p.ldp * 4, kAlign);
   } else {
@@ -146,6 +149,8 @@ hipError_t sr::timed_launch(int kind, hipStream_t s, hipError_t (*launch)(void*)
   return timed(kind, s, [&] { return launch(ctx); });
 }
 
+hipError_t sr::note_error(int kind, hipError_t e) { return note(kind, e); }
+
 namespace {
 
 sr_status check_layer(const sr_shape* s, const sr_layer& L, int64_t t_total) {
@@ -187,24 +192,25 @@ sr_status sr_replay_workspace_size(const sr_shape* shape, int32_t n_layers, int6
 }
 
 sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_layer* layers, int32_t n_segments,
-                          int64_t t_total, const int32_t* cu_seqlens, const int32_t* slot_ids, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+                          int64_t t_total, const int32_t* cu_seqlens, const int32_t* slot_ids, int32_t n_slots,
+                          int32_t* varlen_status, void* workspace, size_t workspace_bytes, void* stream) {
   sr_status st = check_shape(shape);
   if (st != SR_OK) return st;
   if (!layers) return SR_ERR_NULL_ARG;
   if (n_layers < 1 || n_layers > 256 || n_segments < 0 || t_total < 0 || t_total >= (int64_t(1) << 31))
     return SR_ERR_BAD_SHAPE;
+  if (n_slots < 0 || n_slots > SR_MAX_SLOTS) return SR_ERR_BAD_SHAPE;
   if (n_segments == 0 && t_total != 0) return SR_ERR_BAD_SHAPE;
   if (n_segments > 0 && !cu_seqlens) return SR_ERR_NULL_ARG;
   for (int l = 0; l < n_layers; ++l) {
     st = check_layer(shape, layers[l], t_total);
     if (st != SR_OK) return st;
   }
+  if (n_segments == 0) return SR_OK;     // nothing to replay, nothing written
   const Plan plan = make_plan(shape, n_layers, t_total);
   if ((size_t)plan.total > workspace_bytes) return SR_ERR_WORKSPACE_TOO_SMALL;
-  if (plan.total > 0 && !workspace) return SR_ERR_NULL_ARG;
-  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SR_ERR_MISALIGNED;
-  if (n_segments == 0) return SR_OK;
+  if (!workspace) return SR_ERR_NULL_ARG;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SR_ERR_MISALIGNED;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
@@ -216,10 +222,16 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
   float* Gb = reinterpret_cast<float*>(ws + plan.off_g);
   float* Bb = reinterpret_cast<float*>(ws + plan.off_b);
 
+  int32_t* flag = reinterpret_cast<int32_t*>(ws + plan.off_flag);
+  if (timed(SR_KERNEL_VALIDATE, s, [&] {
+        return sr::launch_validate(cu_seqlens, slot_ids, n_segments, t_total, n_slots, flag, varlen_status, s);
+      }) != hipSuccess)
+    return SR_ERR_HIP;
+
   const bool fused = plan.op_dtype == SR_BF16;
   sr::RowInfo* info = reinterpret_cast<sr::RowInfo*>(ws + plan.off_info);
   if (fused && t_total > 0) {
-    if (timed(SR_KERNEL_ROW_INFO, s, [&] { return sr::launch_row_info(cu_seqlens, slot_ids, n_segments, info, s); }) != hipSuccess)
+    if (timed(SR_KERNEL_ROW_INFO, s, [&] { return sr::launch_row_info(cu_seqlens, slot_ids, n_segments, info, flag, s); }) != hipSuccess)
       return SR_ERR_HIP;
   }
 
@@ -257,6 +269,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       f.tail_bf16 = shape->tail_dtype == SR_BF16;
       f.c_tail = c_tail;
       f.tail_kv_off = c_q;
+      f.err = flag;
       if (timed(SR_KERNEL_PROJ_CONV, s, [&] { return sr::launch_proj_conv(shape->weight_dtype, d, f, s); }) != hipSuccess)
         return SR_ERR_HIP;
     } else if (t_total > 0) {
@@ -293,6 +306,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       c.tail = w > 1 ? L.tail_out : nullptr;
       c.c_tail = c_tail;
       c.tail_kv_off = c_q;
+      c.err = flag;
       if (timed(SR_KERNEL_CONV_GATE, s, [&] { return sr::launch_conv_gate(plan.op_dtype, shape->conv_dtype, shape->tail_dtype, d, c, s); }) != hipSuccess)
         return SR_ERR_HIP;
     }
@@ -309,6 +323,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       t.w = w;
       t.tail = L.tail_out;
       t.c_tail = c_tail;
+      t.err = flag;
       if (timed(SR_KERNEL_TAIL, s, [&] { return sr::launch_tail(shape->anchor_dtype, shape->weight_dtype, shape->tail_dtype, t, s); }) != hipSuccess)
         return SR_ERR_HIP;
     }
@@ -331,6 +346,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
     a.H_k = hk;
     a.H_v = hv;
     a.n_layers = nl;
+    a.err = flag;
     for (int i = 0; i < nl; ++i) {
       a.state_in[i] = layers[l0 + i].state_in;
       a.state_out[i] = layers[l0 + i].state_out;

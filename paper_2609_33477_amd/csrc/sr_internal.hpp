@@ -60,10 +60,11 @@ struct ProjConvArgs {
   int32_t tail_bf16;
   int32_t c_tail;
   int32_t tail_kv_off;
+  const int32_t* err;   // the call's table-check flag: non-zero = write nothing
 };
 
 hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, RowInfo* info,
-                           hipStream_t s);
+                           const int32_t* err, hipStream_t s);
 hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvArgs& a, hipStream_t s);
 
 // --------------------------------------------------- conv, activations, gates
@@ -87,6 +88,7 @@ struct ConvGateArgs {
   void* tail;         // [slots][c_tail][w-1] or nullptr
   int32_t c_tail;
   int32_t tail_kv_off;  // first k channel inside the tail (q channels precede)
+  const int32_t* err;   // the call's table-check flag: non-zero = write nothing
 };
 
 hipError_t launch_conv_gate(int op_dtype, int conv_dtype, int tail_dtype, int d_head,
@@ -105,6 +107,7 @@ struct TailArgs {
   int32_t w;
   void* tail;           // [slots][c_tail][w-1]
   int32_t c_tail;
+  const int32_t* err;   // the call's table-check flag: non-zero = write nothing
 };
 
 hipError_t launch_tail(int anchor_dtype, int weight_dtype, int tail_dtype, const TailArgs& a,
@@ -126,6 +129,7 @@ struct ScanArgs {
   int32_t n_seg;
   int32_t H_k, H_v;
   int32_t n_layers;     // layers in this launch (<= kScanMaxLayers)
+  const int32_t* err;   // the call's table-check flag: non-zero = write nothing
   const float* state_in[kScanMaxLayers];
   float* state_out[kScanMaxLayers];
 };
@@ -135,10 +139,20 @@ hipError_t launch_scan_bf16(int d_head, const ScanArgs& a, hipStream_t s);
 // per-head-decay recurrence: M = 2^{G_L} M_0 + K^T diag(beta 2^{G_L - G}) V (bf16 path)
 hipError_t launch_decay_state(int d_head, const ScanArgs& a, hipStream_t s);
 
+// ------------------------------------------------------ varlen table check
+// One workgroup: writes 0 or a mask of sr_varlen_error bits to *flag and
+// *status (either may be null).
+hipError_t launch_validate(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, int64_t T, int32_t n_slots,
+                           int32_t* flag, int32_t* status, hipStream_t s);
+
 // ----------------------------------------------------------- launch timing
 // Runs launch(ctx) on stream s under the library's per-kind timing and
 // failed-launch bookkeeping (sr_kernel_timing_*, sr_last_hip_error).
 hipError_t timed_launch(int kind, hipStream_t s, hipError_t (*launch)(void*), void* ctx);
+
+// Records a failed HIP call of kernel kind `kind` for sr_last_hip_error
+// (no-op for hipSuccess); returns e.
+hipError_t note_error(int kind, hipError_t e);
 
 template <typename F>
 hipError_t timed_call(int kind, hipStream_t s, F&& f) {

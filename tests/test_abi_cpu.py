@@ -27,10 +27,12 @@ def declared_functions():
 def test_header_declares_and_library_exports_every_function():
     names = declared_functions()
     assert set(names) == {"sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
-                          "sr_replay_state", "sr_replay_state_noalloc", "sr_kernel_timing_enable", "sr_kernel_timing_read",
+                          "sr_replay_state", "sr_replay_state_noalloc", "sr_validate_varlen",
+                          "sr_validate_varlen_host", "sr_kernel_timing_enable", "sr_kernel_timing_read",
                           "sr_last_hip_error", "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact",
                           "sr_anchor_write", "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
-                          "sr_replay_graph_max_rows", "sr_replay_graph_run", "sr_replay_graph_destroy"}
+                          "sr_replay_graph_max_rows", "sr_replay_graph_fetch", "sr_replay_graph_run",
+                          "sr_replay_graph_wait", "sr_replay_graph_destroy"}
     lib = ctypes.CDLL(sr.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -96,14 +98,14 @@ def _fake_layer(**over):
     return sr.LayerTensors(**base)
 
 
-def _call(layers, shape=None, n_seg=1, t=64, cu=0xA0000, ws=0xB0000, ws_bytes=None, n_layers=None):
+def _call(layers, shape=None, n_seg=1, t=64, cu=0xA0000, ws=0xB0000, ws_bytes=None, n_layers=None, n_slots=4):
     shape = shape or Shape(256, 2, 4, 128, 128)
     if ws_bytes is None:
         ws_bytes = sr.replay_workspace_size(shape, len(layers), t)
     sh = sr.make_shape(shape)
     arr = sr.make_layer_array(layers)
     return sr.LIB.sr_replay_state(ctypes.byref(sh), len(layers) if n_layers is None else n_layers, arr,
-                                  n_seg, t, cu, None, ws, ws_bytes, None)
+                                  n_seg, t, cu, None, n_slots, None, ws, ws_bytes, None)
 
 
 def test_replay_state_host_validation():
@@ -120,7 +122,10 @@ def test_replay_state_host_validation():
     fp8 = Shape(256, 2, 4, 128, 128, weight_dtype=FP8)
     assert _call([_fake_layer()], shape=fp8) == 1            # fp8 needs scales
     assert _call([_fake_layer(s_k=1 << 20, s_v=1 << 21, s_a=1 << 22, s_b=1 << 23, w_q=1 << 24)], shape=fp8) == 1
-    assert sr.LIB.sr_replay_state(None, 1, None, 0, 0, None, None, None, 0, None) == 1
+    assert sr.LIB.sr_replay_state(None, 1, None, 0, 0, None, None, 0, None, None, 0, None) == 1
+    assert _call([_fake_layer()], n_slots=-1) == 2
+    assert _call([_fake_layer()], n_slots=(1 << 19) + 1) == 2
+    assert _call([_fake_layer()], ws=None) == 1               # a call with segments needs a workspace
 
 
 def test_replay_state_empty_batch_is_noop():
@@ -142,11 +147,20 @@ def test_replay_graph_rejects_bad_arguments_before_allocating():
     lay = (sr.SrLayer * 1)()
     h = ctypes.c_void_p()
     rows = (ctypes.c_int64 * 3)(256, 128, 1024)            # not ascending
-    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, 8, rows, 3, ctypes.byref(h)) == 2
+    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, 4, None, 8, rows, 3, None, 0, ctypes.byref(h)) == 2
     rows = (ctypes.c_int64 * 1)(256)
-    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, 0, rows, 1, ctypes.byref(h)) == 2
-    assert sr.LIB.sr_replay_graph_create(None, 1, lay, 8, rows, 1, ctypes.byref(h)) == 1
-    assert sr.LIB.sr_replay_graph_run(None, 1, 10, None, None, None, None) == 1
+    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, 4, None, 0, rows, 1, None, 0, ctypes.byref(h)) == 2
+    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, -1, None, 8, rows, 1, None, 0, ctypes.byref(h)) == 2
+    assert sr.LIB.sr_replay_graph_create(None, 1, lay, 4, None, 8, rows, 1, None, 0, ctypes.byref(h)) == 1
+    # a lent workspace below the largest bucket's need, or misaligned
+    need = sr.replay_workspace_size(W.Shape(256, 2, 4, 128, 128), 1, 256)
+    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, 4, None, 8, rows, 1, 4096, need - 1,
+                                         ctypes.byref(h)) == 4
+    assert sr.LIB.sr_replay_graph_create(ctypes.byref(sh), 1, lay, 4, None, 8, rows, 1, 4096 + 16, need,
+                                         ctypes.byref(h)) == 5
+    assert sr.LIB.sr_replay_graph_run(None, 1, 10, None, None, None, None, 0, None, None) == 1
+    assert sr.LIB.sr_replay_graph_fetch(None, None, 0, None) == 1
+    assert sr.LIB.sr_replay_graph_wait(None, None) == 1
     assert sr.LIB.sr_replay_graph_destroy(None) == 0
     assert sr.LIB.sr_replay_graph_anchors(None, 0) is None and sr.LIB.sr_replay_graph_max_rows(None) == 0
 
@@ -159,7 +173,48 @@ def test_noalloc_refuses_oversized_batches_on_the_host():
     assert sr.replay_workspace_size(shape, 1, t_big) > sr.NOALLOC_SCRATCH_BYTES
     lay = sr.SrLayer()
     arr = (sr.SrLayer * 1)(lay)
-    st = sr.LIB.sr_replay_state_noalloc(ctypes.byref(sr.make_shape(shape)), 1, arr, 1, t_big, None, None, None)
+    st = sr.LIB.sr_replay_state_noalloc(ctypes.byref(sr.make_shape(shape)), 1, arr, 1, t_big, None, None, 1, None,
+                                        None)
     assert st == 4      # SR_ERR_WORKSPACE_TOO_SMALL
-    st = sr.LIB.sr_replay_state_noalloc(None, 1, arr, 1, 8, None, None, None)
+    st = sr.LIB.sr_replay_state_noalloc(None, 1, arr, 1, 8, None, None, 1, None, None)
     assert st == 1      # SR_ERR_NULL_ARG
+
+
+# ------------------------------------------------------- varlen table check
+# (Section 5.2, fail-closed: a bad table must become a miss, not a write
+# outside a buffer).  The per-segment predicate is the one the device kernel
+# runs; here it runs on the host through sr_validate_varlen_host.
+VARLEN_CASES = [
+    # (name, cu_seqlens, slot_ids, t_total, n_slots, expected mask)
+    ("good", [0, 3, 3, 10], [2, -1, 0], 10, 3, 0),
+    ("good_identity", [0, 5, 9], None, 9, 2, 0),
+    ("good_all_sentinel", [0, 4, 8], [-1, -7], 8, 0, 0),
+    ("bad_start", [1, 3, 10], [0, 1], 10, 2, 1),
+    ("not_monotone", [0, 6, 4, 10], [0, 1, 2], 10, 3, 2),
+    ("total_short", [0, 3, 9], [0, 1], 10, 2, 4),
+    ("total_past_end", [0, 3, 12], [0, 1], 10, 2, 4),        # cu[B] > t_total: rows past the buffers
+    ("slot_range", [0, 3, 10], [0, 2], 10, 2, 8),
+    ("identity_range", [0, 3, 6, 10], None, 10, 2, 8),       # NULL slot ids: segment b writes slot b
+    ("slot_duplicate", [0, 3, 6, 10], [1, 0, 1], 10, 2, 16),
+    ("duplicate_ignores_sentinels", [0, 3, 6, 10], [-1, 0, -1], 10, 1, 0),
+    ("several", [2, 1, 7], [5, 5], 9, 3, 1 | 2 | 4 | 8),
+]
+
+
+@pytest.mark.parametrize("name,cu,slots,t,n_slots,want", VARLEN_CASES, ids=[c[0] for c in VARLEN_CASES])
+def test_varlen_check_on_the_host(name, cu, slots, t, n_slots, want):
+    assert sr.validate_varlen_host(cu, slots, t, n_slots) == want
+
+
+def test_varlen_check_many_slots_and_argument_errors():
+    import numpy as np
+    n = 5000
+    cu = np.arange(n + 1, dtype=np.int32) * 2
+    slots = np.random.default_rng(0).permutation(n).astype(np.int32)
+    assert sr.validate_varlen_host(cu, slots, 2 * n, n) == 0
+    slots[4321] = slots[17]
+    assert sr.validate_varlen_host(cu, slots, 2 * n, n) == 16
+    with pytest.raises(sr.SrError):
+        sr.validate_varlen_host([0], None, 0, 1)                  # no segment
+    with pytest.raises(sr.SrError):
+        sr.validate_varlen_host([0, 1], None, 1, (1 << 19) + 1)   # more slots than the bitmap holds
