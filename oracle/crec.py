@@ -45,6 +45,8 @@ def _load():
         lib.oracle_gdn_head.restype = None
         lib.oracle_decay_head.argtypes = common
         lib.oracle_decay_head.restype = None
+        lib.oracle_gdn_head_out.argtypes = common + [P, P, ctypes.c_int64, P, ctypes.c_int64]
+        lib.oracle_gdn_head_out.restype = None
         _lib = lib
     return _lib
 
@@ -99,3 +101,33 @@ def recurrence(kind: str, k: np.ndarray, v: np.ndarray, alpha: np.ndarray, beta:
     if L > 0:
         list(_executor().map(one, range(H)))
     return S
+
+
+def recurrence_with_outputs(k: np.ndarray, v: np.ndarray, q: np.ndarray, alpha: np.ndarray, beta: np.ndarray,
+                            S0: Optional[np.ndarray] = None):
+    """Same contract as oracle.block.gated_delta_outputs: returns (S_L
+    [H, d_v, d_k], O [L, H, d_v]) with o_t = S_t q_t."""
+    lib = _load()
+    if lib is None:
+        raise RuntimeError(f"{LIB_PATH} is not built (oracle.crec.build())")
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    alpha = np.ascontiguousarray(alpha, dtype=np.float64)
+    beta = np.ascontiguousarray(beta, dtype=np.float64)
+    L, H, dk = k.shape
+    dv = v.shape[2]
+    S = np.zeros((H, dv, dk)) if S0 is None else np.array(S0, dtype=np.float64, order="C", copy=True)
+    O = np.zeros((L, H, dv))
+    work = np.zeros((H, dv))
+    f64 = 8
+
+    def one(h: int):
+        lib.oracle_gdn_head_out(L, dk, dv, k.ctypes.data + h * dk * f64, H * dk, v.ctypes.data + h * dv * f64, H * dv,
+                                alpha.ctypes.data + h * f64, beta.ctypes.data + h * f64, H, S[h].ctypes.data,
+                                work[h].ctypes.data, q.ctypes.data + h * dk * f64, H * dk,
+                                O.ctypes.data + h * dv * f64, H * dv)
+
+    if L > 0:
+        list(_executor().map(one, range(H)))
+    return S, O

@@ -62,3 +62,23 @@ void oracle_decay_head(int64_t L, int32_t dk, int32_t dv, const double* k, int64
     }
   }
 }
+
+/* Gated DeltaNet with the per-token read-out of the layer's output
+ * (o_t = S_t q_t, the state after token t applied to that token's query):
+ * as oracle_gdn_head, and row t of the output at o + t * o_stride (d_v
+ * values), with q row t at q + t * q_stride (d_k values). */
+void oracle_gdn_head_out(int64_t L, int32_t dk, int32_t dv, const double* k, int64_t k_stride, const double* v,
+                         int64_t v_stride, const double* alpha, const double* beta, int64_t ab_stride, double* S,
+                         double* work, const double* q, int64_t q_stride, double* o, int64_t o_stride) {
+  for (int64_t t = 0; t < L; ++t) {
+    oracle_gdn_head(1, dk, dv, k + t * k_stride, k_stride, v + t * v_stride, v_stride, alpha + t * ab_stride,
+                    beta + t * ab_stride, ab_stride, S, work);
+    const double* qt = q + t * q_stride;
+    double* ot = o + t * o_stride;
+    for (int32_t i = 0; i < dv; ++i) {
+      double acc = 0.0;
+      for (int32_t j = 0; j < dk; ++j) acc += S[(int64_t)i * dk + j] * qt[j];
+      ot[i] = acc;
+    }
+  }
+}

@@ -91,3 +91,52 @@ def test_padding_rows_are_inert():
     kp = np.concatenate([k, np.zeros((pad, dk))]); vp = np.concatenate([v, np.zeros((pad, dv))])
     gp = np.concatenate([g, np.zeros(pad)]); bp = np.concatenate([beta, np.zeros(pad)])
     np.testing.assert_allclose(chunked_state(kp, vp, gp, bp, 64), token_state(k, v, g, beta), rtol=1e-12, atol=1e-14)
+
+
+def chunked_outputs(k, v, q, g, beta, C, M0=None):
+    """Per-token outputs o_i = M_i^T q_i in chunk form.  Inside a chunk from
+    M0 the state after row i is M_i = e^{G_i} M0 + sum_{j<=i} e^{G_i - G_j}
+    k_j delta_j^T, so
+        O = diag(e^G) Q M0 + (tril(Q K^T) * e^{G_i - G_j}) Delta
+    with Delta = U - W M0 as for the state."""
+    L, dk = k.shape
+    dv = v.shape[1]
+    M = np.zeros((dk, dv)) if M0 is None else M0.copy()
+    O = np.zeros((L, dv))
+    for c0 in range(0, L, C):
+        K, V, Q = k[c0:c0 + C], v[c0:c0 + C], q[c0:c0 + C]
+        gc, bc = g[c0:c0 + C], beta[c0:c0 + C]
+        n = K.shape[0]
+        G = np.cumsum(gc)
+        lower = np.tri(n, n, -1, dtype=bool)
+        dG = np.where(lower, G[:, None] - G[None, :], -np.inf)
+        A = bc[:, None] * np.exp(dG) * (K @ K.T)
+        T = np.linalg.inv(np.eye(n) + A)
+        Delta = T @ (bc[:, None] * V) - T @ ((bc * np.exp(G))[:, None] * K) @ M
+        causal = np.where(np.tri(n, n, 0, dtype=bool), np.exp(np.where(np.tri(n, n, 0, dtype=bool),
+                                                                         G[:, None] - G[None, :], 0.0)), 0.0)
+        O[c0:c0 + n] = np.exp(G)[:, None] * (Q @ M) + (causal * (Q @ K.T)) @ Delta
+        M = np.exp(G[-1]) * M + K.T @ (np.exp(G[-1] - G)[:, None] * Delta)
+    return O, M
+
+
+@pytest.mark.parametrize("L", [1, 5, 63, 64, 65, 130])
+@pytest.mark.parametrize("C", [32, 64])
+def test_chunked_outputs_equal_token_outputs(L, C):
+    """The output algebra of the group-replay kernel (chunk form) against the
+    oracle's token-by-token read-out o_t = S_t q_t, with a non-zero start
+    state; catches a strict instead of an inclusive causal mask."""
+    from oracle import block
+    r = np.random.default_rng(L * 7 + C)
+    dk, dv = 16, 8
+    k = r.standard_normal((L, dk)); k /= np.linalg.norm(k, axis=1, keepdims=True)
+    q = r.standard_normal((L, dk)) * 0.3
+    v = r.standard_normal((L, dv))
+    g = -r.uniform(0.0, 3.0, L)
+    beta = r.uniform(0, 1, L)
+    M0 = r.standard_normal((dk, dv))
+    O, M = chunked_outputs(k, v, q, g, beta, C, M0)
+    S, O_ref = block.gated_delta_outputs(k[:, None], v[:, None], q[:, None], np.exp(g)[:, None], beta[:, None],
+                                         M0.T[None])
+    np.testing.assert_allclose(O, O_ref[:, 0], rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(M, S[0].T, rtol=1e-10, atol=1e-12)
