@@ -256,7 +256,11 @@ typedef enum sr_kernel_kind {
   SR_KERNEL_GRAPH = 11,          /* graph replay: capture, launch, parameter
                                     kernel, anchor fetch (sr_replay_graph.h)    */
   SR_KERNEL_VALIDATE = 12,       /* device check of the varlen tables           */
-  SR_KERNEL_KINDS = 13
+  SR_KERNEL_RMSNORM = 13,        /* group replay: block RMSNorm (sr_group.h)    */
+  SR_KERNEL_GDN_OUTPUT = 14,     /* group replay: states and gated outputs      */
+  SR_KERNEL_GEMM_RESID = 15,     /* group replay: output / down projection      */
+  SR_KERNEL_GEMM_SWIGLU = 16,    /* group replay: MLP gate and up projections   */
+  SR_KERNEL_KINDS = 17
 } sr_kernel_kind;
 
 /* Benchmark instrumentation (not needed by the replay itself).  While

@@ -14,7 +14,7 @@ _BINDING_NAMES = {
     "replay_workspace_size", "state_bytes", "status_str", "SrSidecar", "make_sidecar", "anchor_dest_table",
     "anchor_compact", "anchor_write", "anchor_gather", "ReplayGraph", "SrHostRange", "replay_state_noalloc",
     "NOALLOC_SCRATCH_BYTES", "validate_varlen", "validate_varlen_host", "VARLEN_BAD_START", "VARLEN_NOT_MONOTONE", "VARLEN_BAD_TOTAL",
-    "VARLEN_SLOT_RANGE", "VARLEN_SLOT_DUPLICATE",
+    "VARLEN_SLOT_RANGE", "VARLEN_SLOT_DUPLICATE", "BlockTensors", "group_workspace_size", "replay_group",
 }
 
 

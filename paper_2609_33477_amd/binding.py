@@ -59,6 +59,15 @@ class SrHostRange(ctypes.Structure):
                 ("rows", ctypes.c_int64)]
 
 
+_BLOCK_FIELDS = ("w_q", "w_k", "w_v", "w_z", "w_a", "w_b", "conv_w", "a_log", "dt_bias", "norm_o", "w_o", "ln_in",
+                 "ln_post", "w_gate", "w_up", "w_down", "state_out", "tail_out")
+
+
+class SrBlock(ctypes.Structure):
+    """sr_block: one replayed block's device tensors (include/sr_group.h)."""
+    _fields_ = [(name, ctypes.c_void_p) for name in _BLOCK_FIELDS]
+
+
 class SrSidecar(ctypes.Structure):
     """sr_sidecar: the anchor block pool [n_blocks][n_layers][per_page][d]."""
     _fields_ = [("pool", ctypes.c_void_p), ("n_blocks", ctypes.c_int64), ("n_layers", ctypes.c_int32),
@@ -101,6 +110,13 @@ def _load() -> ctypes.CDLL:
                                             ctypes.c_int32, P(ctypes.c_int32)]
     lib.sr_validate_varlen_host.restype = ctypes.c_int
     lib.sr_replay_state_noalloc.restype = ctypes.c_int
+    lib.sr_group_workspace_size.argtypes = [P(SrShape), ctypes.c_int32, ctypes.c_int64, P(ctypes.c_size_t)]
+    lib.sr_group_workspace_size.restype = ctypes.c_int
+    lib.sr_replay_group.argtypes = [P(SrShape), ctypes.c_int32, ctypes.c_float, ctypes.c_int32, P(SrBlock),
+                                    ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p,
+                                    ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_size_t, ctypes.c_void_p]
+    lib.sr_replay_group.restype = ctypes.c_int
     lib.sr_kernel_timing_enable.argtypes = [ctypes.c_int32]
     lib.sr_kernel_timing_enable.restype = ctypes.c_int
     lib.sr_kernel_timing_read.argtypes = [P(ctypes.c_double), P(ctypes.c_int64)]
@@ -151,10 +167,12 @@ EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace
                     "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact", "sr_anchor_write",
                     "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
                     "sr_replay_graph_max_rows", "sr_replay_graph_fetch", "sr_replay_graph_run",
-                    "sr_replay_graph_wait", "sr_replay_graph_destroy")
+                    "sr_replay_graph_wait", "sr_replay_graph_destroy", "sr_group_workspace_size",
+                    "sr_replay_group")
 
 KERNEL_KINDS = ("proj_gemm", "conv_gate", "tail", "gdn_scan", "proj_conv", "row_info", "anchor_compact",
-                "anchor_write", "anchor_seqlens", "anchor_gather", "decay_state", "graph", "validate")
+                "anchor_write", "anchor_seqlens", "anchor_gather", "decay_state", "graph", "validate", "rmsnorm",
+                "gdn_output", "gemm_resid", "gemm_swiglu")
 
 
 _RECURRENCE_CODES = {"gdn": 0, "decay": 1, 0: 0, 1: 1}
@@ -288,6 +306,54 @@ def replay_state(shape, layers: Sequence[LayerTensors], n_segments: int, t_total
                                  _ptr(cu_seqlens), _ptr(slot_ids), _n_slots(layers, n_slots), _ptr(varlen_status),
                                  _ptr(workspace), int(workspace_bytes), stream_ptr)
     _check(status)
+
+
+# ---------------------------------------------------- group replay chaining
+@dataclass
+class BlockTensors:
+    """Device tensors of one replayed block; field names and layouts as sr_block."""
+    w_q: object
+    w_k: object
+    w_v: object
+    w_z: object
+    w_a: object
+    w_b: object
+    conv_w: object
+    a_log: object
+    dt_bias: object
+    norm_o: object
+    w_o: object
+    ln_in: object
+    ln_post: object
+    w_gate: object
+    w_up: object
+    w_down: object
+    state_out: object
+    tail_out: object = None
+
+
+def group_workspace_size(shape, d_ff: int, t_total: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(LIB.sr_group_workspace_size(ctypes.byref(make_shape(shape)), int(d_ff), int(t_total), ctypes.byref(out)))
+    return int(out.value)
+
+
+def replay_group(shape, d_ff: int, norm_eps: float, blocks: Sequence[BlockTensors], anchors, n_segments: int,
+                 t_total: int, cu_seqlens, slot_ids=None, workspace=None, workspace_bytes: Optional[int] = None,
+                 stream=None, n_slots: Optional[int] = None, varlen_status=None):
+    """sr_replay_group: every layer of one group rebuilt from its group-entry
+    anchors.  ``n_slots`` defaults to the first block's state_out leading
+    dimension.  Raises SrError on a non-OK status."""
+    arr = (SrBlock * len(blocks))()
+    for i, b in enumerate(blocks):
+        for name in _BLOCK_FIELDS:
+            setattr(arr[i], name, _ptr(getattr(b, name)))
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(LIB.sr_replay_group(ctypes.byref(make_shape(shape)), int(d_ff), float(norm_eps), len(blocks), arr,
+                               _ptr(anchors), int(n_segments), int(t_total), _ptr(cu_seqlens), _ptr(slot_ids),
+                               _n_slots(blocks, n_slots), _ptr(varlen_status), _ptr(workspace),
+                               int(workspace_bytes), _stream_ptr(stream)))
 
 
 NOALLOC_SCRATCH_BYTES = 128 << 20      # SR_NOALLOC_SCRATCH_BYTES

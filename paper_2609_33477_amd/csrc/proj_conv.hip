@@ -166,7 +166,7 @@ __device__ __forceinline__ void st_f4(lfloat* p, float x, float y, float z, floa
 __device__ __forceinline__ const uint16_t* col_scale_ptr(const ProjConvArgs& a, int n) {
   const uint16_t* p = static_cast<const uint16_t*>(a.seg[0].scale) + (n - a.seg[0].n0);
 #pragma unroll
-  for (int s = 1; s < 4; ++s)
+  for (int s = 1; s < 6; ++s)
     if (s < a.n_wseg && n >= a.seg[s].n0 && n < a.seg[s].n1) p = static_cast<const uint16_t*>(a.seg[s].scale) + (n - a.seg[s].n0);
   return p;
 }
@@ -288,7 +288,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     const int n = (n0 + row < a.N) ? n0 + row : a.N - 1;
     const char* p = static_cast<const char*>(a.seg[0].ptr);
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+    for (int s = 0; s < 6; ++s)
       if (s < a.n_wseg && n >= a.seg[s].n0 && n < a.seg[s].n1)
         p = static_cast<const char*>(a.seg[s].ptr) + ((int64_t)(n - a.seg[s].n0) * K + coff) * Elem<TB>::bytes;
     b_src[i] = p;
@@ -517,8 +517,9 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
     const int nb = n0 + 128 * wn + hd * D;   // first column of the head (wave-uniform)
     if (nb >= a.N) {
     } else if (nb < a.C_kv) {
-      // ---- k or v head: conv, SiLU, (keys) L2 norm
-      const bool is_k = nb < a.C_k;
+      // ---- q, k or v head: conv, SiLU, (queries and keys) L2 norm
+      const bool is_q = nb < a.C_q;
+      const bool is_k = nb < a.C_k;   // q or k: normalised
       if (any_tail) {
         // the raw projection of the segment's last w-1 rows is the conv state
         static_for<JB>([&](auto jj_c) {
@@ -574,12 +575,13 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
         bfly_step<4, 3, 0x128>(ss, lc);    // row_ror 8: lane ^ 8
         bfly_step<2, 4, -1>(ss, lc);       // swizzle: lane ^ 16
         const int tau = (int)(__builtin_bitreverse32((uint32_t)lc) >> 27);
-        INV[((wid * 2 + hf) * NH + hd) * 32 + tau] = -kLn2 * __builtin_amdgcn_rsqf(kLn2 * kLn2 * ss[0] + a.eps);
+        INV[((wid * 2 + hf) * NH + hd) * 32 + tau] =
+            (is_q ? -kLn2 * a.q_scale : -kLn2) * __builtin_amdgcn_rsqf(kLn2 * kLn2 * ss[0] + a.eps);
         __builtin_amdgcn_s_waitcnt(0xc07f);
       }
       // scale (1/|k| for keys), round to bf16, store two rows per pack
-      const int hh = is_k ? nb / D : (nb - a.C_k) / D;
-      uint16_t* dst = static_cast<uint16_t*>(is_k ? a.Kbuf : a.Vbuf) + ((int64_t)hh * T + t0) * D + lc;
+      const int hh = is_q ? nb / D : (is_k ? (nb - a.C_q) / D : (nb - a.C_k) / D);
+      uint16_t* dst = static_cast<uint16_t*>(is_q ? a.Qbuf : (is_k ? a.Kbuf : a.Vbuf)) + ((int64_t)hh * T + t0) * D + lc;
       const lfloat* ivp = INV + ((wid * 2 + hf) * NH + hd) * 32;
       // SIMPLE: every lane outputs rows 3..31, so only rows 0-2 need a
       // per-lane predicate
@@ -607,20 +609,33 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
       };
       if ((ofull | 7u) == ~0u) out_pass(std::true_type{});
       else out_pass(std::false_type{});
+    } else if (nb < a.C_z) {
+      // ---- z head (output gate): the raw projection, bf16, head-major
+      uint16_t* dst = static_cast<uint16_t*>(a.Zbuf) + ((int64_t)((nb - a.C_kv) / D) * T + t0) * D + lc;
+#pragma unroll
+      for (int u = 0; u < 32; u += 2) {
+        static_for<JB>([&](auto jj_c) {
+          constexpr int jj = decltype(jj_c)::value, j = hd * JB + jj;
+          const float sc = bf16_bits_to_f32(sc_raw[j]);
+          const uint32_t p = pack_bf16x2(XU(j, u) * sc, XU(j, u + 1) * sc);
+          row_store(dst + (int64_t)u * D + 32 * jj, (uint16_t)(p & 0xffffu), u);
+          row_store(dst + (int64_t)(u + 1) * D + 32 * jj, (uint16_t)(p >> 16), u + 1);
+        });
+      }
     } else {
       // ---- gate columns: G = log2 alpha from a, beta from b (no conv)
       static_for<JB>([&](auto jj_c) {
         constexpr int j = hd * JB + decltype(jj_c)::value;
         const int n = ncol + 32 * j;
         const float sc = bf16_bits_to_f32(sc_raw[j]);
-        if (n < a.C_kv + a.H_v) {
-          const int hv = n - a.C_kv;
+        if (n < a.C_z + a.H_v) {
+          const int hv = n - a.C_z;
           const float al = -__expf(a.a_log[hv]) * kLog2e, db = a.dt_bias[hv];
           float* g = a.Gbuf + (int64_t)hv * T + t0;
 #pragma unroll
           for (int u = 0; u < 32; ++u) row_store(g + u, al * softplus(XU(j, u) * sc + db), u);
         } else if (n < a.N) {
-          const int hv = n - a.C_kv - a.H_v;
+          const int hv = n - a.C_z - a.H_v;
           float* bp = a.Bbuf + (int64_t)hv * T + t0;
 #pragma unroll
           for (int u = 0; u < 32; ++u) row_store(bp + u, fast_sigmoid(XU(j, u) * sc), u);

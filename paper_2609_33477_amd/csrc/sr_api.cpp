@@ -257,8 +257,11 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       f.w = w;
       f.a_log = L.a_log;
       f.dt_bias = L.dt_bias;
+      f.C_q = 0;
       f.C_k = c_k;
       f.C_kv = c_k + c_v;
+      f.C_z = c_k + c_v;
+      f.q_scale = 1.f;
       f.H_v = hv;
       f.eps = shape->l2_eps;
       f.Kbuf = Kb + (int64_t)l * plan.k_stride * plan.op_bytes;

@@ -41,17 +41,22 @@ struct ProjConvArgs {
   const void* A;        // anchors [T][K] bf16
   int64_t T;
   int32_t K;
-  int32_t N;            // projection width C_kv + 2 H_v (columns k | v | a | b)
+  int32_t N;            // projection width: columns [q |] k | v [| z] | a | b
   int32_t n_wseg;
-  WeightSeg seg[4];
+  WeightSeg seg[6];
   const RowInfo* info;  // [T]
-  const void* conv_w;   // [C_kv][w]
+  const void* conv_w;   // [C_kv][w]: taps of the conv columns ([q |] k | v)
   int32_t conv_bf16;    // conv_w dtype: 1 bf16, 0 fp32
   int32_t w;
   const float* a_log;
   const float* dt_bias;
-  int32_t C_k, C_kv, H_v;
+  // column ranges: q [0, C_q), k [C_q, C_k), v [C_k, C_kv), z [C_kv, C_z),
+  // a [C_z, C_z + H_v), b [C_z + H_v, N); C_q = 0 and C_z = C_kv without q / z
+  int32_t C_q, C_k, C_kv, C_z, H_v;
   float eps;
+  float q_scale;        // multiplies the normalised q (d^-1/2)
+  void* Qbuf;           // [H_k][T][d] bf16 (with q columns)
+  void* Zbuf;           // [H_v][T][d] bf16 (with z columns)
   void* Kbuf;           // [H_k][T][d] bf16
   void* Vbuf;           // [H_v][T][d] bf16
   float* Gbuf;          // [H_v][T] log2 alpha per row
@@ -138,6 +143,62 @@ hipError_t launch_scan(int op_dtype, int d_head, const ScanArgs& a, hipStream_t 
 hipError_t launch_scan_bf16(int d_head, const ScanArgs& a, hipStream_t s);
 // per-head-decay recurrence: M = 2^{G_L} M_0 + K^T diag(beta 2^{G_L - G}) V (bf16 path)
 hipError_t launch_decay_state(int d_head, const ScanArgs& a, hipStream_t s);
+
+// ------------------------------------------ group replay: block GEMMs, norms
+constexpr int kGemmResid = 0, kGemmSwiglu = 1;
+
+// C = A B^T, A [M][K] bf16 row-major, B [N][K] bf16 (B2: the up weights of
+// the SwiGLU mode, B the gate weights).  kGemmResid: C fp32 [M][ldc] += acc;
+// kGemmSwiglu: C bf16 [M][ldc] = SiLU(A B^T) * (A B2^T), N = 2 * hidden.
+struct BlockGemmArgs {
+  const void* A;
+  int64_t M;
+  int32_t K, N;
+  const void* B;
+  const void* B2;
+  void* C;
+  int64_t ldc;
+  const int32_t* err;
+};
+hipError_t launch_block_gemm(int mode, const BlockGemmArgs& a, hipStream_t s);
+
+// Row RMSNorm: out[t] = bf16(x[t] / sqrt(mean(x[t]^2) + eps) * w) for x
+// bf16 (in_bf16) or fp32 rows of D; copy (optional, fp32) receives x[t].
+struct RmsNormArgs {
+  const void* x;
+  int32_t in_bf16;
+  int64_t T;
+  int32_t D;
+  const void* w;       // bf16 [D]
+  float eps;
+  void* out;           // bf16 [T][D]
+  float* copy;         // fp32 [T][D] or nullptr
+  const int32_t* err;
+};
+hipError_t launch_rmsnorm(const RmsNormArgs& a, hipStream_t s);
+
+// Chunked Gated DeltaNet with per-token outputs (one launch per layer):
+// states as the scan kernels, and y = RMSNorm_head(o) * norm_w * SiLU(z),
+// o_t = S_t q_t, into Y [T][H_v * d] bf16.
+struct OutputArgs {
+  const void* Qbuf;     // [H_k][T][d] bf16, q already scaled by d^-1/2
+  const void* Kbuf;     // [H_k][T][d]
+  const void* Vbuf;     // [H_v][T][d]
+  const void* Zbuf;     // [H_v][T][d]
+  const float* Gbuf;    // [H_v][T] log2 alpha
+  const float* Bbuf;    // [H_v][T] beta
+  int64_t T;
+  const int32_t* cu;
+  const int32_t* slot_ids;
+  int32_t n_seg;
+  int32_t H_k, H_v;
+  const void* norm_w;   // bf16 [d]
+  float eps;
+  void* Y;              // [T][H_v * d] bf16
+  float* state_out;     // [slots][H_v][d][d]
+  const int32_t* err;
+};
+hipError_t launch_gdn_output(int d_head, const OutputArgs& a, hipStream_t s);
 
 // ------------------------------------------------------ varlen table check
 // One workgroup: writes 0 or a mask of sr_varlen_error bits to *flag and

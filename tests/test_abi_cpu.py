@@ -10,7 +10,7 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADERS = [os.path.join(ROOT, "include", h) for h in ("sr_replay.h", "sr_sidecar.h", "sr_replay_graph.h")]
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("sr_replay.h", "sr_sidecar.h", "sr_replay_graph.h", "sr_group.h")]
 GOLDEN = os.path.join(ROOT, "tests", "golden", "storage_table6.json")
 
 sr = pytest.importorskip("paper_2609_33477_amd.binding",
@@ -32,7 +32,8 @@ def test_header_declares_and_library_exports_every_function():
                           "sr_last_hip_error", "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact",
                           "sr_anchor_write", "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
                           "sr_replay_graph_max_rows", "sr_replay_graph_fetch", "sr_replay_graph_run",
-                          "sr_replay_graph_wait", "sr_replay_graph_destroy"}
+                          "sr_replay_graph_wait", "sr_replay_graph_destroy", "sr_group_workspace_size",
+                          "sr_replay_group"}
     lib = ctypes.CDLL(sr.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -218,3 +219,40 @@ def test_varlen_check_many_slots_and_argument_errors():
         sr.validate_varlen_host([0], None, 0, 1)                  # no segment
     with pytest.raises(sr.SrError):
         sr.validate_varlen_host([0, 1], None, 1, (1 << 19) + 1)   # more slots than the bitmap holds
+
+
+def test_group_replay_host_checks():
+    """sr_replay_group refuses unsupported shapes and bad arguments on the
+    host (no device work)."""
+    import numpy as np
+    g = Shape(2560, 16, 32, 128, 128)
+    ws = sr.group_workspace_size(g, 9728, 4096)
+    assert ws > 0
+    with pytest.raises(sr.SrError) as e:
+        sr.group_workspace_size(Shape(2560, 16, 32, 128, 128, weight_dtype=FP8), 9728, 16)
+    assert e.value.status == 3
+    with pytest.raises(sr.SrError) as e:
+        sr.group_workspace_size(Shape(2560, 16, 32, 32, 32), 9728, 16)          # d = 32
+    assert e.value.status == 2
+    with pytest.raises(sr.SrError) as e:
+        sr.group_workspace_size(Shape(2560 + 64, 16, 32, 128, 128), 9728, 16)   # D % 256
+    assert e.value.status == 2
+    with pytest.raises(sr.SrError) as e:
+        sr.group_workspace_size(g, 9728 + 64, 16)                               # d_ff % 128
+    assert e.value.status == 2
+    fake = dict((n, 0x100000 * (i + 1)) for i, n in enumerate(sr._BLOCK_FIELDS))
+    blk = sr.BlockTensors(**fake)
+    args = dict(anchors=0x900000, n_segments=1, t_total=64, cu_seqlens=0xA00000, workspace=None,
+                workspace_bytes=0, n_slots=1, stream=0)
+    with pytest.raises(sr.SrError) as e:                                        # no workspace
+        sr.replay_group(g, 9728, 1e-6, [blk], **args)
+    assert e.value.status == 4
+    with pytest.raises(sr.SrError) as e:
+        sr.replay_group(g, 9728, 1e-6, [sr.BlockTensors(**{**fake, "w_o": None})], **args)
+    assert e.value.status == 1
+    with pytest.raises(sr.SrError) as e:
+        sr.replay_group(g, 9728, 0.0, [blk], **args)                            # eps
+    assert e.value.status == 2
+    with pytest.raises(sr.SrError) as e:
+        sr.replay_group(g, 9728, 1e-6, [blk], **{**args, "anchors": 0x900008})
+    assert e.value.status == 5

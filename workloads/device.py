@@ -65,3 +65,40 @@ def upload(wl: Workload, with_q: bool = True, state_in: Optional[List[np.ndarray
     cu = torch.from_numpy(wl.cu_seqlens).to(device)
     slots = torch.tensor(wl.slot_ids, dtype=torch.int32, device=device) if explicit_slots else None
     return DeviceWorkload(wl=wl, layers=layers, cu_seqlens=cu, slot_ids=slots, with_q=with_q)
+
+
+@dataclass
+class DeviceGroup:
+    gw: object                           # workloads.group.GroupWorkload
+    blocks: List[SimpleNamespace]        # attribute names as sr_block
+    anchors: torch.Tensor
+    cu_seqlens: torch.Tensor
+    slot_ids: Optional[torch.Tensor]
+
+
+def upload_group(gw, out_fill: float = float("nan"), device="cuda") -> DeviceGroup:
+    """Device copies of a group workload's anchors and block tensors, with
+    state and tail outputs prefilled with ``out_fill``.  The block's conv taps
+    are the q taps followed by the mixer's k | v taps ([C_tail][w])."""
+    sh = gw.shape
+    blocks = []
+    for b in gw.blocks:
+        m = b.mixer
+        ns = SimpleNamespace()
+        for name in ("q", "k", "v", "a", "b"):
+            setattr(ns, "w_" + name, to_device(getattr(m, "w_" + name), BF16, device))
+        ns.w_z = to_device(b.w_z, BF16, device)
+        ns.conv_w = to_device(np.concatenate([b.conv_q, m.conv_w]), sh.conv_dtype, device)
+        ns.a_log = to_device(m.a_log, F32, device)
+        ns.dt_bias = to_device(m.dt_bias, F32, device)
+        for name in ("norm_o", "w_o", "ln_in", "ln_post", "w_gate", "w_up", "w_down"):
+            setattr(ns, name, to_device(getattr(b, name), BF16, device))
+        ns.state_out = torch.full((gw.n_slots, sh.n_v_heads, sh.d_k, sh.d_v), out_fill, dtype=torch.float32,
+                                  device=device)
+        ns.tail_out = torch.full((gw.n_slots, sh.c_tail, sh.conv_width - 1), out_fill,
+                                 dtype=TORCH_DTYPES[sh.tail_dtype], device=device)
+        blocks.append(ns)
+    cu = torch.from_numpy(gw.cu_seqlens).to(device)
+    slots = torch.tensor(gw.slot_ids, dtype=torch.int32, device=device)
+    return DeviceGroup(gw=gw, blocks=blocks, anchors=to_device(gw.anchors, BF16, device), cu_seqlens=cu,
+                       slot_ids=slots)
