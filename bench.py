@@ -14,6 +14,7 @@ Prints ONE JSON line on stdout; progress goes to stderr.
     python bench.py --workload sidecar_gather   # anchor sidecar read path (Section 5.2)
     python bench.py --workload sidecar_write    # anchor sidecar write path (Section 5.1)
     python bench.py --workload graph_small      # graph-bucketed replay of a small batch vs eager
+    python bench.py --workload group_qwen35_4b  # group replay chaining: 3 layers from one anchor (Section 4.1)
 
 The two sidecar workloads time the sidecar's own calls instead of the replay
 and report anchor rows (x anchored layers) per second, with the HBM roofline
@@ -415,6 +416,124 @@ def bench_graph(args):
     print(json.dumps(out), flush=True)
 
 
+GROUP_SEGMENTS = [512] * 8          # 8 hits at the Qwen3.5-4B replay cap (k_max = 512): T_max = 4096 rows
+
+
+def group_work(gw):
+    """Per-launch algorithmic work of each group-replay kernel (flops for
+    the MFMA kernels, HBM bytes for the streaming ones), summed over the
+    call's launches of that kernel."""
+    sh = gw.shape
+    T, D, hk, hv, d, F = gw.t_total, sh.d_model, sh.n_k_heads, sh.n_v_heads, sh.d_k, gw.d_ff
+    n = len(gw.blocks)
+    live = [b for b, s in enumerate(gw.slot_ids) if s >= 0]
+    n_full = (hk + hk + hv + hv) * d + 2 * hv          # q | k | v | z | a | b
+    n_last = (hk + hv) * d + 2 * hv                    # k | v | a | b
+    C = 64                                             # chunk rows of the output kernel
+    per_row_head = 10 * C * d + 6 * d * d              # chunk form: 5 C^2 d-sized and 3 C d^2 products
+    return {
+        "proj_conv": ("mfma", 2.0 * T * D * (n_full * (n - 1) + n_last)),
+        "gdn_output": ("mfma_f32", float(per_row_head) * T * hv * (n - 1)),
+        "gemm_resid": ("mfma", 2.0 * T * D * (hv * d + F) * (n - 1)),
+        "gemm_swiglu": ("mfma", 2.0 * T * D * 2 * F * (n - 1)),
+        # input norm of every layer, post-mixer norm of every layer but the last
+        "rmsnorm": ("hbm", T * D * ((2 + 2 + 4) + (n - 1) * (4 + 2) + (n - 1) * (4 + 2))),
+        "gdn_scan": ("hbm", T * ((hk + hv) * d * 2 + hv * 8) + len(live) * hv * d * d * 4),
+        "tail": ("hbm", hk * d * D * 2),
+        "row_info": ("hbm", T * 16),
+        "validate": ("hbm", (2 * len(gw.seg_lens) + 1) * 4 + 4),
+    }
+
+
+def bench_group(args):
+    """Group replay chaining (Section 4.1): a 3-layer group at Qwen3.5-4B's
+    shape rebuilt from its group-entry anchors, for 8 hits of 512 anchors."""
+    import torch
+    import workloads as W
+    from workloads.device import upload_group
+    from workloads.group import make_group
+    import paper_2609_33477_amd as sr
+
+    shape = W.config_shape("varlen16")[0]
+    gw = make_group("group_qwen35_4b", shape, GROUP_SEGMENTS, seed=6)
+    dg = upload_group(gw)
+    blocks = [sr.BlockTensors(**vars(b)) for b in dg.blocks]
+    ws_bytes = sr.group_workspace_size(shape, gw.d_ff, gw.t_total)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    n_seg = len(gw.seg_lens)
+
+    def step():
+        sr.replay_group(shape, gw.d_ff, gw.norm_eps, blocks, dg.anchors, n_seg, gw.t_total, dg.cu_seqlens,
+                        dg.slot_ids, ws, ws_bytes, stream)
+
+    log(f"group: T={gw.t_total} rows x {len(blocks)} layers, d_ff {gw.d_ff}, workspace {ws_bytes / 2**20:.1f} MiB")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    sr.kernel_timing_enable(True)
+    sr.kernel_timing_read()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    kt = sr.kernel_timing_read()
+    sr.kernel_timing_enable(False)
+    ms = start.elapsed_time(stop) / args.steps
+    value = gw.replayed_tokens / (ms / 1e3)
+    log(f"{ms:.3f} ms/step, {value / 1e6:.2f} M tokens/s (rows x layers)")
+    work = group_work(gw)
+    kernels = {}
+    for k, (tot, cnt) in kt.items():
+        if cnt == 0:
+            continue
+        bound, amount = work[k]
+        step_ms = tot / args.steps                           # all launches of the kind in one step
+        if bound == "mfma":
+            ach, peak, unit = amount / (step_ms * 1e-3) / 1e12, PEAK_TFLOPS["bf16"], "TFLOP/s"
+        elif bound == "mfma_f32":
+            ach, peak, unit = amount / (step_ms * 1e-3) / 1e12, PEAK_TFLOPS["f32"], "TFLOP/s"
+        else:
+            ach, peak, unit = amount / (step_ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
+        kernels[k] = {"ms_per_step": round(step_ms, 5), "launches_per_step": cnt / args.steps,
+                      "share": round(tot / max(sum(v[0] for v in kt.values()), 1e-12), 4),
+                      "bound": "mfma" if bound.startswith("mfma") else bound, "achieved": round(ach, 2),
+                      "peak": peak, "unit": unit, "frac": round(ach / peak, 4)}
+    dom = max(kernels, key=lambda k: kernels[k]["share"])
+    dk = kernels[dom]
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import block
+        log("timing the fp64 oracle on a bounded sample")
+        t0 = time.perf_counter()
+        cu = gw.cu_seqlens
+        rows = 0
+        for b in range(n_seg):
+            if time.perf_counter() - t0 > args.cpu_budget_s:
+                break
+            block.replay_group_segment(shape, gw.blocks, gw.anchors[cu[b]:cu[b + 1]], gw.norm_eps)
+            rows += gw.seg_lens[b]
+        el = time.perf_counter() - t0
+        cpu = {"value": rows * len(blocks) / el, "unit": "tokens/s", "kind": "oracle", "cpu": cpu_model(),
+               "cores": int(os.cpu_count() or 1),
+               "sample": f"{rows} anchor rows of {n_seg} segments through {len(blocks)} layers, fp64, {el:.1f} s"}
+    out = {"metric": METRIC + " (group replay chaining)", "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": gw.name, "requests": n_seg, "anchors_per_request": GROUP_SEGMENTS[0],
+                      "layers": len(blocks), "t_total": gw.t_total, "d_model": shape.d_model,
+                      "n_k_heads": shape.n_k_heads, "n_v_heads": shape.n_v_heads, "d_k": shape.d_k,
+                      "d_ff": gw.d_ff},
+           "latency_ms": round(ms, 4),
+           "roofline": {"bound": dk["bound"], "achieved": dk["achieved"], "peak": dk["peak"], "unit": dk["unit"],
+                        "frac": dk["frac"], "traffic": None, "kernel": dom},
+           "kernels": kernels, "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -442,6 +561,9 @@ def main():
         return
     if args.workload == "graph_small":
         bench_graph(args)
+        return
+    if args.workload == "group_qwen35_4b":
+        bench_group(args)
         return
 
     import torch

@@ -54,6 +54,22 @@ struct OutCfg {
 __device__ __forceinline__ float lds_bf16(const char* base, int idx) {
   return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(base)[idx] << 16);
 }
+// four consecutive bf16 values (idx a multiple of 4) as fp32, one 8-byte read
+__device__ __forceinline__ void lds_bf16x4(const char* base, int idx, float* v) {
+  const uint2 u = *reinterpret_cast<const uint2*>(base + idx * 2);
+  v[0] = __uint_as_float(u.x << 16);
+  v[1] = __uint_as_float(u.x & 0xffff0000u);
+  v[2] = __uint_as_float(u.y << 16);
+  v[3] = __uint_as_float(u.y & 0xffff0000u);
+}
+// four consecutive fp32 values (idx a multiple of 4), one 16-byte read
+__device__ __forceinline__ void lds_f32x4(const float* base, int idx, float* v) {
+  const float4 u = *reinterpret_cast<const float4*>(base + idx);
+  v[0] = u.x;
+  v[1] = u.y;
+  v[2] = u.z;
+  v[3] = u.w;
+}
 
 // Longest-first order of the work units (ties by index, sentinel segments
 // last); natural order above kSortMax segments.
@@ -182,11 +198,13 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
       const int q = wid + nq * NW;
       if (q >= 6) continue;
       const int tq = q % 3, ti = (tq + 1) >> 1, tj = tq >> 1;
+      // K and Q are exact in bf16: bf16 MFMA with fp32 accumulation
       const char* Lsrc = q < 3 ? Ks : Qs;
-      for (int s = 0; s < D / 2; ++s) {
-        const float fa = lds_bf16(Lsrc, (32 * ti + lc) * KP + 2 * s + h2);
-        const float fb = lds_bf16(Ks, (32 * tj + lc) * KP + 2 * s + h2);
-        mma(gam[nq], fa, fb);
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        const bf16x8 fa = as_bf16x8(*reinterpret_cast<const uint4*>(Lsrc + ((32 * ti + lc) * KP + 16 * s + 8 * h2) * 2));
+        const bf16x8 fb = as_bf16x8(*reinterpret_cast<const uint4*>(Ks + ((32 * tj + lc) * KP + 16 * s + 8 * h2) * 2));
+        gam[nq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, gam[nq], 0, 0, 0);
       }
     }
     lds_barrier();
@@ -256,37 +274,45 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
       }
     }
 
+    // Operands on the k side of a state product follow the accumulator row
+    // order: step s takes rows perm_k(s, h) of a 32-row tile, i.e. four runs
+    // of four consecutive rows, so the LDS side is read 4 values at a time.
     // ---- 5. X = K M0 (this wave's columns), from the state registers
     f32x16 X[2];
 #pragma unroll
     for (int ti = 0; ti < 2; ++ti) {
       X[ti] = zero16();
 #pragma unroll
-      for (int td = 0; td < NT; ++td)
+      for (int td = 0; td < NT; ++td) {
+        float av[16];
 #pragma unroll
-        for (int s = 0; s < 16; ++s)
-        {
-          mma(X[ti], lds_bf16(Ks, (32 * ti + lc) * KP + 32 * td + perm_k(s, h2)), M[td][s]);
-          if ((s & 3) == 3) __builtin_amdgcn_sched_barrier(0);   // bounds the loads in flight
-        }
+        for (int q = 0; q < 4; ++q) lds_bf16x4(Ks, (32 * ti + lc) * KP + 32 * td + 8 * q + 4 * h2, av + 4 * q);
+#pragma unroll
+        for (int s = 0; s < 16; ++s) mma(X[ti], av[s], M[td][s]);
+      }
     }
     // ---- 6. Delta = T diag(beta) V - T diag(beta 2^G) X
     f32x16 Dl[2];
 #pragma unroll
     for (int ti = 0; ti < 2; ++ti) {
       Dl[ti] = zero16();
-      for (int s = 0; s < kC / 2; ++s) {
-        const int j = 2 * s + h2;
-        mma(Dl[ti], Tm[(32 * ti + lc) * kFP + j] * bs[j], lds_bf16(Vs, j * KP + col));
-      }
 #pragma unroll
-      for (int tj = 0; tj < 2; ++tj)
+      for (int tj = 0; tj < 2; ++tj) {
+        float tv[16], bv[16], wv[16], vv[16];
 #pragma unroll
-        for (int s = 0; s < 16; ++s) {
-          const int j = 32 * tj + perm_k(s, h2);
-          mma(Dl[ti], -Tm[(32 * ti + lc) * kFP + j] * bw[j], X[tj][s]);
-          if ((s & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+        for (int q = 0; q < 4; ++q) {
+          const int j0 = 32 * tj + 8 * q + 4 * h2;
+          lds_f32x4(Tm, (32 * ti + lc) * kFP + j0, tv + 4 * q);
+          lds_f32x4(bs, j0, bv + 4 * q);
+          lds_f32x4(bw, j0, wv + 4 * q);
         }
+#pragma unroll
+        for (int s = 0; s < 16; ++s) vv[s] = lds_bf16(Vs, (32 * tj + perm_k(s, h2)) * KP + col);
+#pragma unroll
+        for (int s = 0; s < 16; ++s) mma(Dl[ti], tv[s] * bv[s], vv[s]);
+#pragma unroll
+        for (int s = 0; s < 16; ++s) mma(Dl[ti], -tv[s] * wv[s], X[tj][s]);
+      }
     }
     // ---- 7. O = diag(2^G) Q M0 + (P o QK^T) Delta
     f32x16 O[2];
@@ -294,23 +320,23 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
     for (int ti = 0; ti < 2; ++ti) {
       O[ti] = zero16();
 #pragma unroll
-      for (int td = 0; td < NT; ++td)
+      for (int td = 0; td < NT; ++td) {
+        float av[16];
 #pragma unroll
-        for (int s = 0; s < 16; ++s)
-        {
-          mma(O[ti], lds_bf16(Qs, (32 * ti + lc) * KP + 32 * td + perm_k(s, h2)), M[td][s]);
-          if ((s & 3) == 3) __builtin_amdgcn_sched_barrier(0);
-        }
+        for (int q = 0; q < 4; ++q) lds_bf16x4(Qs, (32 * ti + lc) * KP + 32 * td + 8 * q + 4 * h2, av + 4 * q);
+#pragma unroll
+        for (int s = 0; s < 16; ++s) mma(O[ti], av[s], M[td][s]);
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) O[ti][r] *= eG[32 * ti + acc_row(r, lane)];
 #pragma unroll
-      for (int tj = 0; tj < 2; ++tj)
+      for (int tj = 0; tj < 2; ++tj) {
+        float pv[16];
 #pragma unroll
-        for (int s = 0; s < 16; ++s) {
-          const int j = 32 * tj + perm_k(s, h2);
-          mma(O[ti], Pm[(32 * ti + lc) * kFP + j], Dl[tj][s]);
-          if ((s & 3) == 3) __builtin_amdgcn_sched_barrier(0);
-        }
+        for (int q = 0; q < 4; ++q) lds_f32x4(Pm, (32 * ti + lc) * kFP + 32 * tj + 8 * q + 4 * h2, pv + 4 * q);
+#pragma unroll
+        for (int s = 0; s < 16; ++s) mma(O[ti], pv[s], Dl[tj][s]);
+      }
     }
     // ---- 8. gated output norm: per row, sum of squares over the head's d columns
 #pragma unroll
@@ -333,13 +359,13 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
 #pragma unroll
       for (int r = 0; r < 16; ++r) M[td][r] *= eGC;
 #pragma unroll
-      for (int tj = 0; tj < 2; ++tj)
+      for (int tj = 0; tj < 2; ++tj) {
+        float kv[16];
 #pragma unroll
-        for (int s = 0; s < 16; ++s) {
-          const int j = 32 * tj + perm_k(s, h2);
-          mma(M[td], lds_bf16(Ks, j * KP + 32 * td + lc), Dl[tj][s]);
-          if ((s & 3) == 3) __builtin_amdgcn_sched_barrier(0);
-        }
+        for (int s = 0; s < 16; ++s) kv[s] = lds_bf16(Ks, (32 * tj + perm_k(s, h2)) * KP + 32 * td + lc);
+#pragma unroll
+        for (int s = 0; s < 16; ++s) mma(M[td], kv[s], Dl[tj][s]);
+      }
     }
     lds_barrier();
     // ---- 10. y = o / sqrt(mean(o^2) + eps) * w * SiLU(z), rows of this chunk
