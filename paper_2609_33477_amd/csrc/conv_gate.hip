@@ -19,8 +19,10 @@
 // k and v.
 //   tail_q_mfma_kernel (bf16 anchors): one small GEMM over the gathered tail
 //     rows of all segments x the q channels, on v_mfma_f32_32x32x16_bf16
-//     (32 x 32 outputs per block, reduction split over its 8 waves, whose
-//     loads are all independent: the kernel is bound by memory latency).
+//     (32 x 32 outputs per block, reduction split over its 8 waves, each
+//     issuing a batch of independent loads before its MFMAs: the kernel is
+//     bound by memory latency); blocks of k | v channels write only the
+//     leading zeros, so the whole tail is one launch.
 //   tail_kernel (fp32 anchors): per (segment, 64 channels) dot products.
 #include "sr_device.hpp"
 
@@ -298,17 +300,44 @@ __device__ __forceinline__ int64_t tail_row(const TailArgs& a, int r, int* slot,
   return (*slot >= 0 && t >= s0) ? t : -1;
 }
 
-// Block: 32 tail rows x 32 q channels; the 4 waves split the reduction over
-// d_model in quarters and combine their accumulators through LDS.
+// Block: 32 tail rows x 32 tail channels.  For q channels (W_q is used
+// nowhere else) the 8 waves split the reduction over d_model, each issuing
+// all of its loads before its MFMAs, and combine their accumulators through
+// LDS; the block writes the q projection of each live tail row and zeros at
+// positions before a segment's first row.  Blocks of k | v channels (whose
+// rows the fused projection writes) only write those leading zeros, so one
+// launch completes the tail.
 constexpr int kTailQWaves = 8;
+constexpr int kTailKMax = 24;   // k-steps of 16 loaded per batch (all of them for d_model <= 3072)
 
 template <typename TW, typename TT>
 __global__ __launch_bounds__(64 * kTailQWaves) void tail_q_mfma_kernel(TailArgs a) {
   if (a.err && *a.err) return;   // the call's table check failed: write nothing
   __shared__ float part[kTailQWaves - 1][16][64];
+  __shared__ int row_slot[32], row_pos[32];   // per tail row of the block: slot (< 0: none), position (< 0: zero)
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int R = a.n_seg * (a.w - 1);
+  const int w1 = a.w - 1;
   const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+  if (threadIdx.x < 32) {
+    const int rr = r0 + threadIdx.x;
+    int sl = -1, ps = 0;
+    bool live = false;
+    if (rr < R) live = tail_row(a, rr, &sl, &ps) >= 0;
+    row_slot[threadIdx.x] = sl;
+    row_pos[threadIdx.x] = live ? ps : -1 - ps;
+  }
+  if (c0 >= a.c_q) {
+    // k | v channels: zeros at positions before each segment's first row
+    __syncthreads();
+    for (int e = threadIdx.x; e < 32 * 32; e += 64 * kTailQWaves) {
+      const int i = e / 32, col = c0 + e % 32;
+      const int sl = row_slot[i], pp = row_pos[i];
+      if (sl >= 0 && pp < 0 && col < a.c_tail)
+        Elem<TT>::store(a.tail, ((int64_t)sl * a.c_tail + col) * w1 + (-1 - pp), 0.f);
+    }
+    return;
+  }
   int slot, pos;
   const int r = r0 + (lane & 31);
   const int64_t t = r < R ? tail_row(a, r, &slot, &pos) : -1;
@@ -318,13 +347,21 @@ __global__ __launch_bounds__(64 * kTailQWaves) void tail_q_mfma_kernel(TailArgs 
   // 16-wide k-steps (d_model is a multiple of 64), split evenly over the waves
   const int ksteps = a.D / 16;
   const int k_lo = wid * ksteps / kTailQWaves, k_hi = (wid + 1) * ksteps / kTailQWaves;
+  // Loads are unconditional (k clamped to the wave's last step) so a batch's
+  // loads all issue before the first MFMA; surplus steps multiply zeros.
   f32x16 acc = zero16();
-#pragma unroll 10
-  for (int ks = k_lo; ks < k_hi; ++ks) {
-    const int k = 16 * ks + 8 * (lane >> 5);
-    const bf16x8 av = as_bf16x8(*reinterpret_cast<const uint4*>(xa + k));
-    const bf16x8 bv = load_w8<TW>(a.w_q, wrow + k);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
+  const bf16x8 zero8 = as_bf16x8(make_uint4(0, 0, 0, 0));
+  for (int kb = k_lo; kb < k_hi; kb += kTailKMax) {
+    bf16x8 av[kTailKMax], bv[kTailKMax];
+#pragma unroll
+    for (int i = 0; i < kTailKMax; ++i) {
+      const int k = 16 * min(kb + i, k_hi - 1) + 8 * (lane >> 5);
+      av[i] = as_bf16x8(*reinterpret_cast<const uint4*>(xa + k));
+      bv[i] = load_w8<TW>(a.w_q, wrow + k);
+    }
+#pragma unroll
+    for (int i = 0; i < kTailKMax; ++i)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb + i < k_hi ? av[i] : zero8, bv[i], acc, 0, 0, 0);
   }
   if (wid > 0) {
 #pragma unroll
@@ -339,30 +376,13 @@ __global__ __launch_bounds__(64 * kTailQWaves) void tail_q_mfma_kernel(TailArgs 
   const int col = c0 + (lane & 31);
   if (col >= a.c_q) return;
   const float scale = std::is_same<TW, fp8_t>::value ? Elem<bf16_t>::load(a.s_q, col) : 1.f;
-  const int w1 = a.w - 1;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const int rr = r0 + acc_row(i, lane);
-    if (rr >= R) continue;
-    int sl, ps;
-    if (tail_row(a, rr, &sl, &ps) >= 0)
-      Elem<TT>::store(a.tail, ((int64_t)sl * a.c_tail + col) * w1 + ps, acc[i] * scale);
-  }
-}
-
-// Zeros at tail positions before a segment's first row, every channel.
-template <typename TT>
-__global__ __launch_bounds__(256) void tail_zero_kernel(TailArgs a) {
-  if (a.err && *a.err) return;   // the call's table check failed: write nothing
-  const int b = blockIdx.x;
-  const int slot = a.slot_ids ? a.slot_ids[b] : b;
-  const int w1 = a.w - 1;
-  const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
-  const int npos = (int)min<int64_t>(w1, max<int64_t>(0, s0 - (s1 - w1)));  // leading positions to clear
-  if (slot < 0 || npos == 0) return;
-  for (int idx = threadIdx.x; idx < a.c_tail * npos; idx += blockDim.x) {
-    const int c = idx / npos, p = idx % npos;
-    Elem<TT>::store(a.tail, ((int64_t)slot * a.c_tail + c) * w1 + p, 0.f);
+    const int ri = acc_row(i, lane);
+    const int sl = row_slot[ri], pp = row_pos[ri];
+    if (sl >= 0)
+      Elem<TT>::store(a.tail, ((int64_t)sl * a.c_tail + col) * w1 + (pp >= 0 ? pp : -1 - pp),
+                      pp >= 0 ? acc[i] * scale : 0.f);
   }
 }
 
@@ -370,11 +390,8 @@ template <typename TA, typename TW, typename TT>
 hipError_t run_tail(const TailArgs& a, hipStream_t s) {
   if (a.n_seg == 0 || a.w < 2 || a.c_tail == 0) return hipSuccess;
   if constexpr (std::is_same<TA, bf16_t>::value) {
-    hipLaunchKernelGGL((tail_zero_kernel<TT>), dim3(a.n_seg), dim3(256), 0, s, a);
-    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
-    if (a.c_q == 0) return hipSuccess;
     const int R = a.n_seg * (a.w - 1);
-    dim3 grid((a.c_q + 31) / 32, (R + 31) / 32);
+    dim3 grid((a.c_tail + 31) / 32, (R + 31) / 32);
     hipLaunchKernelGGL((tail_q_mfma_kernel<TW, TT>), grid, dim3(64 * kTailQWaves), 0, s, a);
     return hipGetLastError();
   } else {
