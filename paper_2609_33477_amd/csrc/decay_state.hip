@@ -28,7 +28,6 @@ namespace {
 
 constexpr int kRows = 64;        // rows per chunk
 constexpr int kThreads = 256;    // 4 waves
-constexpr int kSortMax = 256;    // longest-first ordering up to this many segments
 
 typedef __attribute__((address_space(3))) char lchar;
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -43,35 +42,6 @@ struct DCfg {
   static constexpr int NI = TI >= 4 ? TI / 4 : 1;  // tiles per wave: NI rows x NJ columns
   static constexpr int NJ = TI >= 4 ? TI : 1;
 };
-
-// ds_read_b64_tr_b16: lane i of each 16-lane group receives rows
-// kbase .. kbase + 3 of column n0 + i when lane j of the group addresses row
-// kbase + j / 4, columns n0 + 4 (j % 4) .. + 3.
-__device__ __forceinline__ uint2 tr4(const lchar* p) {
-  const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)p);
-  return __builtin_bit_cast(uint2, v);
-}
-
-// segment of the given rank when live segments are ordered longest first
-// (ties by index); sentinel segments (slot < 0) come last
-__device__ int segment_of_rank(const ScanArgs& a, int rank, int* shared_sel) {
-  if (a.n_seg > kSortMax) return rank;
-  auto len = [&](int s) -> int {
-    const int slot = a.slot_ids ? a.slot_ids[s] : s;
-    return slot < 0 ? -1 : a.cu[s + 1] - a.cu[s];
-  };
-  for (int s = threadIdx.x; s < a.n_seg; s += blockDim.x) {
-    const int ls = len(s);
-    int r = 0;
-    for (int s2 = 0; s2 < a.n_seg; ++s2) {
-      const int l2 = len(s2);
-      r += (l2 > ls) || (l2 == ls && s2 < s);
-    }
-    if (r == rank) *shared_sel = s;
-  }
-  __syncthreads();
-  return *shared_sel;
-}
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void decay_state_kernel(ScanArgs a) {
@@ -178,13 +148,13 @@ __global__ __launch_bounds__(kThreads, 2) void decay_state_kernel(ScanArgs a) {
 #pragma unroll
       for (int x = 0; x < NI; ++x) {
         const lchar* p = Kb + (rowb * P + 16 * (it0 + x) + 4 * (j & 3)) * 2;
-        const uint2 lo = tr4(p), hi = tr4(p + 4 * P * 2);
+        const uint2 lo = lds_tr4(p), hi = lds_tr4(p + 4 * P * 2);
         fa[x] = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
       }
 #pragma unroll
       for (int y = 0; y < NJ; ++y) {
         const lchar* p = Vb + (rowb * P + 16 * (jt0 + y) + 4 * (j & 3)) * 2;
-        const uint2 lo = tr4(p), hi = tr4(p + 4 * P * 2);
+        const uint2 lo = lds_tr4(p), hi = lds_tr4(p + 4 * P * 2);
         fb[y] = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
       }
 #pragma unroll

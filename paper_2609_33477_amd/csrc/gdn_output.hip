@@ -31,7 +31,6 @@ namespace {
 
 constexpr int kC = 64;         // chunk rows
 constexpr int kFP = 68;        // fp32 pitch of A, T, P
-constexpr int kSortMax = 256;
 
 template <int D>
 struct OutCfg {
@@ -71,27 +70,6 @@ __device__ __forceinline__ void lds_f32x4(const float* base, int idx, float* v) 
   v[3] = u.w;
 }
 
-// Longest-first order of the work units (ties by index, sentinel segments
-// last); natural order above kSortMax segments.
-__device__ int segment_for_rank(const OutputArgs& a, int rank, int* shared_sel) {
-  if (a.n_seg > kSortMax) return rank;
-  auto len = [&](int s) -> int {
-    const int slot = a.slot_ids ? a.slot_ids[s] : s;
-    return slot < 0 ? -1 : a.cu[s + 1] - a.cu[s];
-  };
-  for (int s = threadIdx.x; s < a.n_seg; s += blockDim.x) {
-    const int ls = len(s);
-    int r = 0;
-    for (int s2 = 0; s2 < a.n_seg; ++s2) {
-      const int l2 = len(s2);
-      r += (l2 > ls) || (l2 == ls && s2 < s);
-    }
-    if (r == rank) *shared_sel = s;
-  }
-  __syncthreads();
-  return *shared_sel;
-}
-
 __device__ __forceinline__ float silu(float x) { return x * __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
 
 __device__ __forceinline__ void mma(f32x16& c, float a, float b) {
@@ -128,7 +106,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
   const int u = blockIdx.x;
   const int head = u % a.H_v;
   const int rank = u / a.H_v;
-  const int b = segment_for_rank(a, rank, &sel);
+  const int b = segment_of_rank(a, rank, &sel);
   const int slot = a.slot_ids ? a.slot_ids[b] : b;
   if (slot < 0) return;
   const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];

@@ -39,7 +39,6 @@ namespace {
 
 constexpr int kC = 64;       // chunk rows
 constexpr int kFP = 68;      // fp32 pitch of A and T
-constexpr int kSortMax = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 
 template <typename OP, int D>
@@ -171,28 +170,6 @@ __device__ __forceinline__ void store_transposed<float>(char* base, int pitch, i
   p[(col + 3) * pitch + row] = __uint_as_float(v.w);
 }
 
-// Longest-first schedule: the segment holding `rank` in descending length
-// order (ties by index, sentinel segments last).  Natural order above
-// kSortMax segments.
-__device__ int segment_for_rank(const ScanArgs& a, int rank, int* shared_sel) {
-  if (a.n_seg > kSortMax) return rank;
-  auto len = [&](int s) -> int {
-    const int slot = a.slot_ids ? a.slot_ids[s] : s;
-    return slot < 0 ? -1 : a.cu[s + 1] - a.cu[s];
-  };
-  for (int s = threadIdx.x; s < a.n_seg; s += blockDim.x) {
-    const int ls = len(s);
-    int r = 0;
-    for (int s2 = 0; s2 < a.n_seg; ++s2) {
-      const int l2 = len(s2);
-      r += (l2 > ls) || (l2 == ls && s2 < s);
-    }
-    if (r == rank) *shared_sel = s;
-  }
-  __syncthreads();
-  return *shared_sel;
-}
-
 template <typename OP, int D>
 __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
   if (a.err && *a.err) return;   // the call's table check failed: write nothing
@@ -225,7 +202,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
   const int head = u % a.H_v;
   const int layer = (u / a.H_v) % a.n_layers;
   const int rank = u / (a.H_v * a.n_layers);
-  const int b = segment_for_rank(a, rank, &sel);
+  const int b = segment_of_rank(a, rank, &sel);
   const int slot = a.slot_ids ? a.slot_ids[b] : b;
   if (slot < 0) return;
   const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];

@@ -54,7 +54,6 @@ constexpr int kC = 64;       // rows staged per step
 constexpr int kS = 32;       // sub-chunk rows
 constexpr int kAP = 36;      // fp32 pitch of a sub-chunk's A (rows read as float4)
 constexpr int kTP = 48;      // bf16 pitch of the T^T blocks (transposed reads)
-constexpr int kSortMax = 256;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
@@ -84,13 +83,6 @@ __device__ __forceinline__ void lds_stf4(lchar* p, const float* v) {
 }
 __device__ __forceinline__ void lds_st8(lchar* p, const uint2& v) {
   *reinterpret_cast<SR_LDS nu32x2*>(p) = __builtin_bit_cast(nu32x2, v);
-}
-
-// Transposed read (see the file comment); `p` includes the lane part of the
-// address.
-__device__ __forceinline__ uint2 tr4(const lchar* p) {
-  const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SR_LDS v4i16*)p);
-  return __builtin_bit_cast(uint2, v);
 }
 
 __device__ __forceinline__ bf16x8 join(uint2 lo, uint2 hi, bool negate) {
@@ -179,25 +171,6 @@ __device__ __forceinline__ int kv_off(int r, int cb, int h) {
   return r * 2 * D + 32 * (cb ^ ((r / RPL) % NCP)) + 8 * h;
 }
 
-__device__ int rank_to_segment(const ScanArgs& a, int rank, int* shared_sel) {
-  if (a.n_seg > kSortMax) return rank;
-  auto len = [&](int s) -> int {
-    const int slot = a.slot_ids ? a.slot_ids[s] : s;
-    return slot < 0 ? -1 : a.cu[s + 1] - a.cu[s];
-  };
-  for (int s = threadIdx.x; s < a.n_seg; s += blockDim.x) {
-    const int ls = len(s);
-    int r = 0;
-    for (int s2 = 0; s2 < a.n_seg; ++s2) {
-      const int l2 = len(s2);
-      r += (l2 > ls) || (l2 == ls && s2 < s);
-    }
-    if (r == rank) *shared_sel = s;
-  }
-  __syncthreads();
-  return *shared_sel;
-}
-
 template <int D>
 __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(ScanArgs a) {
   if (a.err && *a.err) return;   // the call's table check failed: write nothing
@@ -226,7 +199,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int head = u % a.H_v;
   const int layer = (u / a.H_v) % a.n_layers;
   const int rank = u / (a.H_v * a.n_layers);
-  const int b = rank_to_segment(a, rank, &sel);
+  const int b = segment_of_rank(a, rank, &sel);
   const int slot = a.slot_ids ? a.slot_ids[b] : b;
   if (slot < 0) return;
   const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
@@ -253,7 +226,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   // A 32-wide reduction operand from a transposed-read matrix: rows
   // kbase + {4g..4g+3} and kbase + 16 + {4g..4g+3} of the lane's column.
   auto tr_pair = [&](const lchar* p, int pitch_bytes, bool negate) {
-    return join(tr4(p), tr4(p + 16 * pitch_bytes), negate);
+    return join(lds_tr4(p), lds_tr4(p + 16 * pitch_bytes), negate);
   };
   // the same for column block cb (16 columns) of a K or V sub-chunk
   auto tr_kv = [&](const lchar* base, int cb) { return tr_pair(base + kv_off<D>(tr_row, cb, tr_h), 2 * D, false); };

@@ -149,4 +149,40 @@ __device__ __forceinline__ void wait_vm() {
 
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
+// ds_read_b64_tr_b16: lane i of each 16-lane group receives rows
+// kbase .. kbase + 3 of column n0 + i (4 bf16) when lane j of the group
+// addresses row kbase + j / 4, columns n0 + 4 (j % 4) .. + 3.
+__device__ __forceinline__ uint2 lds_tr4(const __attribute__((address_space(3))) char* p) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  const v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)p);
+  return __builtin_bit_cast(uint2, v);
+}
+
+// Work units are ordered longest segment first, so the longest serial chain
+// starts first.  Returns the segment holding `rank` when the live segments
+// are ordered by descending length (ties by index, sentinel segments last);
+// the natural order above kSortMax segments.  Every thread of the block must
+// call it: it ends with a barrier.  A: any argument block with n_seg, cu and
+// slot_ids.
+constexpr int kSortMax = 256;
+template <typename A>
+__device__ int segment_of_rank(const A& a, int rank, int* shared_sel) {
+  if (a.n_seg > kSortMax) return rank;
+  auto len = [&](int s) -> int {
+    const int slot = a.slot_ids ? a.slot_ids[s] : s;
+    return slot < 0 ? -1 : a.cu[s + 1] - a.cu[s];
+  };
+  for (int s = threadIdx.x; s < a.n_seg; s += blockDim.x) {
+    const int ls = len(s);
+    int r = 0;
+    for (int s2 = 0; s2 < a.n_seg; ++s2) {
+      const int l2 = len(s2);
+      r += (l2 > ls) || (l2 == ls && s2 < s);
+    }
+    if (r == rank) *shared_sel = s;
+  }
+  __syncthreads();
+  return *shared_sel;
+}
+
 }  // namespace sr
