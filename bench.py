@@ -59,14 +59,18 @@ def algorithmic_work(wl, with_q=True):
     live = [b for b, s in enumerate(wl.slot_ids) if s >= 0]
     n_layers = len(wl.layers)
     c_q = hk * d if with_q else 0
+    tail_rows = len(live) * (w - 1)
     return {
         # one launch per layer
         "proj_gemm": ("mfma", 2.0 * T * D * N),
         "conv_gate": ("hbm", T * N * 4 + T * c_kv * es + 2 * T * hv * 4),
         # fused projection + conv epilogue: the contraction is the bound; its
-        # HBM traffic is anchors + weights in, k_hat | v | G | beta out
-        "proj_conv": ("mfma", 2.0 * T * D * N),
-        "tail": ("hbm", c_q * D * wb + len(live) * (w - 1) * ((c_q + c_kv) * tb + D * es)),
+        # HBM traffic is anchors + weights in, k_hat | v | G | beta out.  The
+        # q part of the conv tail (a GEMM over the live segments' last w-1
+        # rows) runs in the same grid.
+        "proj_conv": ("mfma", 2.0 * T * D * N + 2.0 * tail_rows * D * c_q),
+        # fp32 anchors: the tail's own launch
+        "tail": ("hbm", c_q * D * wb + tail_rows * ((c_q + c_kv) * tb + D * es)),
         # one launch per call: 16 bytes of segment info per row
         "row_info": ("hbm", T * 16),
         # one launch per call: the varlen tables in, one flag word out
@@ -80,7 +84,7 @@ def algorithmic_work(wl, with_q=True):
 
 # sources each kernel is built from (the traffic record is void once they change)
 KERNEL_SOURCES = {
-    "proj_conv": ("proj_conv.hip", "sr_device.hpp", "sr_internal.hpp"),
+    "proj_conv": ("proj_conv.hip", "tail_q.hpp", "sr_device.hpp", "sr_internal.hpp"),
     "gdn_scan": ("gdn_scan_bf16.hip", "sr_device.hpp", "sr_internal.hpp"),
     "proj_gemm": ("proj_gemm.hip", "sr_device.hpp", "sr_internal.hpp"),
     "decay_state": ("decay_state.hip", "sr_device.hpp", "sr_internal.hpp"),
@@ -431,15 +435,16 @@ def group_work(gw):
     n_last = (hk + hv) * d + 2 * hv                    # k | v | a | b
     C = 64                                             # chunk rows of the output kernel
     per_row_head = 10 * C * d + 6 * d * d              # chunk form: 5 C^2 d-sized and 3 C d^2 products
+    tail_rows = len(live) * (sh.conv_width - 1)
     return {
-        "proj_conv": ("mfma", 2.0 * T * D * (n_full * (n - 1) + n_last)),
+        # the last layer's projection grid also runs the q part of the conv tail
+        "proj_conv": ("mfma", 2.0 * T * D * (n_full * (n - 1) + n_last) + 2.0 * tail_rows * D * hk * d),
         "gdn_output": ("mfma_f32", float(per_row_head) * T * hv * (n - 1)),
         "gemm_resid": ("mfma", 2.0 * T * D * (hv * d + F) * (n - 1)),
         "gemm_swiglu": ("mfma", 2.0 * T * D * 2 * F * (n - 1)),
         # input norm of every layer, post-mixer norm of every layer but the last
         "rmsnorm": ("hbm", T * D * ((2 + 2 + 4) + (n - 1) * (4 + 2) + (n - 1) * (4 + 2))),
         "gdn_scan": ("hbm", T * ((hk + hv) * d * 2 + hv * 8) + len(live) * hv * d * d * 4),
-        "tail": ("hbm", hk * d * D * 2),
         "row_info": ("hbm", T * 16),
         "validate": ("hbm", (2 * len(gw.seg_lens) + 1) * 4 + 4),
     }

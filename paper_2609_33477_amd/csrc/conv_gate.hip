@@ -13,17 +13,11 @@
 // Outputs are head-major ([H][T][d], [H][T]) so the scan reads each 64-row
 // chunk of a head as one contiguous block.
 //
-// Conv tail, q part (W_q is used nowhere else): the q projections of every
-// segment's last w-1 rows, and zeros at positions before a segment's first
-// row (every channel).  The k | v channels of existing rows are written with
-// k and v.
-//   tail_q_mfma_kernel (bf16 anchors): one small GEMM over the gathered tail
-//     rows of all segments x the q channels, on v_mfma_f32_32x32x16_bf16
-//     (32 x 32 outputs per block, reduction split over its 8 waves, each
-//     issuing a batch of independent loads before its MFMAs: the kernel is
-//     bound by memory latency); blocks of k | v channels write only the
-//     leading zeros, so the whole tail is one launch.
-//   tail_kernel (fp32 anchors): per (segment, 64 channels) dot products.
+// tail_kernel (fp32 anchors): per (segment, 64 channels), the q projections
+// of the segment's last w-1 rows as dot products (W_q is used nowhere else),
+// and zeros at positions before the segment's first row (every channel); the
+// k | v channels of existing rows are written with k and v.  With bf16
+// anchors the tail is computed inside the fused projection's grid.
 #include "sr_device.hpp"
 
 #include <type_traits>
@@ -190,30 +184,11 @@ constexpr int kTailChannels = 64;
 template <typename T>
 __device__ __forceinline__ void load8(const void* p, int64_t i, float* out);
 template <>
-__device__ __forceinline__ void load8<bf16_t>(const void* p, int64_t i, float* out) {
-  const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i);
-  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    out[2 * j] = bf16_bits_to_f32(w[j] & 0xffffu);
-    out[2 * j + 1] = bf16_bits_to_f32(w[j] >> 16);
-  }
-}
-template <>
 __device__ __forceinline__ void load8<float>(const void* p, int64_t i, float* out) {
   const float4* q = reinterpret_cast<const float4*>(static_cast<const float*>(p) + i);
   const float4 x = q[0], y = q[1];
   out[0] = x.x; out[1] = x.y; out[2] = x.z; out[3] = x.w;
   out[4] = y.x; out[5] = y.y; out[6] = y.z; out[7] = y.w;
-}
-template <>
-__device__ __forceinline__ void load8<fp8_t>(const void* p, int64_t i, float* out) {
-  const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p) + i);
-  const uint32_t w[2] = {v.x, v.y};
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) out[4 * j + q] = e4m3_to_f32((w[j] >> (8 * q)) & 0xffu);
 }
 
 template <typename TA, typename TW, typename TT>
@@ -269,143 +244,17 @@ __global__ __launch_bounds__(kTailThreads) void tail_kernel(TailArgs a) {
   }
 }
 
-// 8 consecutive weights at element i as a bf16 MFMA operand (fp8: exact)
-template <typename TW>
-__device__ __forceinline__ bf16x8 load_w8(const void* p, int64_t i);
-template <>
-__device__ __forceinline__ bf16x8 load_w8<bf16_t>(const void* p, int64_t i) {
-  return as_bf16x8(*reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i));
-}
-template <>
-__device__ __forceinline__ bf16x8 load_w8<fp8_t>(const void* p, int64_t i) {
-  const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p) + i);
-  uint4 o;
-  o.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, false));
-  o.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, true));
-  o.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, false));
-  o.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, true));
-  return as_bf16x8(o);
-}
-
-// Tail row r = (segment r / (w-1), position r % (w-1)) -> anchor row, or -1
-// when the position precedes the segment's first row or the slot is a
-// sentinel.
-__device__ __forceinline__ int64_t tail_row(const TailArgs& a, int r, int* slot, int* pos) {
-  const int w1 = a.w - 1;
-  const int b = r / w1;
-  *pos = r - b * w1;
-  *slot = a.slot_ids ? a.slot_ids[b] : b;
-  const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
-  const int64_t t = s1 - w1 + *pos;
-  return (*slot >= 0 && t >= s0) ? t : -1;
-}
-
-// Block: 32 tail rows x 32 tail channels.  For q channels (W_q is used
-// nowhere else) the 8 waves split the reduction over d_model, each issuing
-// all of its loads before its MFMAs, and combine their accumulators through
-// LDS; the block writes the q projection of each live tail row and zeros at
-// positions before a segment's first row.  Blocks of k | v channels (whose
-// rows the fused projection writes) only write those leading zeros, so one
-// launch completes the tail.
-constexpr int kTailQWaves = 8;
-constexpr int kTailKMax = 24;   // k-steps of 16 loaded per batch (all of them for d_model <= 3072)
-
-template <typename TW, typename TT>
-__global__ __launch_bounds__(64 * kTailQWaves) void tail_q_mfma_kernel(TailArgs a) {
-  if (a.err && *a.err) return;   // the call's table check failed: write nothing
-  __shared__ float part[kTailQWaves - 1][16][64];
-  __shared__ int row_slot[32], row_pos[32];   // per tail row of the block: slot (< 0: none), position (< 0: zero)
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int R = a.n_seg * (a.w - 1);
-  const int w1 = a.w - 1;
-  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
-  if (threadIdx.x < 32) {
-    const int rr = r0 + threadIdx.x;
-    int sl = -1, ps = 0;
-    bool live = false;
-    if (rr < R) live = tail_row(a, rr, &sl, &ps) >= 0;
-    row_slot[threadIdx.x] = sl;
-    row_pos[threadIdx.x] = live ? ps : -1 - ps;
-  }
-  if (c0 >= a.c_q) {
-    // k | v channels: zeros at positions before each segment's first row
-    __syncthreads();
-    for (int e = threadIdx.x; e < 32 * 32; e += 64 * kTailQWaves) {
-      const int i = e / 32, col = c0 + e % 32;
-      const int sl = row_slot[i], pp = row_pos[i];
-      if (sl >= 0 && pp < 0 && col < a.c_tail)
-        Elem<TT>::store(a.tail, ((int64_t)sl * a.c_tail + col) * w1 + (-1 - pp), 0.f);
-    }
-    return;
-  }
-  int slot, pos;
-  const int r = r0 + (lane & 31);
-  const int64_t t = r < R ? tail_row(a, r, &slot, &pos) : -1;
-  const int c = min(c0 + (lane & 31), a.c_q - 1);
-  const uint16_t* xa = static_cast<const uint16_t*>(a.anchors) + (t >= 0 ? t : 0) * a.D;
-  const int64_t wrow = (int64_t)c * a.D;
-  // 16-wide k-steps (d_model is a multiple of 64), split evenly over the waves
-  const int ksteps = a.D / 16;
-  const int k_lo = wid * ksteps / kTailQWaves, k_hi = (wid + 1) * ksteps / kTailQWaves;
-  // Loads are unconditional (k clamped to the wave's last step) so a batch's
-  // loads all issue before the first MFMA; surplus steps multiply zeros.
-  f32x16 acc = zero16();
-  const bf16x8 zero8 = as_bf16x8(make_uint4(0, 0, 0, 0));
-  for (int kb = k_lo; kb < k_hi; kb += kTailKMax) {
-    bf16x8 av[kTailKMax], bv[kTailKMax];
-#pragma unroll
-    for (int i = 0; i < kTailKMax; ++i) {
-      const int k = 16 * min(kb + i, k_hi - 1) + 8 * (lane >> 5);
-      av[i] = as_bf16x8(*reinterpret_cast<const uint4*>(xa + k));
-      bv[i] = load_w8<TW>(a.w_q, wrow + k);
-    }
-#pragma unroll
-    for (int i = 0; i < kTailKMax; ++i)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb + i < k_hi ? av[i] : zero8, bv[i], acc, 0, 0, 0);
-  }
-  if (wid > 0) {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) part[wid - 1][i][lane] = acc[i];
-  }
-  __syncthreads();
-  if (wid > 0) return;
-#pragma unroll
-  for (int w = 0; w < kTailQWaves - 1; ++w)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) acc[i] += part[w][i][lane];
-  const int col = c0 + (lane & 31);
-  if (col >= a.c_q) return;
-  const float scale = std::is_same<TW, fp8_t>::value ? Elem<bf16_t>::load(a.s_q, col) : 1.f;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int ri = acc_row(i, lane);
-    const int sl = row_slot[ri], pp = row_pos[ri];
-    if (sl >= 0)
-      Elem<TT>::store(a.tail, ((int64_t)sl * a.c_tail + col) * w1 + (pp >= 0 ? pp : -1 - pp),
-                      pp >= 0 ? acc[i] * scale : 0.f);
-  }
-}
-
 template <typename TA, typename TW, typename TT>
 hipError_t run_tail(const TailArgs& a, hipStream_t s) {
   if (a.n_seg == 0 || a.w < 2 || a.c_tail == 0) return hipSuccess;
-  if constexpr (std::is_same<TA, bf16_t>::value) {
-    const int R = a.n_seg * (a.w - 1);
-    dim3 grid((a.c_tail + 31) / 32, (R + 31) / 32);
-    hipLaunchKernelGGL((tail_q_mfma_kernel<TW, TT>), grid, dim3(64 * kTailQWaves), 0, s, a);
-    return hipGetLastError();
-  } else {
-    dim3 grid(a.n_seg, (a.c_tail + kTailChannels - 1) / kTailChannels);
-    hipLaunchKernelGGL((tail_kernel<TA, TW, TT>), grid, dim3(kTailThreads), 0, s, a);
-    return hipGetLastError();
-  }
+  dim3 grid(a.n_seg, (a.c_tail + kTailChannels - 1) / kTailChannels);
+  hipLaunchKernelGGL((tail_kernel<TA, TW, TT>), grid, dim3(kTailThreads), 0, s, a);
+  return hipGetLastError();
 }
 
 template <typename TT>
 hipError_t tail_by_input(int ad, int wd, const TailArgs& a, hipStream_t s) {
   if (ad == SR_F32 && wd == SR_F32) return run_tail<float, float, TT>(a, s);
-  if (ad == SR_BF16 && wd == SR_BF16) return run_tail<bf16_t, bf16_t, TT>(a, s);
-  if (ad == SR_BF16 && wd == SR_FP8_E4M3) return run_tail<bf16_t, fp8_t, TT>(a, s);
   return hipErrorInvalidValue;
 }
 

@@ -45,7 +45,12 @@
 // start, a segment end (the conv tail) or the tile edge take masked
 // variants decided per row for the whole wave.  The segment info and conv
 // taps the epilogue needs are loaded before the main loop.
+//
+// Blocks past the tiles compute the q part of the conv tail and the tail's
+// leading zeros (tail_q.hpp): they need nothing the tiles write, so they run
+// in the grid's last, partial round or on CUs the tiles leave idle.
 #include "sr_device.hpp"
+#include "tail_q.hpp"
 
 #include <type_traits>
 #include <utility>
@@ -198,6 +203,12 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   constexpr int LDS = NS * STAGE > EPI_OFF + EPI_BYTES ? NS * STAGE : EPI_OFF + EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem_raw[LDS];
   lchar* smem = (lchar*)smem_raw;
+  static_assert(LDS >= kTqLds && THREADS == 64 * kTqWaves, "q-tail blocks share the tile's LDS and waves");
+  if ((int)blockIdx.x >= tiles_m * tiles_n) {
+    const int b = (int)blockIdx.x - tiles_m * tiles_n, gx = tail_q_grid_x(a.tq);
+    tail_q_block<TB>(a.tq, b % gx, b / gx, smem_raw);
+    return;
+  }
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
@@ -648,10 +659,11 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
 
 template <typename TB, int D>
 hipError_t run(const ProjConvArgs& a, hipStream_t s) {
-  if (a.T == 0) return hipSuccess;
   if (a.K % BK) return hipErrorInvalidValue;
   const int tm = (int)((a.T + SM - 1) / SM), tn = (a.N + BN - 1) / BN;
-  hipLaunchKernelGGL((proj_conv_kernel<TB, D>), dim3(tm * tn), dim3(THREADS), 0, s, a, tm, tn);
+  const int blocks = tm * tn + a.tq_blocks;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL((proj_conv_kernel<TB, D>), dim3(blocks), dim3(THREADS), 0, s, a, tm, tn);
   return hipGetLastError();
 }
 

@@ -243,7 +243,23 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
                                    {L.w_v, L.s_v, c_k, c_k + c_v},
                                    {L.w_a, L.s_a, c_k + c_v, c_k + c_v + hv},
                                    {L.w_b, L.s_b, c_k + c_v + hv, c_k + c_v + 2 * hv}};
-    if (t_total > 0 && fused) {
+    const bool with_tail = L.tail_out && w > 1;
+    sr::TailArgs t{};
+    t.anchors = L.anchors;
+    t.D = shape->d_model;
+    t.w_q = L.w_q;
+    t.s_q = L.s_q;
+    t.c_q = c_q;
+    t.cu = cu_seqlens;
+    t.slot_ids = slot_ids;
+    t.n_seg = n_segments;
+    t.w = w;
+    t.tail = L.tail_out;
+    t.tail_bf16 = shape->tail_dtype == SR_BF16;
+    t.c_tail = c_tail;
+    t.err = flag;
+    if (fused && (t_total > 0 || with_tail)) {
+      // the q-tail blocks ride in the projection's grid (alone when T = 0)
       sr::ProjConvArgs f{};
       f.A = L.anchors;
       f.T = t_total;
@@ -273,6 +289,10 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       f.c_tail = c_tail;
       f.tail_kv_off = c_q;
       f.err = flag;
+      if (with_tail) {
+        f.tq = t;
+        f.tq_blocks = sr::tail_q_grid_x(t) * sr::tail_q_grid_y(t);
+      }
       if (timed(SR_KERNEL_PROJ_CONV, s, [&] { return sr::launch_proj_conv(shape->weight_dtype, d, f, s); }) != hipSuccess)
         return SR_ERR_HIP;
     } else if (t_total > 0) {
@@ -313,20 +333,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       if (timed(SR_KERNEL_CONV_GATE, s, [&] { return sr::launch_conv_gate(plan.op_dtype, shape->conv_dtype, shape->tail_dtype, d, c, s); }) != hipSuccess)
         return SR_ERR_HIP;
     }
-    if (L.tail_out && w > 1) {
-      sr::TailArgs t{};
-      t.anchors = L.anchors;
-      t.D = shape->d_model;
-      t.w_q = L.w_q;
-      t.s_q = L.s_q;
-      t.c_q = c_q;
-      t.cu = cu_seqlens;
-      t.slot_ids = slot_ids;
-      t.n_seg = n_segments;
-      t.w = w;
-      t.tail = L.tail_out;
-      t.c_tail = c_tail;
-      t.err = flag;
+    if (with_tail && !fused) {
       if (timed(SR_KERNEL_TAIL, s, [&] { return sr::launch_tail(shape->anchor_dtype, shape->weight_dtype, shape->tail_dtype, t, s); }) != hipSuccess)
         return SR_ERR_HIP;
     }

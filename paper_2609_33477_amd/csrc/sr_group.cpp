@@ -13,7 +13,7 @@
 //     gemm resid  h += m W_down^T
 //     rmsnorm     h -> x (the next layer's input, its ln_in)
 //   last layer: the state-only path of sr_replay_state (projection without
-//   q / z, q part of the tail, chunked scan).
+//   q / z, with the q part of the tail in its grid; chunked scan).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -221,7 +221,7 @@ sr_status sr_replay_group(const sr_shape* shape, int32_t d_ff, float norm_eps, i
       f.Zbuf = Zb;
       f.tail_kv_off = 0;
     } else {
-      // state only: k | v | a | b (the q channels of the tail come from the tail kernel)
+      // state only: k | v | a | b (the q channels of the tail come from the q-tail blocks)
       f.N = c_kv - c_q + 2 * hv;
       f.n_wseg = 4;
       f.seg[0] = {B.w_k, nullptr, 0, c_k - c_q};
@@ -236,27 +236,30 @@ sr_status sr_replay_group(const sr_shape* shape, int32_t d_ff, float norm_eps, i
       f.q_scale = 1.f;
       f.tail_kv_off = c_q;
     }
-    if (fail(sr::timed_call(SR_KERNEL_PROJ_CONV, s, [&] { return sr::launch_proj_conv(SR_BF16, d, f, s); })) !=
-        SR_OK)
-      return SR_ERR_HIP;
-
-    if (!last && w > 1 && B.tail_out) {
-      // zeros at the tail positions before each segment's first row (the
-      // projection's epilogue writes the rows themselves)
+    if (w > 1 && B.tail_out) {
+      // blocks appended to the projection's grid: the q channels of the tail
+      // (last layer) and the zeros at tail positions before each segment's
+      // first row (the projection's epilogue writes the rows themselves)
       sr::TailArgs t{};
+      t.anchors = X;
       t.D = D;
+      t.w_q = last ? B.w_q : nullptr;
+      t.c_q = last ? c_q : 0;
       t.cu = cu_seqlens;
       t.slot_ids = slot_ids;
       t.n_seg = n_segments;
       t.w = w;
       t.tail = B.tail_out;
+      t.tail_bf16 = shape->tail_dtype == SR_BF16;
       t.c_tail = c_tail;
       t.err = flag;
-      if (fail(sr::timed_call(SR_KERNEL_TAIL, s, [&] {
-            return sr::launch_tail(SR_BF16, SR_BF16, shape->tail_dtype, t, s);
-          })) != SR_OK)
-        return SR_ERR_HIP;
+      f.tq = t;
+      f.tq_blocks = sr::tail_q_grid_x(t) * sr::tail_q_grid_y(t);
     }
+    if (fail(sr::timed_call(SR_KERNEL_PROJ_CONV, s, [&] { return sr::launch_proj_conv(SR_BF16, d, f, s); })) !=
+        SR_OK)
+      return SR_ERR_HIP;
+
     if (!last) {
       sr::OutputArgs o{};
       o.Qbuf = Qb; o.Kbuf = Kb; o.Vbuf = Vb; o.Zbuf = Zb; o.Gbuf = Gb; o.Bbuf = Bb;
@@ -270,24 +273,6 @@ sr_status sr_replay_group(const sr_shape* shape, int32_t d_ff, float norm_eps, i
       if (fail(gemm(sr::kGemmResid, Mh, d_ff, D, B.w_down, nullptr, H, D)) != SR_OK) return SR_ERR_HIP;
       if (fail(rmsnorm(H, false, blocks[l + 1].ln_in, X, nullptr)) != SR_OK) return SR_ERR_HIP;
     } else {
-      if (w > 1 && B.tail_out) {
-        sr::TailArgs t{};
-        t.anchors = X;
-        t.D = D;
-        t.w_q = B.w_q;
-        t.c_q = c_q;
-        t.cu = cu_seqlens;
-        t.slot_ids = slot_ids;
-        t.n_seg = n_segments;
-        t.w = w;
-        t.tail = B.tail_out;
-        t.c_tail = c_tail;
-        t.err = flag;
-        if (fail(sr::timed_call(SR_KERNEL_TAIL, s, [&] {
-              return sr::launch_tail(SR_BF16, SR_BF16, shape->tail_dtype, t, s);
-            })) != SR_OK)
-          return SR_ERR_HIP;
-      }
       sr::ScanArgs a{};
       a.Kbuf = Kb;
       a.Vbuf = Vb;

@@ -37,6 +37,29 @@ struct RowInfo {
   int32_t pos, rem, slot, seg;
 };
 
+// ------------------------------------------------- conv tail: q part + zeros
+struct TailArgs {
+  const void* anchors;  // [T][D]
+  int32_t D;
+  const void* w_q;      // [c_q][D] or nullptr
+  const void* s_q;      // bf16 [c_q] (fp8 only)
+  int32_t c_q;          // q channels in the tail (0 without w_q)
+  const int32_t* cu;
+  const int32_t* slot_ids;
+  int32_t n_seg;
+  int32_t w;
+  void* tail;           // [slots][c_tail][w-1]
+  int32_t tail_bf16;    // tail dtype (q-tail blocks of the fused projection): 1 bf16, 0 fp32
+  int32_t c_tail;
+  const int32_t* err;   // the call's table-check flag: non-zero = write nothing
+};
+
+// q-tail grid (bf16 anchors): x = 32-channel blocks of the q channels + 1
+// block for the leading zeros of the others; y = 32-row blocks of the
+// n_seg (w-1) tail rows.
+__host__ __device__ inline int tail_q_grid_x(const TailArgs& a) { return (a.c_q + 31) / 32 + 1; }
+__host__ __device__ inline int tail_q_grid_y(const TailArgs& a) { return (a.n_seg * (a.w - 1) + 31) / 32; }
+
 struct ProjConvArgs {
   const void* A;        // anchors [T][K] bf16
   int64_t T;
@@ -66,6 +89,10 @@ struct ProjConvArgs {
   int32_t c_tail;
   int32_t tail_kv_off;
   const int32_t* err;   // the call's table-check flag: non-zero = write nothing
+  // q part of the conv tail and its leading zeros (bf16 anchors), run by
+  // blocks appended to the projection's grid; tq_blocks = 0: none
+  TailArgs tq;
+  int32_t tq_blocks;
 };
 
 hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, RowInfo* info,
@@ -99,22 +126,7 @@ struct ConvGateArgs {
 hipError_t launch_conv_gate(int op_dtype, int conv_dtype, int tail_dtype, int d_head,
                             const ConvGateArgs& a, hipStream_t s);
 
-// ------------------------------------------------- conv tail: q part + zeros
-struct TailArgs {
-  const void* anchors;  // [T][D]
-  int32_t D;
-  const void* w_q;      // [c_q][D] or nullptr
-  const void* s_q;      // bf16 [c_q] (fp8 only)
-  int32_t c_q;          // q channels in the tail (0 without w_q)
-  const int32_t* cu;
-  const int32_t* slot_ids;
-  int32_t n_seg;
-  int32_t w;
-  void* tail;           // [slots][c_tail][w-1]
-  int32_t c_tail;
-  const int32_t* err;   // the call's table-check flag: non-zero = write nothing
-};
-
+// fp32 anchors only (the bf16 tail rides in the fused projection's grid)
 hipError_t launch_tail(int anchor_dtype, int weight_dtype, int tail_dtype, const TailArgs& a,
                        hipStream_t s);
 

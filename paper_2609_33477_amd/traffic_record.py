@@ -21,7 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 
 # kernel key -> (name fragment in the trace, sources)
 KERNELS = {
-    "proj_conv": ("proj_conv_kernel", ("proj_conv.hip", "sr_device.hpp", "sr_internal.hpp")),
+    "proj_conv": ("proj_conv_kernel", ("proj_conv.hip", "tail_q.hpp", "sr_device.hpp", "sr_internal.hpp")),
     "gdn_scan": ("gdn_scan_bf16_kernel", ("gdn_scan_bf16.hip", "sr_device.hpp", "sr_internal.hpp")),
     "decay_state": ("decay_state_kernel", ("decay_state.hip", "sr_device.hpp", "sr_internal.hpp")),
     "anchor_gather": ("gather_kernel", ("sidecar.hip", "sr_internal.hpp")),
