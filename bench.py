@@ -434,12 +434,15 @@ def group_work(gw):
     n_full = (hk + hk + hv + hv) * d + 2 * hv          # q | k | v | z | a | b
     n_last = (hk + hv) * d + 2 * hv                    # k | v | a | b
     C = 64                                             # chunk rows of the output kernel
-    per_row_head = 10 * C * d + 6 * d * d              # chunk form: 5 C^2 d-sized and 3 C d^2 products
+    # chunk form: four C^2 d-sized products (K K^T, Q K^T, T diag(beta) R,
+    # (P o Q K^T) Delta) and three C d^2-sized ones (K M0, Q M0, K^T Delta);
+    # the kernel runs them as bf16 hi/lo split products on the bf16 MFMA
+    per_row_head = 8 * C * d + 6 * d * d
     tail_rows = len(live) * (sh.conv_width - 1)
     return {
         # the last layer's projection grid also runs the q part of the conv tail
         "proj_conv": ("mfma", 2.0 * T * D * (n_full * (n - 1) + n_last) + 2.0 * tail_rows * D * hk * d),
-        "gdn_output": ("mfma_f32", float(per_row_head) * T * hv * (n - 1)),
+        "gdn_output": ("mfma", float(per_row_head) * T * hv * (n - 1)),
         "gemm_resid": ("mfma", 2.0 * T * D * (hv * d + F) * (n - 1)),
         "gemm_swiglu": ("mfma", 2.0 * T * D * 2 * F * (n - 1)),
         # input norm of every layer, post-mixer norm of every layer but the last
@@ -499,8 +502,6 @@ def bench_group(args):
         step_ms = tot / args.steps                           # all launches of the kind in one step
         if bound == "mfma":
             ach, peak, unit = amount / (step_ms * 1e-3) / 1e12, PEAK_TFLOPS["bf16"], "TFLOP/s"
-        elif bound == "mfma_f32":
-            ach, peak, unit = amount / (step_ms * 1e-3) / 1e12, PEAK_TFLOPS["f32"], "TFLOP/s"
         else:
             ach, peak, unit = amount / (step_ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
         kernels[k] = {"ms_per_step": round(step_ms, 5), "launches_per_step": cnt / args.steps,

@@ -5,23 +5,35 @@
 // M0 (M = S^T, [d_k][d_v]), with G_i the in-chunk prefix sum of log2 alpha
 // (Section 2.1, Eq. recurrence unrolled over the chunk):
 //   A_ij  = beta_i 2^{G_i - G_j} k_i.k_j  (i > j)        T = (I + A)^{-1}
-//   U     = T diag(beta) V,   X = K M0,   Delta = U - T diag(beta 2^G) X
+//   X     = K M0,   R = V - diag(2^G) X,   Delta = T diag(beta) R
 //   O     = diag(2^G) Q M0 + (P o (Q K^T)) Delta,   P_ij = 2^{G_i - G_j} (i >= j)
 //   M_C   = 2^{G_C} M0 + K^T diag(2^{G_C - G}) Delta
-// (o_i = M_i^T q_i, the state after row i applied to its query), then the
-// output gate and norm of the block: y_i = RMSNorm(o_i) * w * SiLU(z_i) per
-// head, stored bf16 as row i of Y [T][H_v d].  The final M is stored like the
-// state-only scan's.
+// (Delta = U - W M0 of the WY form with U = T diag(beta) V and
+// W = T diag(beta 2^G) K, taken as one product; o_i = M_i^T q_i, the state
+// after row i applied to its query), then the output gate and norm of the
+// block: y_i = RMSNorm(o_i) * w * SiLU(z_i) per head, stored bf16 as row i of
+// Y [T][H_v d].  The final M is stored like the state-only scan's.
 //
-// Every product runs on v_mfma_f32_32x32x2f32 in fp32: K, Q, V and Z arrive
-// in bf16 (exact in fp32), T, Delta, X and the state never get rounded, so the
-// output carries only the rounding of the block's bf16 operands.  One
-// workgroup of d/32 waves per (segment, head); wave w owns columns
-// [32 w, 32 w + 32) of the state, of Delta and of O.  K, Q and V rows of the
-// chunk are staged in LDS (bf16, pitch d + 8); A, T and P are fp32 in LDS.
-// The state-side operands come straight from accumulator registers (the k
-// index of the MFMA follows the accumulator row layout, the LDS operand is
-// read with the same permutation).
+// Precision: A, T, Delta, O and the state stay fp32.  The products run on
+// v_mfma_f32_32x32x16_bf16 with every fp32 operand split into a bf16 high
+// part and a bf16 low part (x = hi + lo to 2^-18 |x|): an operand that is
+// exact in bf16 (K, Q, V) takes two products (with hi and with lo), two fp32
+// operands take three (hi.hi + hi.lo + lo.hi), so each product keeps about
+// 16 significant bits and nothing is rounded to bf16 on the way; the output
+// carries the rounding of the block's bf16 operands and of y itself.
+//
+// One workgroup of d/32 waves per (segment, head); wave w owns columns
+// [32 w, 32 w + 32) of the state, of Delta and of O, each a stack of 32 x 32
+// accumulator tiles.  A 16-deep k-step of a product whose reduction runs over
+// accumulator rows (the chunk rows of X, R and Delta; the d_k rows of M) uses
+// the k-slot order of the accumulator: slot 8h + j of lane half h is row
+// 8 (j / 4) + 4 h + j % 4, so registers 8 s .. 8 s + 7 of a tile are k-step s
+// of its B operand as they stand; the A operand is read from LDS in the same
+// order (two 8-byte row reads, or two transposed reads for K^T).  K, Q, V, Z
+// rows of the chunk are staged in LDS (bf16, pitch d + 8); A and T are fp32
+// in LDS, T diag(beta) and P bf16 hi | lo.  The output norm runs row-wise
+// over an fp32 copy of O in LDS, one row per d/32 lanes, with coalesced
+// 64-byte stores.
 #include "sr_device.hpp"
 
 #include <cstddef>
@@ -30,75 +42,103 @@ namespace sr {
 namespace {
 
 constexpr int kC = 64;         // chunk rows
-constexpr int kFP = 68;        // fp32 pitch of A, T, P
+constexpr int kFP = 68;        // fp32 pitch of A and T
+constexpr int kBP = 68;        // bf16 pitch of the hi / lo parts of T diag(beta) and P
 
 template <int D>
 struct OutCfg {
   static constexpr int NW = D / 32;
   static constexpr int THREADS = 64 * NW;
-  static constexpr int KP = D + 8;                       // bf16 pitch of K, Q, V rows
+  static constexpr int KP = D + 8;                        // bf16 pitch of K, Q, V, Z rows
+  static constexpr int OP = D + 4;                        // fp32 pitch of the output rows
   static constexpr int SZ_ROWS = kC * KP * 2;
-  static constexpr int OFF_K = 0, OFF_Q = SZ_ROWS, OFF_V = 2 * SZ_ROWS;
-  static constexpr int OFF_A = 3 * SZ_ROWS;
-  static constexpr int OFF_T = OFF_A + kC * kFP * 4;
-  static constexpr int OFF_P = OFF_T + kC * kFP * 4;
-  static constexpr int OFF_VEC = OFF_P + kC * kFP * 4;   // gs, bs, Gc, eG, eD, bw: 6 x 64 floats
-  static constexpr int OFF_SS = OFF_VEC + 6 * kC * 4;    // [NW][64] row sums of squares of O
-  static constexpr int LDS = OFF_SS + NW * kC * 4;
-  static constexpr int PIECES = kC * D / 8;              // 16-byte pieces of one chunk matrix
+  static constexpr int OFF_K = 0, OFF_Q = SZ_ROWS, OFF_V = 2 * SZ_ROWS, OFF_Z = 3 * SZ_ROWS;
+  static constexpr int OFF_A = 4 * SZ_ROWS;                // A (fp32); then, with T, the output rows
+  static constexpr int OFF_T = OFF_A + kC * kFP * 4;       // T (fp32), then T diag(beta) hi | lo
+  static constexpr int OFF_P = OFF_T + kC * kFP * 4;       // P hi | lo
+  static constexpr int OFF_VEC = OFF_P + 2 * kC * kBP * 2; // gs, bs, Gc, eG, eD: 5 x 64 floats
+  static constexpr int OFF_NW = OFF_VEC + 5 * kC * 4;      // norm weight (fp32) [D]
+  static constexpr int LDS = OFF_NW + D * 4;
+  static constexpr int PIECES = kC * D / 8;               // 16-byte pieces of one chunk matrix
   static constexpr int PER_T = PIECES / THREADS;
   static_assert(PIECES % THREADS == 0, "chunk split");
+  static_assert(kC * OP * 4 <= 2 * kC * kFP * 4, "output rows in the place of A and T");
+  static_assert(2 * kC * kBP * 2 <= kC * kFP * 4, "T diag(beta) hi | lo in the place of T");
 };
 
-__device__ __forceinline__ float lds_bf16(const char* base, int idx) {
-  return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(base)[idx] << 16);
+typedef __attribute__((address_space(3))) char lchar;
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint2 ld8(const lchar* p) {
+  return __builtin_bit_cast(uint2, *reinterpret_cast<const __attribute__((address_space(3))) u32x2*>(p));
 }
-// four consecutive bf16 values (idx a multiple of 4) as fp32, one 8-byte read
-__device__ __forceinline__ void lds_bf16x4(const char* base, int idx, float* v) {
-  const uint2 u = *reinterpret_cast<const uint2*>(base + idx * 2);
-  v[0] = __uint_as_float(u.x << 16);
-  v[1] = __uint_as_float(u.x & 0xffff0000u);
-  v[2] = __uint_as_float(u.y << 16);
-  v[3] = __uint_as_float(u.y & 0xffff0000u);
+__device__ __forceinline__ uint4 ld16(const lchar* p) {
+  return __builtin_bit_cast(uint4, *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p));
 }
-// four consecutive fp32 values (idx a multiple of 4), one 16-byte read
-__device__ __forceinline__ void lds_f32x4(const float* base, int idx, float* v) {
-  const float4 u = *reinterpret_cast<const float4*>(base + idx);
-  v[0] = u.x;
-  v[1] = u.y;
-  v[2] = u.z;
-  v[3] = u.w;
+__device__ __forceinline__ float4 ldf4(const lchar* p) {
+  const f32x4v v = *reinterpret_cast<const __attribute__((address_space(3))) f32x4v*>(p);
+  return make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ float lo_f(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float hi_f(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+
+// A-operand fragment of k-step [k0, k0 + 16) from a row-major bf16 row: slots
+// 8h .. 8h + 3 are columns k0 + 4h .. + 3, slots 8h + 4 .. 8h + 7 columns
+// k0 + 8 + 4h .. + 3
+__device__ __forceinline__ bf16x8 frag_row(const lchar* row, int k0, int h) {
+  const uint2 a = ld8(row + (k0 + 4 * h) * 2), b = ld8(row + (k0 + 8 + 4 * h) * 2);
+  return as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
+}
+
+// Eight fp32 values (accumulator registers 8s .. 8s + 7) as a bf16 high part
+// and the bf16 rounding of the remainder.
+__device__ __forceinline__ void split8(const f32x16& v, int s, bf16x8& hi, bf16x8& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float x0 = v[8 * s + 2 * e], x1 = v[8 * s + 2 * e + 1];
+    h[e] = pack_bf16x2(x0, x1);
+    l[e] = pack_bf16x2(x0 - lo_f(h[e]), x1 - hi_f(h[e]));
+  }
+  hi = as_bf16x8(make_uint4(h[0], h[1], h[2], h[3]));
+  lo = as_bf16x8(make_uint4(l[0], l[1], l[2], l[3]));
+}
+
+__device__ __forceinline__ f32x16 mma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ __forceinline__ float silu(float x) { return x * __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
-
-__device__ __forceinline__ void mma(f32x16& c, float a, float b) {
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-}
-
-// k index (row of the accumulator tile) of step s for lane half h
-__device__ __forceinline__ int perm_k(int s, int h) { return 8 * (s >> 2) + 4 * h + (s & 3); }
 
 template <int D>
 __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a) {
   if (a.err && *a.err) return;   // the call's table check failed: write nothing
   using CF = OutCfg<D>;
-  constexpr int NW = CF::NW, KP = CF::KP, NT = D / 32;
+  constexpr int NW = CF::NW, KP = CF::KP, NT = D / 32, OP = CF::OP;
   __shared__ __attribute__((aligned(16))) char smem[CF::LDS];
   __shared__ int sel;
-  char* Ks = smem + CF::OFF_K;
-  char* Qs = smem + CF::OFF_Q;
-  char* Vs = smem + CF::OFF_V;
+  lchar* L = (lchar*)smem;
+  lchar* Ks = L + CF::OFF_K;
+  lchar* Qs = L + CF::OFF_Q;
+  lchar* Vs = L + CF::OFF_V;
+  lchar* Zs = L + CF::OFF_Z;
   float* Am = reinterpret_cast<float*>(smem + CF::OFF_A);
   float* Tm = reinterpret_cast<float*>(smem + CF::OFF_T);
-  float* Pm = reinterpret_cast<float*>(smem + CF::OFF_P);
-  float* gs = reinterpret_cast<float*>(smem + CF::OFF_VEC);   // log2 alpha
-  float* bs = gs + kC;                                        // beta
-  float* Gc = bs + kC;                                        // in-chunk prefix of log2 alpha
-  float* eG = Gc + kC;                                        // 2^{G_i}
-  float* eD = eG + kC;                                        // 2^{G_C - G_i}
-  float* bw = eD + kC;                                        // beta_i 2^{G_i}
-  float* SS = reinterpret_cast<float*>(smem + CF::OFF_SS);
+  lchar* Tbh = L + CF::OFF_T;                                   // T diag(beta): hi, then lo
+  lchar* Tbl = Tbh + kC * kBP * 2;
+  lchar* Ph = L + CF::OFF_P;                                    // P o (Q K^T): hi, then lo
+  lchar* Pl = Ph + kC * kBP * 2;
+  uint16_t* Ph16 = reinterpret_cast<uint16_t*>(smem + CF::OFF_P);
+  uint16_t* Pl16 = Ph16 + kC * kBP;
+  float* Os = reinterpret_cast<float*>(smem + CF::OFF_A);      // output rows (after A and T are done)
+  float* gs = reinterpret_cast<float*>(smem + CF::OFF_VEC);    // log2 alpha
+  float* bs = gs + kC;                                         // beta
+  float* Gc = bs + kC;                                         // in-chunk prefix of log2 alpha
+  float* eG = Gc + kC;                                         // 2^{G_i}
+  float* eD = eG + kC;                                         // 2^{G_C - G_i}
+  float* nws = reinterpret_cast<float*>(smem + CF::OFF_NW);    // norm weight
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int lc = lane & 31, h2 = lane >> 5;
@@ -118,12 +158,16 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
   const float* Gp = a.Gbuf + (int64_t)head * a.T;
   const float* Bp = a.Bbuf + (int64_t)head * a.T;
   const int col = 32 * wid + lc;                        // this lane's column of Delta, O and M
-  const float nw = __uint_as_float((uint32_t) static_cast<const uint16_t*>(a.norm_w)[col] << 16);
-  uint16_t* Yp = static_cast<uint16_t*>(a.Y) + (int64_t)head * D + col;
   const int64_t ldy = (int64_t)a.H_v * D;
+  if (tid < D) nws[tid] = __uint_as_float((uint32_t) static_cast<const uint16_t*>(a.norm_w)[tid] << 16);
 
-  // T's strictly upper 16x16 blocks stay zero for the whole segment
-  for (int i = tid; i < kC * kFP; i += CF::THREADS) Tm[i] = 0.f;
+  // transposed reads of a row-major bf16 matrix (pitch KP): lane (lc, h2)
+  // receives rows row0 + 4 h2 .. + 3 of column c0 + lc
+  const int tr_r = lane & 15;                           // lane within its 16-lane group
+  const int tr_n = 16 * ((lane >> 4) & 1) + 4 * (tr_r & 3);
+  auto tr4 = [&](const lchar* base, int row0, int c0) {
+    return lds_tr4(base + ((row0 + 4 * h2 + (tr_r >> 2)) * KP + c0 + tr_n) * 2);
+  };
 
   f32x16 M[NT];
 #pragma unroll
@@ -131,21 +175,24 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
 
   for (int64_t c0 = s0; c0 < s1; c0 += kC) {
     const int n = (int)(s1 - c0 < kC ? s1 - c0 : kC);   // live rows of this chunk
-    // ---- 1. stage K, Q, V rows (zero past the segment end), gates
+    // ---- 1. stage K, Q, V, Z rows (zero past the segment end), gates
 #pragma unroll
     for (int i = 0; i < CF::PER_T; ++i) {
       const int p = tid + i * CF::THREADS;
       const int row = p / (D / 8), cc = p % (D / 8);
-      uint4 kv = make_uint4(0, 0, 0, 0), qv = kv, vv = kv;
+      uint4 kv = make_uint4(0, 0, 0, 0), qv = kv, vv = kv, zv = kv;
       if (row < n) {
         const int64_t off = (c0 + row) * D + cc * 8;
         kv = *reinterpret_cast<const uint4*>(Kp + off);
         qv = *reinterpret_cast<const uint4*>(Qp + off);
         vv = *reinterpret_cast<const uint4*>(Vp + off);
+        zv = *reinterpret_cast<const uint4*>(Zp + off);
       }
-      *reinterpret_cast<uint4*>(Ks + (row * KP + cc * 8) * 2) = kv;
-      *reinterpret_cast<uint4*>(Qs + (row * KP + cc * 8) * 2) = qv;
-      *reinterpret_cast<uint4*>(Vs + (row * KP + cc * 8) * 2) = vv;
+      const int lo = (row * KP + cc * 8) * 2;
+      *reinterpret_cast<uint4*>(smem + CF::OFF_K + lo) = kv;
+      *reinterpret_cast<uint4*>(smem + CF::OFF_Q + lo) = qv;
+      *reinterpret_cast<uint4*>(smem + CF::OFF_V + lo) = vv;
+      *reinterpret_cast<uint4*>(smem + CF::OFF_Z + lo) = zv;
     }
     if (tid < kC) {
       gs[tid] = tid < n ? Gp[c0 + tid] : 0.f;
@@ -165,7 +212,6 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
       Gc[lane] = x;
       eG[lane] = exp2f(x);
       eD[lane] = exp2f(gC - x);
-      bw[lane] = bs[lane] * exp2f(x);
     }
     // tiles q = 0..5: (0,0), (1,0), (1,1) of K K^T, then of Q K^T
     constexpr int GQ = (6 + NW - 1) / NW;
@@ -176,18 +222,18 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
       const int q = wid + nq * NW;
       if (q >= 6) continue;
       const int tq = q % 3, ti = (tq + 1) >> 1, tj = tq >> 1;
-      // K and Q are exact in bf16: bf16 MFMA with fp32 accumulation
-      const char* Lsrc = q < 3 ? Ks : Qs;
+      const lchar* Lsrc = q < 3 ? Ks : Qs;
 #pragma unroll
       for (int s = 0; s < D / 16; ++s) {
-        const bf16x8 fa = as_bf16x8(*reinterpret_cast<const uint4*>(Lsrc + ((32 * ti + lc) * KP + 16 * s + 8 * h2) * 2));
-        const bf16x8 fb = as_bf16x8(*reinterpret_cast<const uint4*>(Ks + ((32 * tj + lc) * KP + 16 * s + 8 * h2) * 2));
-        gam[nq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, gam[nq], 0, 0, 0);
+        const bf16x8 fa = as_bf16x8(ld16(Lsrc + ((32 * ti + lc) * KP + 16 * s + 8 * h2) * 2));
+        const bf16x8 fb = as_bf16x8(ld16(Ks + ((32 * tj + lc) * KP + 16 * s + 8 * h2) * 2));
+        gam[nq] = mma(fa, fb, gam[nq]);
       }
     }
     lds_barrier();
 
-    // ---- 3. A_ij = beta_i 2^{G_i - G_j} Gamma_ij (i > j); P_ij = 2^{G_i - G_j} (QK^T)_ij (i >= j)
+    // ---- 3. A_ij = beta_i 2^{G_i - G_j} Gamma_ij (i > j), fp32;
+    //         P_ij = 2^{G_i - G_j} (Q K^T)_ij (i >= j), bf16 hi | lo
 #pragma unroll
     for (int nq = 0; nq < GQ; ++nq) {
       const int q = wid + nq * NW;
@@ -195,16 +241,35 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
       const int tq = q % 3, ti = (tq + 1) >> 1, tj = tq >> 1;
       const int j = 32 * tj + lc;
       const float gj = Gc[j];
+      // this lane's rows 32 ti + 8 r4 + 4 h2 .. + 3 (r4 = 0..3)
+      float gi[16], bi[16];
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int i0 = 32 * ti + 8 * r4 + 4 * h2;
+        const float4 g4 = ldf4((const lchar*)(Gc + i0));
+        const float4 b4 = ldf4((const lchar*)(bs + i0));
+        gi[4 * r4] = g4.x; gi[4 * r4 + 1] = g4.y; gi[4 * r4 + 2] = g4.z; gi[4 * r4 + 3] = g4.w;
+        bi[4 * r4] = b4.x; bi[4 * r4 + 1] = b4.y; bi[4 * r4 + 2] = b4.z; bi[4 * r4 + 3] = b4.w;
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int i = 32 * ti + acc_row(r, lane);
-        const float dec = exp2f(fminf(Gc[i] - gj, 0.f));
-        if (q < 3) Am[i * kFP + j] = (i > j) ? bs[i] * dec * gam[nq][r] : 0.f;
-        else Pm[i * kFP + j] = (i >= j) ? dec * gam[nq][r] : 0.f;
+        const float dec = exp2f(fminf(gi[r] - gj, 0.f));
+        if (q < 3) {
+          Am[i * kFP + j] = (i > j) ? bi[r] * dec * gam[nq][r] : 0.f;
+        } else {
+          const float v = (i >= j) ? dec * gam[nq][r] : 0.f;
+          const uint32_t hv = pack_bf16x2(v, 0.f);
+          Ph16[i * kBP + j] = (uint16_t)hv;
+          Pl16[i * kBP + j] = (uint16_t)pack_bf16x2(v - lo_f(hv), 0.f);
+        }
       }
-      if (tq == 1) {   // the strictly upper tile (0,1) of P is zero
+      if (q == 4) {   // the strictly upper tile (0,1) of P is zero
 #pragma unroll
-        for (int r = 0; r < 16; ++r) Pm[(acc_row(r, lane)) * kFP + 32 + lc] = 0.f;
+        for (int r = 0; r < 16; ++r) {
+          Ph16[acc_row(r, lane) * kBP + 32 + lc] = 0;
+          Pl16[acc_row(r, lane) * kBP + 32 + lc] = 0;
+        }
       }
     }
     lds_barrier();
@@ -251,118 +316,184 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
         lds_barrier();
       }
     }
+    // T diag(beta) as bf16 hi | lo in T's place (the strictly upper 16x16
+    // blocks of T are zero; their storage is not written for T)
+    {
+      constexpr int PER = kC * kC / 4 / CF::THREADS;   // 4-column pieces per thread
+      float tv[PER][4];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int p = tid + e * CF::THREADS, row = p / 16, c4 = p % 16;
+        const float4 t4 = ldf4((const lchar*)(Tm + row * kFP + 4 * c4));
+        const float4 b4 = ldf4((const lchar*)(bs + 4 * c4));
+        const bool upper = (c4 >> 2) > (row >> 4);
+        tv[e][0] = upper ? 0.f : t4.x * b4.x;
+        tv[e][1] = upper ? 0.f : t4.y * b4.y;
+        tv[e][2] = upper ? 0.f : t4.z * b4.z;
+        tv[e][3] = upper ? 0.f : t4.w * b4.w;
+      }
+      lds_barrier();
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int p = tid + e * CF::THREADS, row = p / 16, c4 = p % 16;
+        const uint32_t h0 = pack_bf16x2(tv[e][0], tv[e][1]), h1 = pack_bf16x2(tv[e][2], tv[e][3]);
+        const uint32_t l0 = pack_bf16x2(tv[e][0] - lo_f(h0), tv[e][1] - hi_f(h0));
+        const uint32_t l1 = pack_bf16x2(tv[e][2] - lo_f(h1), tv[e][3] - hi_f(h1));
+        *reinterpret_cast<uint2*>(smem + CF::OFF_T + (row * kBP + 4 * c4) * 2) = make_uint2(h0, h1);
+        *reinterpret_cast<uint2*>(smem + CF::OFF_T + kC * kBP * 2 + (row * kBP + 4 * c4) * 2) = make_uint2(l0, l1);
+      }
+      lds_barrier();
+    }
 
-    // Operands on the k side of a state product follow the accumulator row
-    // order: step s takes rows perm_k(s, h) of a 32-row tile, i.e. four runs
-    // of four consecutive rows, so the LDS side is read 4 values at a time.
-    // ---- 5. X = K M0 (this wave's columns), from the state registers
-    f32x16 X[2];
+    // ---- 5. X = K M0 and Q M0 (this wave's columns): K and Q exact in bf16,
+    // M0 as hi + lo
+    f32x16 X[2], O[2];
 #pragma unroll
     for (int ti = 0; ti < 2; ++ti) {
       X[ti] = zero16();
+      O[ti] = zero16();
+    }
 #pragma unroll
-      for (int td = 0; td < NT; ++td) {
-        float av[16];
+    for (int td = 0; td < NT; ++td) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) lds_bf16x4(Ks, (32 * ti + lc) * KP + 32 * td + 8 * q + 4 * h2, av + 4 * q);
+      for (int s = 0; s < 2; ++s) {
+        bf16x8 mh, ml;
+        split8(M[td], s, mh, ml);
 #pragma unroll
-        for (int s = 0; s < 16; ++s) mma(X[ti], av[s], M[td][s]);
+        for (int ti = 0; ti < 2; ++ti) {
+          const int off = (32 * ti + lc) * KP * 2;
+          const bf16x8 ka = frag_row(Ks + off, 32 * td + 16 * s, h2);
+          const bf16x8 qa = frag_row(Qs + off, 32 * td + 16 * s, h2);
+          X[ti] = mma(ka, ml, mma(ka, mh, X[ti]));
+          O[ti] = mma(qa, ml, mma(qa, mh, O[ti]));
+        }
       }
     }
-    // ---- 6. Delta = T diag(beta) V - T diag(beta 2^G) X
+    // ---- 6. R = V - diag(2^G) X (in X's registers); Delta = T diag(beta) R
+#pragma unroll
+    for (int tj = 0; tj < 2; ++tj) {
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const uint2 v4 = tr4(Vs, 32 * tj + 8 * r4, 32 * wid);
+        const float4 g4 = ldf4((const lchar*)(eG + 32 * tj + 8 * r4 + 4 * h2));
+        X[tj][4 * r4 + 0] = fmaf(-g4.x, X[tj][4 * r4 + 0], lo_f(v4.x));
+        X[tj][4 * r4 + 1] = fmaf(-g4.y, X[tj][4 * r4 + 1], hi_f(v4.x));
+        X[tj][4 * r4 + 2] = fmaf(-g4.z, X[tj][4 * r4 + 2], lo_f(v4.y));
+        X[tj][4 * r4 + 3] = fmaf(-g4.w, X[tj][4 * r4 + 3], hi_f(v4.y));
+      }
+    }
     f32x16 Dl[2];
 #pragma unroll
-    for (int ti = 0; ti < 2; ++ti) {
-      Dl[ti] = zero16();
+    for (int ti = 0; ti < 2; ++ti) Dl[ti] = zero16();
 #pragma unroll
-      for (int tj = 0; tj < 2; ++tj) {
-        float tv[16], bv[16], wv[16], vv[16];
+    for (int tj = 0; tj < 2; ++tj)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int j0 = 32 * tj + 8 * q + 4 * h2;
-          lds_f32x4(Tm, (32 * ti + lc) * kFP + j0, tv + 4 * q);
-          lds_f32x4(bs, j0, bv + 4 * q);
-          lds_f32x4(bw, j0, wv + 4 * q);
+      for (int s = 0; s < 2; ++s) {
+        bf16x8 rh, rl;
+        split8(X[tj], s, rh, rl);
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti) {
+          const int off = (32 * ti + lc) * kBP * 2;
+          const bf16x8 th = frag_row(Tbh + off, 32 * tj + 16 * s, h2);
+          const bf16x8 tl = frag_row(Tbl + off, 32 * tj + 16 * s, h2);
+          Dl[ti] = mma(tl, rh, mma(th, rl, mma(th, rh, Dl[ti])));
         }
-#pragma unroll
-        for (int s = 0; s < 16; ++s) vv[s] = lds_bf16(Vs, (32 * tj + perm_k(s, h2)) * KP + col);
-#pragma unroll
-        for (int s = 0; s < 16; ++s) mma(Dl[ti], tv[s] * bv[s], vv[s]);
-#pragma unroll
-        for (int s = 0; s < 16; ++s) mma(Dl[ti], -tv[s] * wv[s], X[tj][s]);
       }
-    }
-    // ---- 7. O = diag(2^G) Q M0 + (P o QK^T) Delta
-    f32x16 O[2];
-#pragma unroll
-    for (int ti = 0; ti < 2; ++ti) {
-      O[ti] = zero16();
-#pragma unroll
-      for (int td = 0; td < NT; ++td) {
-        float av[16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) lds_bf16x4(Qs, (32 * ti + lc) * KP + 32 * td + 8 * q + 4 * h2, av + 4 * q);
-#pragma unroll
-        for (int s = 0; s < 16; ++s) mma(O[ti], av[s], M[td][s]);
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) O[ti][r] *= eG[32 * ti + acc_row(r, lane)];
-#pragma unroll
-      for (int tj = 0; tj < 2; ++tj) {
-        float pv[16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) lds_f32x4(Pm, (32 * ti + lc) * kFP + 32 * tj + 8 * q + 4 * h2, pv + 4 * q);
-#pragma unroll
-        for (int s = 0; s < 16; ++s) mma(O[ti], pv[s], Dl[tj][s]);
-      }
-    }
-    // ---- 8. gated output norm: per row, sum of squares over the head's d columns
+    // ---- 7. O = diag(2^G) Q M0 + (P o Q K^T) Delta
 #pragma unroll
     for (int ti = 0; ti < 2; ++ti)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = O[ti][r] * O[ti][r];
-#pragma unroll
-        for (int off = 16; off >= 1; off >>= 1) v += __shfl_xor(v, off);   // over the 32 columns
-        if (lc == 0) SS[wid * kC + 32 * ti + acc_row(r, lane)] = v;
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const float4 g4 = ldf4((const lchar*)(eG + 32 * ti + 8 * r4 + 4 * h2));
+        O[ti][4 * r4 + 0] *= g4.x;
+        O[ti][4 * r4 + 1] *= g4.y;
+        O[ti][4 * r4 + 2] *= g4.z;
+        O[ti][4 * r4 + 3] *= g4.w;
       }
-    // ---- 9. M = 2^{G_C} M0 + K^T diag(2^{G_C - G}) Delta
+#pragma unroll
+    for (int tj = 0; tj < 2; ++tj)
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        bf16x8 dh, dlo;
+        split8(Dl[tj], s, dh, dlo);
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti) {
+          const int off = (32 * ti + lc) * kBP * 2;
+          const bf16x8 ph = frag_row(Ph + off, 32 * tj + 16 * s, h2);
+          const bf16x8 pl = frag_row(Pl + off, 32 * tj + 16 * s, h2);
+          O[ti] = mma(pl, dh, mma(ph, dlo, mma(ph, dh, O[ti])));
+        }
+      }
+    lds_barrier();   // every wave is done with T diag(beta): O goes where A and T were
+#pragma unroll
+    for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) Os[(32 * ti + acc_row(r, lane)) * OP + col] = O[ti][r];
+    // ---- 8. M = 2^{G_C} M0 + K^T diag(2^{G_C - G}) Delta (K^T by transposed reads)
     const float eGC = eG[kC - 1];
 #pragma unroll
     for (int tj = 0; tj < 2; ++tj)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) Dl[tj][r] *= eD[32 * tj + acc_row(r, lane)];
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const float4 e4 = ldf4((const lchar*)(eD + 32 * tj + 8 * r4 + 4 * h2));
+        Dl[tj][4 * r4 + 0] *= e4.x;
+        Dl[tj][4 * r4 + 1] *= e4.y;
+        Dl[tj][4 * r4 + 2] *= e4.z;
+        Dl[tj][4 * r4 + 3] *= e4.w;
+      }
 #pragma unroll
-    for (int td = 0; td < NT; ++td) {
+    for (int td = 0; td < NT; ++td)
 #pragma unroll
       for (int r = 0; r < 16; ++r) M[td][r] *= eGC;
 #pragma unroll
-      for (int tj = 0; tj < 2; ++tj) {
-        float kv[16];
+    for (int tj = 0; tj < 2; ++tj)
 #pragma unroll
-        for (int s = 0; s < 16; ++s) kv[s] = lds_bf16(Ks, (32 * tj + perm_k(s, h2)) * KP + 32 * td + lc);
+      for (int s = 0; s < 2; ++s) {
+        bf16x8 dh, dlo;
+        split8(Dl[tj], s, dh, dlo);
 #pragma unroll
-        for (int s = 0; s < 16; ++s) mma(M[td], kv[s], Dl[tj][s]);
-      }
-    }
-    lds_barrier();
-    // ---- 10. y = o / sqrt(mean(o^2) + eps) * w * SiLU(z), rows of this chunk
-#pragma unroll
-    for (int ti = 0; ti < 2; ++ti)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = 32 * ti + acc_row(r, lane);
-        if (i < n) {
-          float ss = 0.f;
-#pragma unroll
-          for (int w = 0; w < NW; ++w) ss += SS[w * kC + i];
-          const float inv = __builtin_amdgcn_rsqf(ss / (float)D + a.eps);
-          const int64_t t = c0 + i;
-          const float z = __uint_as_float((uint32_t)Zp[t * D + col] << 16);
-          Yp[t * ldy] = f32_to_bf16_bits(O[ti][r] * inv * nw * silu(z));
+        for (int td = 0; td < NT; ++td) {
+          const int k0 = 32 * tj + 16 * s;
+          const uint2 x0 = tr4(Ks, k0, 32 * td), x1 = tr4(Ks, k0 + 8, 32 * td);
+          const bf16x8 ka = as_bf16x8(make_uint4(x0.x, x0.y, x1.x, x1.y));
+          M[td] = mma(ka, dlo, mma(ka, dh, M[td]));
         }
       }
-    lds_barrier();   // the next chunk's staging overwrites K, Q, V and SS
+    lds_barrier();   // the output rows are complete
+    // ---- 9. y = o / sqrt(mean(o^2) + eps) * w * SiLU(z): NW lanes per row,
+    // 32 columns each
+    {
+      const int row = tid / NW, part = tid % NW;
+      const float* orow = Os + row * OP + 32 * part;
+      float ov[32];
+      float ss = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float4 v = ldf4((const lchar*)(orow + 4 * e));
+        ov[4 * e] = v.x; ov[4 * e + 1] = v.y; ov[4 * e + 2] = v.z; ov[4 * e + 3] = v.w;
+        ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
+      }
+#pragma unroll
+      for (int off = 1; off < NW; off <<= 1) ss += __shfl_xor(ss, off);
+      const float inv = __builtin_amdgcn_rsqf(ss / (float)D + a.eps);
+      if (row < n) {
+        uint16_t* yrow = static_cast<uint16_t*>(a.Y) + (c0 + row) * ldy + (int64_t)head * D + 32 * part;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint4 z8 = ld16(Zs + (row * KP + 32 * part + 8 * e) * 2);
+          const uint32_t zw[4] = {z8.x, z8.y, z8.z, z8.w};
+          uint32_t yw[4];
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            const int c = 8 * e + 2 * p;
+            const float w0 = nws[32 * part + c], w1 = nws[32 * part + c + 1];
+            yw[p] = pack_bf16x2(ov[c] * inv * w0 * silu(lo_f(zw[p])), ov[c + 1] * inv * w1 * silu(hi_f(zw[p])));
+          }
+          *reinterpret_cast<uint4*>(yrow + 8 * e) = make_uint4(yw[0], yw[1], yw[2], yw[3]);
+        }
+      }
+    }
+    lds_barrier();   // the next chunk's staging overwrites K, Q, V, Z; A overwrites the output rows
   }
 
   float* out = a.state_out + ((size_t)slot * a.H_v + head) * D * D;
