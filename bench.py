@@ -15,6 +15,7 @@ Prints ONE JSON line on stdout; progress goes to stderr.
     python bench.py --workload sidecar_write    # anchor sidecar write path (Section 5.1)
     python bench.py --workload graph_small      # graph-bucketed replay of a small batch vs eager
     python bench.py --workload group_qwen35_4b  # group replay chaining: 3 layers from one anchor (Section 4.1)
+    python bench.py --workload olmo_varlen      # OLMo-Hybrid-7B's d_k=96 / d_v=192 heads (Appendix A)
 
 The two sidecar workloads time the sidecar's own calls instead of the replay
 and report anchor rows (x anchored layers) per second, with the HBM roofline
@@ -50,15 +51,15 @@ def algorithmic_work(wl, with_q=True):
     HBM bytes for the streaming kernels), from the shapes alone."""
     sh = wl.shape
     T = wl.t_total
-    D, hk, hv, d, w = sh.d_model, sh.n_k_heads, sh.n_v_heads, sh.d_k, sh.conv_width
-    c_kv = (hk + hv) * d
+    D, hk, hv, w = sh.d_model, sh.n_k_heads, sh.n_v_heads, sh.conv_width
+    c_kv = hk * sh.d_k + hv * sh.d_v
     N = c_kv + 2 * hv
     es = 4 if sh.anchor_dtype == "f32" else 2             # k/v operand bytes
     wb = {"f32": 4, "bf16": 2, "fp8_e4m3": 1}[sh.weight_dtype]
     tb = 4 if sh.tail_dtype == "f32" else 2
     live = [b for b, s in enumerate(wl.slot_ids) if s >= 0]
     n_layers = len(wl.layers)
-    c_q = hk * d if with_q else 0
+    c_q = hk * sh.d_k if with_q else 0
     tail_rows = len(live) * (w - 1)
     return {
         # one launch per layer
@@ -76,9 +77,9 @@ def algorithmic_work(wl, with_q=True):
         # one launch per call: the varlen tables in, one flag word out
         "validate": ("hbm", (2 * len(wl.seg_lens) + 1) * 4 + 4),
         # one launch covers all layers (up to 32)
-        "gdn_scan": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * d * d * 4)),
+        "gdn_scan": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * sh.d_k * sh.d_v * 4)),
         # the per-head-decay state reads the same operands and writes the same states
-        "decay_state": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * d * d * 4)),
+        "decay_state": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * sh.d_k * sh.d_v * 4)),
     }
 
 

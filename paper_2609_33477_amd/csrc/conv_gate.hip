@@ -19,6 +19,7 @@
 // k | v channels of existing rows are written with k and v.  With bf16
 // anchors the tail is computed inside the fused projection's grid.
 #include "sr_device.hpp"
+#include "tail_q.hpp"
 
 #include <type_traits>
 
@@ -159,8 +160,133 @@ hipError_t run_conv(const ConvGateArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Heads whose key and value widths differ (Appendix A: OLMo-Hybrid's
+// d_k = 96, d_v = 192): one wave per (row block, head), lane l owning
+// channels l, l + 64, ... of its head, walking the block's rows as above; a
+// key head's sum of squares is reduced over the wave.  G is written as
+// log2 alpha, the convention of the chunk kernel that reads it.
+template <typename OUT, typename CW, typename TT, int DK, int DV>
+__global__ __launch_bounds__(kConvThreads) void conv_gate_rect_kernel(ConvGateArgs a) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
+  constexpr int QMAX = ((DK > DV ? DK : DV) + 63) / 64;   // channels per lane, at most
+  constexpr int WMAX = 4;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
+  const int64_t r1 = min(a.T, r0 + kRowsPerBlock);
+  const int n_heads = a.H_k + a.H_v;
+  const int C_kv = a.H_k * DK + a.H_v * DV;
+
+  if ((int)blockIdx.y == (int)gridDim.y - 1) {
+    // ---- gates: thread -> (head, row), rows fastest: log2 alpha and beta per row
+    const int rows = (int)(r1 - r0);
+    for (int idx = tid; idx < rows * a.H_v; idx += kConvThreads) {
+      const int h = idx / rows;
+      const int64_t t = r0 + idx % rows;
+      const float av = a.P[t * a.ldp + C_kv + h];
+      const float bv = a.P[t * a.ldp + C_kv + a.H_v + h];
+      a.Gbuf[(int64_t)h * a.T + t] = -expf(a.a_log[h]) * softplus(av + a.dt_bias[h]) * 1.4426950408889634f;
+      a.Bbuf[(int64_t)h * a.T + t] = sigmoid(bv);
+    }
+    return;
+  }
+
+  const int head = blockIdx.y * (kConvThreads / 64) + wid;
+  if (head >= n_heads) return;                     // wave-uniform; the kernel has no block barrier
+  const bool is_k = head < a.H_k;
+  const int DH = is_k ? DK : DV;
+  const int hh = is_k ? head : head - a.H_k;
+  const int c0 = is_k ? head * DK : a.H_k * DK + hh * DV;   // first channel of the head
+  const int w = a.w;
+
+  float taps[QMAX][WMAX];
+#pragma unroll
+  for (int q = 0; q < QMAX; ++q) {
+    const int ch = lane + 64 * q;
+#pragma unroll
+    for (int i = 0; i < WMAX; ++i)
+      taps[q][i] = (ch < DH && i < w) ? Elem<CW>::load(a.conv_w, (int64_t)(c0 + ch) * w + i) : 0.f;
+  }
+  // prev[j][q] = raw value at row t-1-j
+  float prev[WMAX - 1][QMAX];
+#pragma unroll
+  for (int j = 0; j < WMAX - 1; ++j)
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+      const int ch = lane + 64 * q;
+      const int64_t t = r0 - 1 - j;
+      prev[j][q] = (ch < DH && j < w - 1 && t >= 0) ? a.P[t * a.ldp + c0 + ch] : 0.f;
+    }
+
+  int b = segment_of_row(a.cu, a.n_seg, r0);
+  int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
+  int slot = a.slot_ids ? a.slot_ids[b] : b;
+  void* dst = is_k ? a.Kbuf : a.Vbuf;
+
+  for (int64_t t = r0; t < r1; ++t) {
+    while (t >= s1) {
+      ++b;
+      s0 = a.cu[b];
+      s1 = a.cu[b + 1];
+      slot = a.slot_ids ? a.slot_ids[b] : b;
+    }
+    float raw[QMAX], act[QMAX];
+    float ss = 0.f;
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+      const int ch = lane + 64 * q;
+      raw[q] = ch < DH ? a.P[t * a.ldp + c0 + ch] : 0.f;
+      float y = taps[q][w - 1] * raw[q];
+#pragma unroll
+      for (int j = 0; j < WMAX - 1; ++j)
+        if (j < w - 1 && t - 1 - j >= s0) y = fmaf(taps[q][w - 2 - j], prev[j][q], y);
+      act[q] = silu(y);
+      ss = fmaf(act[q], act[q], ss);
+    }
+    if (is_k) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+      const float inv = 1.f / sqrtf(ss + a.eps);
+#pragma unroll
+      for (int q = 0; q < QMAX; ++q) act[q] *= inv;
+    }
+    const int64_t base = ((int64_t)hh * a.T + t) * DH;
+    const bool tail_row = a.tail && slot >= 0 && t >= s1 - (w - 1);
+    const int pos = (int)(t - (s1 - (w - 1)));
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+      const int ch = lane + 64 * q;
+      if (ch < DH) {
+        Elem<OUT>::store(dst, base + ch, act[q]);
+        if (tail_row) Elem<TT>::store(a.tail, ((int64_t)slot * a.c_tail + a.tail_kv_off + c0 + ch) * (w - 1) + pos, raw[q]);
+      }
+    }
+#pragma unroll
+    for (int j = WMAX - 2; j > 0; --j)
+#pragma unroll
+      for (int q = 0; q < QMAX; ++q) prev[j][q] = prev[j - 1][q];
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) prev[0][q] = raw[q];
+  }
+}
+
+template <typename OUT, typename CW, typename TT, int DK, int DV>
+hipError_t run_conv_rect(const ConvGateArgs& a, hipStream_t s) {
+  if (a.T == 0) return hipSuccess;
+  const int n_heads = a.H_k + a.H_v;
+  constexpr int HPB = kConvThreads / 64;   // heads per block
+  dim3 grid((unsigned)((a.T + kRowsPerBlock - 1) / kRowsPerBlock), (n_heads + HPB - 1) / HPB + 1);
+  hipLaunchKernelGGL((conv_gate_rect_kernel<OUT, CW, TT, DK, DV>), grid, dim3(kConvThreads), 0, s, a);
+  return hipGetLastError();
+}
+
 template <typename OUT, typename CW, typename TT>
 hipError_t conv_by_head(int d, const ConvGateArgs& a, hipStream_t s) {
+  if (a.d_k != a.d_v) {
+    if constexpr (std::is_same<OUT, bf16_t>::value) {
+      if (a.d_k == 96 && a.d_v == 192) return run_conv_rect<OUT, CW, TT, 96, 192>(a, s);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (d) {
     case 32: return run_conv<OUT, CW, TT, 32>(a, s);
     case 64: return run_conv<OUT, CW, TT, 64>(a, s);
@@ -258,6 +384,15 @@ hipError_t tail_by_input(int ad, int wd, const TailArgs& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+// The q-tail blocks of tail_q.hpp in a grid of their own (bf16 anchors on a
+// path without the fused projection)
+template <typename TW>
+__global__ __launch_bounds__(64 * kTqWaves) void tail_q_kernel(TailArgs a) {
+  if (a.err && *a.err) return;   // the call's table check failed: write nothing
+  __shared__ __attribute__((aligned(1024))) char smem[kTqLds];
+  tail_q_block<TW>(a, blockIdx.x, blockIdx.y, smem);
+}
+
 }  // namespace
 
 hipError_t launch_conv_gate(int op_dtype, int conv_dtype, int tail_dtype, int d_head,
@@ -274,6 +409,14 @@ hipError_t launch_conv_gate(int op_dtype, int conv_dtype, int tail_dtype, int d_
 
 hipError_t launch_tail(int anchor_dtype, int weight_dtype, int tail_dtype, const TailArgs& a,
                        hipStream_t s) {
+  if (anchor_dtype == SR_BF16) {
+    if (a.n_seg == 0 || a.w < 2 || a.c_tail == 0) return hipSuccess;
+    const dim3 grid(tail_q_grid_x(a), tail_q_grid_y(a));
+    if (weight_dtype == SR_BF16) hipLaunchKernelGGL((tail_q_kernel<bf16_t>), grid, dim3(64 * kTqWaves), 0, s, a);
+    else if (weight_dtype == SR_FP8_E4M3) hipLaunchKernelGGL((tail_q_kernel<fp8_t>), grid, dim3(64 * kTqWaves), 0, s, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (tail_dtype == SR_F32) return tail_by_input<float>(anchor_dtype, weight_dtype, a, s);
   if (tail_dtype == SR_BF16) return tail_by_input<bf16_t>(anchor_dtype, weight_dtype, a, s);
   return hipErrorInvalidValue;

@@ -1,5 +1,8 @@
 // Chunked Gated DeltaNet with per-token outputs, for group replay chaining
-// (Section 4.1: a replayed layer's output is the next layer's input).
+// (Section 4.1: a replayed layer's output is the next layer's input), and the
+// same chunk algebra without outputs as the state-only scan of heads whose
+// key and value widths differ (Appendix A: OLMo-Hybrid's d_k = 96,
+// d_v = 192), where the pipelined scan's square tiling does not apply.
 //
 // Per (segment, value head) and chunk of C = 64 rows starting from the state
 // M0 (M = S^T, [d_k][d_v]), with G_i the in-chunk prefix sum of log2 alpha
@@ -22,18 +25,19 @@
 // 16 significant bits and nothing is rounded to bf16 on the way; the output
 // carries the rounding of the block's bf16 operands and of y itself.
 //
-// One workgroup of d/32 waves per (segment, head); wave w owns columns
-// [32 w, 32 w + 32) of the state, of Delta and of O, each a stack of 32 x 32
-// accumulator tiles.  A 16-deep k-step of a product whose reduction runs over
-// accumulator rows (the chunk rows of X, R and Delta; the d_k rows of M) uses
+// One workgroup of d_v/32 waves per (segment, head) (and layer, state-only);
+// wave w owns columns [32 w, 32 w + 32) of the state, of Delta and of O,
+// each a stack of 32 x 32 accumulator tiles.  A 16-deep k-step of a product
+// whose reduction runs over accumulator rows (the chunk rows of X, R and
+// Delta; the d_k rows of M) uses
 // the k-slot order of the accumulator: slot 8h + j of lane half h is row
 // 8 (j / 4) + 4 h + j % 4, so registers 8 s .. 8 s + 7 of a tile are k-step s
 // of its B operand as they stand; the A operand is read from LDS in the same
 // order (two 8-byte row reads, or two transposed reads for K^T).  K, Q, V, Z
-// rows of the chunk are staged in LDS (bf16, pitch d + 8); A and T are fp32
-// in LDS, T diag(beta) and P bf16 hi | lo.  The output norm runs row-wise
-// over an fp32 copy of O in LDS, one row per d/32 lanes, with coalesced
-// 64-byte stores.
+// rows of the chunk are staged in LDS (bf16, pitch width + 8); A and T are
+// fp32 in LDS, T diag(beta) and P bf16 hi | lo.  The output norm runs
+// row-wise over an fp32 copy of O in LDS, one row per d_v/32 lanes, with
+// coalesced 64-byte stores.
 #include "sr_device.hpp"
 
 #include <cstddef>
@@ -45,24 +49,27 @@ constexpr int kC = 64;         // chunk rows
 constexpr int kFP = 68;        // fp32 pitch of A and T
 constexpr int kBP = 68;        // bf16 pitch of the hi / lo parts of T diag(beta) and P
 
-template <int D>
+template <int DK, int DV, bool OUT>
 struct OutCfg {
-  static constexpr int NW = D / 32;
+  static constexpr int NW = DV / 32;
   static constexpr int THREADS = 64 * NW;
-  static constexpr int KP = D + 8;                        // bf16 pitch of K, Q, V, Z rows
-  static constexpr int OP = D + 4;                        // fp32 pitch of the output rows
-  static constexpr int SZ_ROWS = kC * KP * 2;
-  static constexpr int OFF_K = 0, OFF_Q = SZ_ROWS, OFF_V = 2 * SZ_ROWS, OFF_Z = 3 * SZ_ROWS;
-  static constexpr int OFF_A = 4 * SZ_ROWS;                // A (fp32); then, with T, the output rows
+  static constexpr int KP = DK + 8, VP = DV + 8;          // bf16 pitches of K | Q and V | Z rows
+  static constexpr int OP = DV + 4;                       // fp32 pitch of the output rows
+  static constexpr int SZ_K = kC * KP * 2, SZ_V = kC * VP * 2;
+  static constexpr int OFF_K = 0, OFF_V = SZ_K;
+  static constexpr int OFF_Q = OFF_V + SZ_V;              // Q and Z with outputs only
+  static constexpr int OFF_Z = OFF_Q + (OUT ? SZ_K : 0);
+  static constexpr int OFF_A = OFF_Z + (OUT ? SZ_V : 0);  // A (fp32); then, with T, the output rows
   static constexpr int OFF_T = OFF_A + kC * kFP * 4;       // T (fp32), then T diag(beta) hi | lo
-  static constexpr int OFF_P = OFF_T + kC * kFP * 4;       // P hi | lo
-  static constexpr int OFF_VEC = OFF_P + 2 * kC * kBP * 2; // gs, bs, Gc, eG, eD: 5 x 64 floats
-  static constexpr int OFF_NW = OFF_VEC + 5 * kC * 4;      // norm weight (fp32) [D]
-  static constexpr int LDS = OFF_NW + D * 4;
-  static constexpr int PIECES = kC * D / 8;               // 16-byte pieces of one chunk matrix
-  static constexpr int PER_T = PIECES / THREADS;
-  static_assert(PIECES % THREADS == 0, "chunk split");
-  static_assert(kC * OP * 4 <= 2 * kC * kFP * 4, "output rows in the place of A and T");
+  static constexpr int OFF_P = OFF_T + kC * kFP * 4;       // P hi | lo (outputs only)
+  static constexpr int OFF_VEC = OFF_P + (OUT ? 2 * kC * kBP * 2 : 0);   // gs, bs, Gc, eG, eD
+  static constexpr int OFF_NW = OFF_VEC + 5 * kC * 4;      // norm weight (fp32) [DV]
+  static constexpr int LDS = OFF_NW + (OUT ? DV * 4 : 0);
+  static constexpr int PER_K = kC * DK / 8 / THREADS;     // 16-byte pieces per thread of a K | Q chunk
+  static constexpr int PER_V = kC * DV / 8 / THREADS;     // ... of a V | Z chunk
+  static_assert(DK % 32 == 0 && DV % 32 == 0 && DK <= 128 && DV <= 256, "head widths");
+  static_assert(kC * DK / 8 % THREADS == 0 && kC * DV / 8 % THREADS == 0, "chunk split");
+  static_assert(!OUT || kC * OP * 4 <= 2 * kC * kFP * 4, "output rows in the place of A and T");
   static_assert(2 * kC * kBP * 2 <= kC * kFP * 4, "T diag(beta) hi | lo in the place of T");
 };
 
@@ -112,11 +119,13 @@ __device__ __forceinline__ f32x16 mma(const bf16x8& a, const bf16x8& b, const f3
 
 __device__ __forceinline__ float silu(float x) { return x * __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
 
-template <int D>
-__global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a) {
+// A: OutputArgs (one layer, with outputs) or ScanArgs (state only, up to
+// kScanMaxLayers layers per launch, initial states allowed).
+template <int DK, int DV, bool OUT, typename A>
+__global__ __launch_bounds__(64 * (DV / 32)) void gdn_chunk_kernel(A a) {
   if (a.err && *a.err) return;   // the call's table check failed: write nothing
-  using CF = OutCfg<D>;
-  constexpr int NW = CF::NW, KP = CF::KP, NT = D / 32, OP = CF::OP;
+  using CF = OutCfg<DK, DV, OUT>;
+  constexpr int NW = CF::NW, KP = CF::KP, VP = CF::VP, NT = DK / 32, OP = CF::OP;
   __shared__ __attribute__((aligned(16))) char smem[CF::LDS];
   __shared__ int sel;
   lchar* L = (lchar*)smem;
@@ -143,56 +152,125 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int lc = lane & 31, h2 = lane >> 5;
 
+  // unit -> (segment, layer, value head)
   const int u = blockIdx.x;
   const int head = u % a.H_v;
-  const int rank = u / a.H_v;
+  int layer = 0, rank = u / a.H_v;
+  if constexpr (!OUT) {
+    layer = rank % a.n_layers;
+    rank /= a.n_layers;
+  }
   const int b = segment_of_rank(a, rank, &sel);
   const int slot = a.slot_ids ? a.slot_ids[b] : b;
   if (slot < 0) return;
   const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
   const int hk = (head * a.H_k) / a.H_v;
-  const uint16_t* Kp = static_cast<const uint16_t*>(a.Kbuf) + (int64_t)hk * a.T * D;
-  const uint16_t* Qp = static_cast<const uint16_t*>(a.Qbuf) + (int64_t)hk * a.T * D;
-  const uint16_t* Vp = static_cast<const uint16_t*>(a.Vbuf) + (int64_t)head * a.T * D;
-  const uint16_t* Zp = static_cast<const uint16_t*>(a.Zbuf) + (int64_t)head * a.T * D;
-  const float* Gp = a.Gbuf + (int64_t)head * a.T;
-  const float* Bp = a.Bbuf + (int64_t)head * a.T;
+  const uint16_t* Kp;
+  const uint16_t* Vp;
+  const uint16_t* Qp = nullptr;
+  const uint16_t* Zp = nullptr;
+  const float* Gp;
+  const float* Bp;
+  const float* st_in = nullptr;
+  float* st_out;
+  if constexpr (OUT) {
+    Kp = static_cast<const uint16_t*>(a.Kbuf) + (int64_t)hk * a.T * DK;
+    Qp = static_cast<const uint16_t*>(a.Qbuf) + (int64_t)hk * a.T * DK;
+    Vp = static_cast<const uint16_t*>(a.Vbuf) + (int64_t)head * a.T * DV;
+    Zp = static_cast<const uint16_t*>(a.Zbuf) + (int64_t)head * a.T * DV;
+    Gp = a.Gbuf + (int64_t)head * a.T;
+    Bp = a.Bbuf + (int64_t)head * a.T;
+    st_out = a.state_out;
+  } else {
+    Kp = static_cast<const uint16_t*>(a.Kbuf) + layer * a.k_layer_stride + (int64_t)hk * a.T * DK;
+    Vp = static_cast<const uint16_t*>(a.Vbuf) + layer * a.v_layer_stride + (int64_t)head * a.T * DV;
+    Gp = a.Gbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
+    Bp = a.Bbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
+    // per-layer state pointers from the kernel arguments at a uniform offset
+    // (the argument block is the only kernel argument)
+    const char* kargs = (const char*)__builtin_amdgcn_kernarg_segment_ptr();
+    st_in = *reinterpret_cast<const float* const*>(kargs + offsetof(ScanArgs, state_in) + sizeof(void*) * layer);
+    st_out = *reinterpret_cast<float* const*>(kargs + offsetof(ScanArgs, state_out) + sizeof(void*) * layer);
+  }
+  const size_t state_base = ((size_t)slot * a.H_v + head) * DK * DV;
   const int col = 32 * wid + lc;                        // this lane's column of Delta, O and M
-  const int64_t ldy = (int64_t)a.H_v * D;
-  if (tid < D) nws[tid] = __uint_as_float((uint32_t) static_cast<const uint16_t*>(a.norm_w)[tid] << 16);
+  if constexpr (OUT) {
+    if (tid < DV) nws[tid] = __uint_as_float((uint32_t) static_cast<const uint16_t*>(a.norm_w)[tid] << 16);
+  }
 
-  // transposed reads of a row-major bf16 matrix (pitch KP): lane (lc, h2)
-  // receives rows row0 + 4 h2 .. + 3 of column c0 + lc
+  // transposed reads of a row-major bf16 matrix of pitch `pitch`: lane
+  // (lc, h2) receives rows row0 + 4 h2 .. + 3 of column c0 + lc
   const int tr_r = lane & 15;                           // lane within its 16-lane group
   const int tr_n = 16 * ((lane >> 4) & 1) + 4 * (tr_r & 3);
-  auto tr4 = [&](const lchar* base, int row0, int c0) {
-    return lds_tr4(base + ((row0 + 4 * h2 + (tr_r >> 2)) * KP + c0 + tr_n) * 2);
+  auto tr4 = [&](const lchar* base, int pitch, int row0, int c0) {
+    return lds_tr4(base + ((row0 + 4 * h2 + (tr_r >> 2)) * pitch + c0 + tr_n) * 2);
   };
 
   f32x16 M[NT];
 #pragma unroll
-  for (int td = 0; td < NT; ++td) M[td] = zero16();
+  for (int td = 0; td < NT; ++td) {
+    M[td] = zero16();
+    if (st_in) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) M[td][r] = st_in[state_base + (size_t)(32 * td + acc_row(r, lane)) * DV + col];
+    }
+  }
 
   for (int64_t c0 = s0; c0 < s1; c0 += kC) {
     const int n = (int)(s1 - c0 < kC ? s1 - c0 : kC);   // live rows of this chunk
-    // ---- 1. stage K, Q, V, Z rows (zero past the segment end), gates
+    // ---- 1. stage K (, Q), V (, Z) rows (zero past the segment end), gates
+    if constexpr (DK == DV) {
 #pragma unroll
-    for (int i = 0; i < CF::PER_T; ++i) {
+      for (int i = 0; i < CF::PER_K; ++i) {
+        const int p = tid + i * CF::THREADS;
+        const int row = p / (DK / 8), cc = p % (DK / 8);
+        uint4 kv = make_uint4(0, 0, 0, 0), qv = kv, vv = kv, zv = kv;
+        if (row < n) {
+          const int64_t off = (c0 + row) * DK + cc * 8;
+          kv = *reinterpret_cast<const uint4*>(Kp + off);
+          vv = *reinterpret_cast<const uint4*>(Vp + off);
+          if constexpr (OUT) {
+            qv = *reinterpret_cast<const uint4*>(Qp + off);
+            zv = *reinterpret_cast<const uint4*>(Zp + off);
+          }
+        }
+        const int lo = (row * KP + cc * 8) * 2;
+        *reinterpret_cast<uint4*>(smem + CF::OFF_K + lo) = kv;
+        *reinterpret_cast<uint4*>(smem + CF::OFF_V + lo) = vv;
+        if constexpr (OUT) {
+          *reinterpret_cast<uint4*>(smem + CF::OFF_Q + lo) = qv;
+          *reinterpret_cast<uint4*>(smem + CF::OFF_Z + lo) = zv;
+        }
+      }
+    } else {
+#pragma unroll
+    for (int i = 0; i < CF::PER_K; ++i) {
       const int p = tid + i * CF::THREADS;
-      const int row = p / (D / 8), cc = p % (D / 8);
-      uint4 kv = make_uint4(0, 0, 0, 0), qv = kv, vv = kv, zv = kv;
+      const int row = p / (DK / 8), cc = p % (DK / 8);
+      uint4 kv = make_uint4(0, 0, 0, 0), qv = kv;
       if (row < n) {
-        const int64_t off = (c0 + row) * D + cc * 8;
+        const int64_t off = (c0 + row) * DK + cc * 8;
         kv = *reinterpret_cast<const uint4*>(Kp + off);
-        qv = *reinterpret_cast<const uint4*>(Qp + off);
-        vv = *reinterpret_cast<const uint4*>(Vp + off);
-        zv = *reinterpret_cast<const uint4*>(Zp + off);
+        if constexpr (OUT) qv = *reinterpret_cast<const uint4*>(Qp + off);
       }
       const int lo = (row * KP + cc * 8) * 2;
       *reinterpret_cast<uint4*>(smem + CF::OFF_K + lo) = kv;
-      *reinterpret_cast<uint4*>(smem + CF::OFF_Q + lo) = qv;
+      if constexpr (OUT) *reinterpret_cast<uint4*>(smem + CF::OFF_Q + lo) = qv;
+    }
+#pragma unroll
+    for (int i = 0; i < CF::PER_V; ++i) {
+      const int p = tid + i * CF::THREADS;
+      const int row = p / (DV / 8), cc = p % (DV / 8);
+      uint4 vv = make_uint4(0, 0, 0, 0), zv = vv;
+      if (row < n) {
+        const int64_t off = (c0 + row) * DV + cc * 8;
+        vv = *reinterpret_cast<const uint4*>(Vp + off);
+        if constexpr (OUT) zv = *reinterpret_cast<const uint4*>(Zp + off);
+      }
+      const int lo = (row * VP + cc * 8) * 2;
       *reinterpret_cast<uint4*>(smem + CF::OFF_V + lo) = vv;
-      *reinterpret_cast<uint4*>(smem + CF::OFF_Z + lo) = zv;
+      if constexpr (OUT) *reinterpret_cast<uint4*>(smem + CF::OFF_Z + lo) = zv;
+    }
     }
     if (tid < kC) {
       gs[tid] = tid < n ? Gp[c0 + tid] : 0.f;
@@ -213,18 +291,19 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
       eG[lane] = exp2f(x);
       eD[lane] = exp2f(gC - x);
     }
-    // tiles q = 0..5: (0,0), (1,0), (1,1) of K K^T, then of Q K^T
-    constexpr int GQ = (6 + NW - 1) / NW;
+    // tiles q = 0..5: (0,0), (1,0), (1,1) of K K^T, then (outputs only) of Q K^T
+    constexpr int NQ = OUT ? 6 : 3;
+    constexpr int GQ = (NQ + NW - 1) / NW;
     f32x16 gam[GQ];
 #pragma unroll
     for (int nq = 0; nq < GQ; ++nq) {
       gam[nq] = zero16();
       const int q = wid + nq * NW;
-      if (q >= 6) continue;
+      if (q >= NQ) continue;
       const int tq = q % 3, ti = (tq + 1) >> 1, tj = tq >> 1;
       const lchar* Lsrc = q < 3 ? Ks : Qs;
 #pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
+      for (int s = 0; s < DK / 16; ++s) {
         const bf16x8 fa = as_bf16x8(ld16(Lsrc + ((32 * ti + lc) * KP + 16 * s + 8 * h2) * 2));
         const bf16x8 fb = as_bf16x8(ld16(Ks + ((32 * tj + lc) * KP + 16 * s + 8 * h2) * 2));
         gam[nq] = mma(fa, fb, gam[nq]);
@@ -237,7 +316,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
 #pragma unroll
     for (int nq = 0; nq < GQ; ++nq) {
       const int q = wid + nq * NW;
-      if (q >= 6) continue;
+      if (q >= NQ) continue;
       const int tq = q % 3, ti = (tq + 1) >> 1, tj = tq >> 1;
       const int j = 32 * tj + lc;
       const float gj = Gc[j];
@@ -319,11 +398,12 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
     // T diag(beta) as bf16 hi | lo in T's place (the strictly upper 16x16
     // blocks of T are zero; their storage is not written for T)
     {
-      constexpr int PER = kC * kC / 4 / CF::THREADS;   // 4-column pieces per thread
+      constexpr int PER = (kC * kC / 4 + CF::THREADS - 1) / CF::THREADS;   // 4-column pieces per thread
       float tv[PER][4];
 #pragma unroll
       for (int e = 0; e < PER; ++e) {
-        const int p = tid + e * CF::THREADS, row = p / 16, c4 = p % 16;
+        const int p = tid + e * CF::THREADS, c4 = p % 16;
+        const int row = (kC * kC / 4) % CF::THREADS == 0 ? p / 16 : (p / 16) & (kC - 1);   // wraps past the end: unused
         const float4 t4 = ldf4((const lchar*)(Tm + row * kFP + 4 * c4));
         const float4 b4 = ldf4((const lchar*)(bs + 4 * c4));
         const bool upper = (c4 >> 2) > (row >> 4);
@@ -336,6 +416,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
 #pragma unroll
       for (int e = 0; e < PER; ++e) {
         const int p = tid + e * CF::THREADS, row = p / 16, c4 = p % 16;
+        if ((kC * kC / 4) % CF::THREADS != 0 && p >= kC * kC / 4) break;
         const uint32_t h0 = pack_bf16x2(tv[e][0], tv[e][1]), h1 = pack_bf16x2(tv[e][2], tv[e][3]);
         const uint32_t l0 = pack_bf16x2(tv[e][0] - lo_f(h0), tv[e][1] - hi_f(h0));
         const uint32_t l1 = pack_bf16x2(tv[e][2] - lo_f(h1), tv[e][3] - hi_f(h1));
@@ -363,9 +444,13 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
         for (int ti = 0; ti < 2; ++ti) {
           const int off = (32 * ti + lc) * KP * 2;
           const bf16x8 ka = frag_row(Ks + off, 32 * td + 16 * s, h2);
-          const bf16x8 qa = frag_row(Qs + off, 32 * td + 16 * s, h2);
-          X[ti] = mma(ka, ml, mma(ka, mh, X[ti]));
-          O[ti] = mma(qa, ml, mma(qa, mh, O[ti]));
+          if constexpr (OUT) {
+            const bf16x8 qa = frag_row(Qs + off, 32 * td + 16 * s, h2);
+            X[ti] = mma(ka, ml, mma(ka, mh, X[ti]));
+            O[ti] = mma(qa, ml, mma(qa, mh, O[ti]));
+          } else {
+            X[ti] = mma(ka, ml, mma(ka, mh, X[ti]));
+          }
         }
       }
     }
@@ -374,7 +459,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
     for (int tj = 0; tj < 2; ++tj) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
-        const uint2 v4 = tr4(Vs, 32 * tj + 8 * r4, 32 * wid);
+        const uint2 v4 = tr4(Vs, VP, 32 * tj + 8 * r4, 32 * wid);
         const float4 g4 = ldf4((const lchar*)(eG + 32 * tj + 8 * r4 + 4 * h2));
         X[tj][4 * r4 + 0] = fmaf(-g4.x, X[tj][4 * r4 + 0], lo_f(v4.x));
         X[tj][4 * r4 + 1] = fmaf(-g4.y, X[tj][4 * r4 + 1], hi_f(v4.x));
@@ -400,6 +485,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
         }
       }
     // ---- 7. O = diag(2^G) Q M0 + (P o Q K^T) Delta
+    if constexpr (OUT) {
 #pragma unroll
     for (int ti = 0; ti < 2; ++ti)
 #pragma unroll
@@ -429,6 +515,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
     for (int ti = 0; ti < 2; ++ti)
 #pragma unroll
       for (int r = 0; r < 16; ++r) Os[(32 * ti + acc_row(r, lane)) * OP + col] = O[ti][r];
+    }
     // ---- 8. M = 2^{G_C} M0 + K^T diag(2^{G_C - G}) Delta (K^T by transposed reads)
     const float eGC = eG[kC - 1];
 #pragma unroll
@@ -454,15 +541,15 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
 #pragma unroll
         for (int td = 0; td < NT; ++td) {
           const int k0 = 32 * tj + 16 * s;
-          const uint2 x0 = tr4(Ks, k0, 32 * td), x1 = tr4(Ks, k0 + 8, 32 * td);
+          const uint2 x0 = tr4(Ks, KP, k0, 32 * td), x1 = tr4(Ks, KP, k0 + 8, 32 * td);
           const bf16x8 ka = as_bf16x8(make_uint4(x0.x, x0.y, x1.x, x1.y));
           M[td] = mma(ka, dlo, mma(ka, dh, M[td]));
         }
       }
-    lds_barrier();   // the output rows are complete
+    lds_barrier();   // the output rows are complete; every wave is done with T
     // ---- 9. y = o / sqrt(mean(o^2) + eps) * w * SiLU(z): NW lanes per row,
     // 32 columns each
-    {
+    if constexpr (OUT) {
       const int row = tid / NW, part = tid % NW;
       const float* orow = Os + row * OP + 32 * part;
       float ov[32];
@@ -475,12 +562,12 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
       }
 #pragma unroll
       for (int off = 1; off < NW; off <<= 1) ss += __shfl_xor(ss, off);
-      const float inv = __builtin_amdgcn_rsqf(ss / (float)D + a.eps);
+      const float inv = __builtin_amdgcn_rsqf(ss / (float)DV + a.eps);
       if (row < n) {
-        uint16_t* yrow = static_cast<uint16_t*>(a.Y) + (c0 + row) * ldy + (int64_t)head * D + 32 * part;
+        uint16_t* yrow = static_cast<uint16_t*>(a.Y) + (c0 + row) * ((int64_t)a.H_v * DV) + (int64_t)head * DV + 32 * part;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const uint4 z8 = ld16(Zs + (row * KP + 32 * part + 8 * e) * 2);
+          const uint4 z8 = ld16(Zs + (row * VP + 32 * part + 8 * e) * 2);
           const uint32_t zw[4] = {z8.x, z8.y, z8.z, z8.w};
           uint32_t yw[4];
 #pragma unroll
@@ -496,18 +583,28 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_output_kernel(OutputArgs a)
     lds_barrier();   // the next chunk's staging overwrites K, Q, V, Z; A overwrites the output rows
   }
 
-  float* out = a.state_out + ((size_t)slot * a.H_v + head) * D * D;
+  float* out = st_out + state_base;
 #pragma unroll
   for (int td = 0; td < NT; ++td)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) out[(size_t)(32 * td + acc_row(r, lane)) * D + col] = M[td][r];
+    for (int r = 0; r < 16; ++r) out[(size_t)(32 * td + acc_row(r, lane)) * DV + col] = M[td][r];
 }
 
 template <int D>
 hipError_t run_output(const OutputArgs& a, hipStream_t s) {
   const int64_t units = (int64_t)a.n_seg * a.H_v;
   if (units == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_output_kernel<D>), dim3((unsigned)units), dim3(OutCfg<D>::THREADS), 0, s, a);
+  hipLaunchKernelGGL((gdn_chunk_kernel<D, D, true, OutputArgs>), dim3((unsigned)units), dim3(OutCfg<D, D, true>::THREADS),
+                     0, s, a);
+  return hipGetLastError();
+}
+
+template <int DK, int DV>
+hipError_t run_state(const ScanArgs& a, hipStream_t s) {
+  const int64_t units = (int64_t)a.n_seg * a.n_layers * a.H_v;
+  if (units == 0) return hipSuccess;
+  hipLaunchKernelGGL((gdn_chunk_kernel<DK, DV, false, ScanArgs>), dim3((unsigned)units),
+                     dim3(OutCfg<DK, DV, false>::THREADS), 0, s, a);
   return hipGetLastError();
 }
 
@@ -518,6 +615,11 @@ hipError_t launch_gdn_output(int d_head, const OutputArgs& a, hipStream_t s) {
     case 64: return run_output<64>(a, s);
     case 128: return run_output<128>(a, s);
   }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_chunk_state(int d_k, int d_v, const ScanArgs& a, hipStream_t s) {
+  if (d_k == 96 && d_v == 192) return run_state<96, 192>(a, s);
   return hipErrorInvalidValue;
 }
 

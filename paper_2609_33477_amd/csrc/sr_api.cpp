@@ -44,8 +44,11 @@ sr_status check_shape(const sr_shape* s) {
   if (s->d_model < 64 || s->d_model > 16384 || s->d_model % 64 != 0) return SR_ERR_BAD_SHAPE;
   if (s->n_k_heads < 1 || s->n_v_heads < s->n_k_heads || s->n_v_heads > 128) return SR_ERR_BAD_SHAPE;
   if (s->n_v_heads % s->n_k_heads != 0) return SR_ERR_BAD_SHAPE;
-  if (s->d_k != s->d_v) return SR_ERR_BAD_SHAPE;
-  if (s->d_k != 32 && s->d_k != 64 && s->d_k != 128) return SR_ERR_BAD_SHAPE;
+  // square heads d_k = d_v in {32, 64, 128}, or OLMo-Hybrid's 96 x 192
+  // (bf16 anchors, Gated DeltaNet only)
+  const bool square = s->d_k == s->d_v && (s->d_k == 32 || s->d_k == 64 || s->d_k == 128);
+  const bool rect = s->d_k == 96 && s->d_v == 192;
+  if (!square && !rect) return SR_ERR_BAD_SHAPE;
   if (s->conv_width < 1 || s->conv_width > 4) return SR_ERR_BAD_SHAPE;
   if (!(s->l2_eps > 0.f)) return SR_ERR_BAD_SHAPE;
   const bool pair_ok = (s->anchor_dtype == SR_F32 && s->weight_dtype == SR_F32) ||
@@ -56,6 +59,7 @@ sr_status check_shape(const sr_shape* s) {
   if (s->tail_dtype != SR_F32 && s->tail_dtype != SR_BF16) return SR_ERR_UNSUPPORTED_DTYPE;
   if (s->recurrence != SR_RECURRENCE_GDN && s->recurrence != SR_RECURRENCE_DECAY) return SR_ERR_BAD_SHAPE;
   if (s->recurrence == SR_RECURRENCE_DECAY && s->anchor_dtype != SR_BF16) return SR_ERR_UNSUPPORTED_DTYPE;
+  if (rect && (s->anchor_dtype != SR_BF16 || s->recurrence != SR_RECURRENCE_GDN)) return SR_ERR_UNSUPPORTED_DTYPE;
   return SR_OK;
 }
 
@@ -64,21 +68,23 @@ struct Plan {
   int64_t off_flag, off_p, off_info, off_k, off_v, off_g, off_b, total;
   int64_t k_stride, v_stride, g_stride;   // per-layer strides (elements)
   int op_dtype, op_bytes;
+  bool fused;                        // bf16 square heads: projection fused with the conv epilogue
 };
 
 Plan make_plan(const sr_shape* s, int32_t n_layers, int64_t T) {
   Plan p{};
-  const int64_t hk = s->n_k_heads, hv = s->n_v_heads, d = s->d_k;
-  const int64_t N = (hk + hv) * d + 2 * hv;
+  const int64_t hk = s->n_k_heads, hv = s->n_v_heads;
+  const int64_t N = hk * s->d_k + hv * s->d_v + 2 * hv;
   p.ldp = align_up(N, 4);
   p.op_dtype = s->anchor_dtype == SR_F32 ? SR_F32 : SR_BF16;
   p.op_bytes = dtype_bytes(p.op_dtype);
-  p.k_stride = hk * T * d;
-  p.v_stride = hv * T * d;
+  p.fused = p.op_dtype == SR_BF16 && s->d_k == s->d_v;
+  p.k_stride = hk * T * s->d_k;
+  p.v_stride = hv * T * s->d_v;
   p.g_stride = hv * T;
   int64_t off = 0;
   p.off_flag = off; off = align_up(off + 4, kAlign);   // the table check's result word
-  if (p.op_dtype == SR_F32) {        // only the unfused fp32 path stores the projection
+  if (!p.fused) {                    // only the unfused paths store the projection
     p.off_p = off; off = align_up(off + T * p.ldp * 4, kAlign);
   } else {
     p.off_info = off; off = align_up(off + T * (int64_t)sizeof(sr::RowInfo), kAlign);
@@ -215,7 +221,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   const int hk = shape->n_k_heads, hv = shape->n_v_heads, d = shape->d_k, w = shape->conv_width;
-  const int c_k = hk * d, c_v = hv * d;
+  const int c_k = hk * shape->d_k, c_v = hv * shape->d_v;
   float* P = reinterpret_cast<float*>(ws + plan.off_p);
   char* Kb = ws + plan.off_k;
   char* Vb = ws + plan.off_v;
@@ -228,7 +234,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       }) != hipSuccess)
     return SR_ERR_HIP;
 
-  const bool fused = plan.op_dtype == SR_BF16;
+  const bool fused = plan.fused;
   sr::RowInfo* info = reinterpret_cast<sr::RowInfo*>(ws + plan.off_info);
   if (fused && t_total > 0) {
     if (timed(SR_KERNEL_ROW_INFO, s, [&] { return sr::launch_row_info(cu_seqlens, slot_ids, n_segments, info, flag, s); }) != hipSuccess)
@@ -321,6 +327,8 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       c.dt_bias = L.dt_bias;
       c.H_k = hk;
       c.H_v = hv;
+      c.d_k = shape->d_k;
+      c.d_v = shape->d_v;
       c.eps = shape->l2_eps;
       c.Kbuf = Kb + (int64_t)l * plan.k_stride * plan.op_bytes;
       c.Vbuf = Vb + (int64_t)l * plan.v_stride * plan.op_bytes;
@@ -363,6 +371,9 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
     }
     if (shape->recurrence == SR_RECURRENCE_DECAY) {
       if (timed(SR_KERNEL_DECAY_STATE, s, [&] { return sr::launch_decay_state(d, a, s); }) != hipSuccess)
+        return SR_ERR_HIP;
+    } else if (shape->d_k != shape->d_v) {
+      if (timed(SR_KERNEL_GDN_SCAN, s, [&] { return sr::launch_chunk_state(shape->d_k, shape->d_v, a, s); }) != hipSuccess)
         return SR_ERR_HIP;
     } else if (timed(SR_KERNEL_GDN_SCAN, s, [&] { return sr::launch_scan(plan.op_dtype, d, a, s); }) != hipSuccess)
       return SR_ERR_HIP;

@@ -121,12 +121,16 @@ struct ConvGateArgs {
   int32_t c_tail;
   int32_t tail_kv_off;  // first k channel inside the tail (q channels precede)
   const int32_t* err;   // the call's table-check flag: non-zero = write nothing
+  // key and value head widths; d_k != d_v takes the one-head-per-wave kernel
+  // (bf16 operands), whose G is log2 alpha (the chunk kernel's convention)
+  int32_t d_k, d_v;
 };
 
 hipError_t launch_conv_gate(int op_dtype, int conv_dtype, int tail_dtype, int d_head,
                             const ConvGateArgs& a, hipStream_t s);
 
-// fp32 anchors only (the bf16 tail rides in the fused projection's grid)
+// fp32 anchors: per-segment dot products; bf16 anchors: the q-tail blocks on
+// their own (the fused projection's grid carries them when it runs)
 hipError_t launch_tail(int anchor_dtype, int weight_dtype, int tail_dtype, const TailArgs& a,
                        hipStream_t s);
 
@@ -211,6 +215,9 @@ struct OutputArgs {
   const int32_t* err;
 };
 hipError_t launch_gdn_output(int d_head, const OutputArgs& a, hipStream_t s);
+// State-only chunked scan of heads with d_k != d_v (bf16 operands, log2 alpha
+// gates), the same chunk algebra as the output kernel; (d_k, d_v) = (96, 192)
+hipError_t launch_chunk_state(int d_k, int d_v, const ScanArgs& a, hipStream_t s);
 
 // ------------------------------------------------------ varlen table check
 // One workgroup: writes 0 or a mask of sr_varlen_error bits to *flag and

@@ -256,3 +256,25 @@ def test_group_replay_host_checks():
     with pytest.raises(sr.SrError) as e:
         sr.replay_group(g, 9728, 1e-6, [blk], **{**args, "anchors": 0x900008})
     assert e.value.status == 5
+
+
+def test_rect_heads_host_checks():
+    """OLMo-Hybrid's 96 x 192 heads are accepted for bf16 anchors with the
+    Gated DeltaNet recurrence; other rectangles and the other paths refuse."""
+    rect = Shape(3840, 30, 30, 96, 192)
+    T = 1000
+    ws = sr.replay_workspace_size(rect, 1, T)
+    # unfused: the fp32 projection rows, bf16 k | v, fp32 gates
+    n = 30 * 96 + 30 * 192 + 60
+    assert ws >= T * n * 4 + T * 30 * (96 + 192) * 2 + 2 * T * 30 * 4
+    for bad in (Shape(256, 2, 2, 96, 96), Shape(256, 2, 2, 64, 192), Shape(256, 2, 2, 192, 96),
+                Shape(256, 2, 2, 96, 128)):
+        with pytest.raises(sr.SrError) as e:
+            sr.replay_workspace_size(bad, 1, T)
+        assert e.value.status == 2, bad
+    f32 = Shape(256, 2, 2, 96, 192, anchor_dtype=F32, weight_dtype=F32, conv_dtype=F32, tail_dtype=F32)
+    decay = Shape(256, 2, 2, 96, 192, recurrence="decay")
+    for bad in (f32, decay):
+        with pytest.raises(sr.SrError) as e:
+            sr.replay_workspace_size(bad, 1, T)
+        assert e.value.status == 3, bad

@@ -238,13 +238,18 @@ CONFIG_NAMES = ("tiny", "gdn_single", "varlen16", "multilayer12", "stress64")
 # Variants of a named workload: same seed and tensors, another recurrence.
 VARIANTS = {"varlen16_decay": ("varlen16", "decay")}
 
+# Workloads beyond the five: OLMo-Hybrid-7B's linear-layer shape (Appendix A:
+# d_model 3840, 30 key and 30 value heads, d_k = 96, d_v = 192) on
+# varlen16's length distribution.
+EXTRA_SEEDS = {"olmo_varlen": 6}
+
 
 def _config_table(name: str):
     if name in VARIANTS:
         base, rec = VARIANTS[name]
         seed, shape, seg, n_layers, mu = _config_table(base)
         return seed, replace(shape, recurrence=rec), seg, n_layers, mu
-    seed = CONFIG_NAMES.index(name) + 1
+    seed = EXTRA_SEEDS[name] if name in EXTRA_SEEDS else CONFIG_NAMES.index(name) + 1
     rng = np.random.default_rng((seed, SEGMENT_STREAM))
     if name == "tiny":
         shape = Shape(128, 2, 2, 32, 32, anchor_dtype=F32, weight_dtype=F32,
@@ -259,6 +264,8 @@ def _config_table(name: str):
     if name == "stress64":
         return (seed, Shape(4096, 32, 32, 128, 128), _page_lengths(rng, 64, 1024, 8192), 1,
                 LONG_MEMORY_DT_BIAS_MEAN)
+    if name == "olmo_varlen":
+        return seed, Shape(3840, 30, 30, 96, 192), _page_lengths(rng, 16, 512, 4096), 1, 0.0
     raise KeyError(name)
 
 
@@ -280,6 +287,8 @@ def make_config(name: str) -> Workload:
     stress64      64 requests, L ~ 64*U{16..128}, D=4096, H=32, bf16,
                   dt_bias shifted so mean alpha is 0.995
     varlen16_decay  varlen16's inputs under the per-head-decay recurrence
+    olmo_varlen   16 requests, L ~ 64*U{8..64}, D=3840, H=30, d_k=96, d_v=192,
+                  bf16 (OLMo-Hybrid-7B's linear layers)
     Weights ~ N(0, 0.02), anchors ~ N(0, 1), A_log ~ U(log 1, log 16),
     dt_bias ~ N(mu, 0.5), zero initial state.
     """
