@@ -74,7 +74,10 @@ typedef enum sr_dtype {
 /* Shape and storage types of one linear-attention layer.
  *  d_model     anchor width D; multiple of 64, 64 <= D <= 16384
  *  n_k_heads   H_k >= 1;  n_v_heads H_v, a multiple of H_k, H_v <= 128
- *  d_k, d_v    head dims; each 32, 64 or 128
+ *  d_k, d_v    head dims: d_k = d_v in {32, 64, 128}, or d_k = 96 with
+ *              d_v = 192 (OLMo-Hybrid-7B, Appendix A; BF16 anchors and the
+ *              Gated DeltaNet recurrence only, SR_ERR_UNSUPPORTED_DTYPE
+ *              otherwise); any other pair is SR_ERR_BAD_SHAPE
  *  conv_width  w in 1..4 (the paper's models use 4)
  *  l2_eps      key-norm epsilon (> 0)
  *  dtypes      supported (anchor, weight) pairs: (F32, F32), (BF16, BF16),
