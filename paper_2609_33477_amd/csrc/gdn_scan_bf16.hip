@@ -23,8 +23,10 @@
 //     16x16 fp32 accumulator tiles for the whole segment: at step n they
 //     run the state lines of sub-chunk n from registers, then read the
 //     operands of sub-chunk n+1, so the reads' latency overlaps the MFMAs
-//     and the barrier; they request K(n+4) and V(n+3) by global -> LDS
-//     DMA, waited for one step later.
+//     and the barrier.
+// K(n+4) and V(n+3) go global -> LDS by DMA, requested at step n by the prep
+// wave whose phase there is Gram or A (the two lightest) and waited for one
+// step later, so the state waves issue nothing but LDS reads and MFMAs.
 // Rings (sub-chunk slots): K 4, V 3, W 2, Tu 4, gate vectors 16.
 //
 // Every product is v_mfma_f32_16x16x32_bf16.  A 32-wide reduction over
@@ -131,7 +133,7 @@ struct Cfg {
   static constexpr int RPL = 128 / D;                 // rows per 256-byte bank line
   static constexpr int NCP = D / 16;                  // 32-byte chunk pairs per row
   static constexpr int DMA_ROWS = 512 / D;            // rows per 1 KB DMA block
-  static constexpr int DMA_PER = kS * 2 * D / 1024 / NSW;   // DMA blocks per state wave and matrix
+  static constexpr int DMA_BLK = kS * 2 * D / 1024;         // 1 KB DMA blocks of one K or V sub-chunk
   static constexpr int WP = D + 16;                   // W row pitch (bf16): 16-byte row reads
   static constexpr int NK = 4;                        // K ring: K(n) DMA issued at step n-4
   static constexpr int NV = 3;                        // V ring: V(n) DMA issued at step n-3
@@ -154,7 +156,7 @@ struct Cfg {
   static constexpr int OFF_PRIV = OFF_VEC + NVEC * SZ_VEC;
   static constexpr int LDS = OFF_PRIV + NP * SZ_PRIV;
   static constexpr int QG = D / 32;                   // 32-wide d blocks (Gram k-steps)
-  static_assert(DMA_PER * NSW * 1024 == kS * 2 * D, "staging split");
+  static_assert(DMA_BLK * 1024 == kS * 2 * D, "staging split");
   static_assert(NT % 2 == 0, "state tiles pair up along d");
   static_assert(2 * SZ_TT <= 2 * SZ_A, "Tw^T of both sub-chunks reuses the A^T area");
   static_assert(LDS <= 160 * 1024, "LDS");
@@ -248,6 +250,69 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     float gv = 0.f, bv = 0.f;
     f32x4 gr[2][3];        // Gram tiles (0,0), (1,0), (1,1) of each sub-chunk
     float x[kS];           // column `col` of T, carried over the solve phases
+
+    // DMA staging of K and V, global -> LDS: at step n the prep wave in its
+    // Gram or A phase (the two lightest) requests K(n + 4) and V(n + 3), all
+    // DMA_BLK 1 KB blocks of each, and waits for them at the end of step
+    // n + 1, before the barrier that publishes them (K(j) is read from step
+    // j - 2 on, V(j) at step j - 1).  Lane l carries the 16 bytes at byte
+    // 16 l of a block: dma_off is their byte offset from the sub-chunk's first
+    // row in the swizzled layout.  Rows past the segment end are read from
+    // its last row: their beta and log decay are 0, so T has unit rows and
+    // zero columns there and any finite values are multiplied by exact zeros.
+    uint32_t dma_off[CF::DMA_BLK];
+#pragma unroll
+    for (int i = 0; i < CF::DMA_BLK; ++i) {
+      const int byte = i * 1024 + 16 * lane;
+      const int r = byte / (2 * D), pos = byte % (2 * D);
+      const int cbp = (pos / 32) ^ ((r / CF::RPL) % CF::NCP);
+      dma_off[i] = (uint32_t)((r * D + 16 * cbp + 8 * ((pos / 16) & 1)) * 2);
+    }
+    auto stage = [&](const char* plane, int j, lchar* buf) {
+      const int64_t c0 = s0 + (int64_t)j * kS;
+      const char* base = plane + c0 * D * 2;
+      const uint32_t lds0 = (uint32_t)(uintptr_t)buf;
+      if (c0 + kS <= s1) {
+#pragma unroll
+        for (int i = 0; i < CF::DMA_BLK; ++i) dma16_s(base, dma_off[i], lds0 + i * 1024);
+      } else {
+        const uint32_t last = (uint32_t)(s1 - 1 - c0);
+#pragma unroll
+        for (int i = 0; i < CF::DMA_BLK; ++i) {
+          const uint32_t r = dma_off[i] / (2 * D), rc = r < last ? r : last;
+          dma16_s(base, dma_off[i] - (r - rc) * (2 * D), lds0 + i * 1024);
+        }
+      }
+    };
+    // the owner of step n: the wave whose phase there is its Gram (even n)
+    // or its A (odd n)
+    auto dma_owner = [](int nn) { return ((nn - (nn & 1)) >> 1) & 3; };
+    int n = -9;                      // the step; every prep barrier advances it
+    int dma_cur = 0, dma_prev = 0;   // blocks this wave requested in this / the previous step
+    auto dma_duty = [&](int nn) {
+      if (dma_owner(nn) != p) return;
+      if (nn + 4 >= 0 && nn + 4 < nsc) {
+        stage(Kplane, nn + 4, kbuf(nn + 4));
+        dma_cur += CF::DMA_BLK;
+      }
+      if (nn + 3 >= 0 && nn + 3 < nsc) {
+        stage(Vplane, nn + 3, vbuf(nn + 3));
+        dma_cur += CF::DMA_BLK;
+      }
+    };
+    // the barrier that ends step nn: the previous step's requests have
+    // landed (this step's may still be in flight)
+    auto pbar = [&](int& nn) {
+      if (dma_prev) {
+        if (dma_cur == 0) wait_vm<0>();
+        else if (dma_cur == CF::DMA_BLK) wait_vm<CF::DMA_BLK>();
+        else wait_vm<2 * CF::DMA_BLK>();
+      }
+      lds_barrier();
+      ++nn;
+      dma_prev = dma_cur;
+      dma_cur = 0;
+    };
 
     // phase 7 of the previous pair: the pair's K rows straight from global
     // memory as Gram fragments, and this lane's log2 alpha and beta.  Rows
@@ -364,7 +429,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       for (int i = 0; i < kS; ++i) x[i] = (i == cl) ? 1.f : 0.f;
 #pragma unroll
       for (int q = 0; q < kS; ++q) {
-        if (q == 6 || q == 14) lds_barrier();          // phases 4 and 5 start here
+        if (q == 6 || q == 14) pbar(n);                // phases 4 and 5 start here
         if (q + 2 < kS) load_col(q + 2, cb[(q + 2) % 3]);
         const float xq = x[q];
         const float4* cv = cb[q % 3];
@@ -442,79 +507,47 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
 
     // steps -9 .. nsc-1, one barrier each: pair m runs phase s at step
     // m - 9 + s, and phase 0 also finishes the previous pair
-    int n = -9;
-    for (; n < 2 * p - 9 && n < nsc; ++n) lds_barrier();
+    while (n < 2 * p - 9 && n < nsc) {
+      dma_duty(n);
+      pbar(n);
+    }
     int m = 2 * p;
     if (m < nsc) issue_loads(m);
     for (; m < nsc; m += 8) {
       if (m >= 8) make_w(m - 7, 1);            // m - 7 < nsc: the previous pair's second sub-chunk
-      lds_barrier();
+      pbar(n);
       gram(m);
-      lds_barrier();
+      dma_duty(n);                             // after the Gram fragments' loads were waited for
+      pbar(n);
       make_a();
       load_col(0, cb[0]);                      // the solve's first columns (same wave: after the A stores)
       load_col(1, cb[1]);
-      lds_barrier();
+      dma_duty(n);
+      pbar(n);
       solve();                                 // phases 3, 4 and 5 (two barriers inside)
-      lds_barrier();
+      pbar(n);
       pack(m);
-      lds_barrier();
+      pbar(n);
       make_w(m, 0);
       if (m + 8 < nsc) issue_loads(m + 8);     // two steps before its Gram
-      lds_barrier();
-      n += 8;
+      pbar(n);
     }
     if (m >= 8 && m - 7 < nsc) {                 // the last pair's second sub-chunk, at step m - 9
       make_w(m - 7, 1);
-      lds_barrier();
-      ++n;
+      dma_duty(n);
+      pbar(n);
     }
-    for (; n < nsc; ++n) lds_barrier();
+    while (n < nsc) {
+      dma_duty(n);
+      pbar(n);
+    }
     return;
   }
 
   // ================================================================== state
   // tile (td, cc) holds M[16 td + 4g + r][32 sw + 16 cc + li]
   const int sw = wid - NP;
-  const int stid = tid - 64 * NP;
   f32x4 M[NT][2];
-
-  // DMA staging of K and V: this wave moves blocks DMA_PER sw .. + DMA_PER - 1
-  // (1 KB each) of a sub-chunk; lane l carries the 16 bytes at byte 16 l of
-  // its block, i.e. row dma_row[i] and logical columns dma_col[i] .. + 7 of
-  // the swizzled layout.  Rows past the segment end are read from its last
-  // row: their beta and log decay are 0, so T has unit rows and zero columns
-  // there and any finite values are multiplied by exact zeros.
-  int dma_row[CF::DMA_PER], dma_col[CF::DMA_PER];
-#pragma unroll
-  for (int i = 0; i < CF::DMA_PER; ++i) {
-    const int byte = (CF::DMA_PER * sw + i) * 1024 + 16 * lane;
-    const int r = byte / (2 * D), pos = byte % (2 * D);
-    const int cb = (pos / 32) ^ ((r / CF::RPL) % CF::NCP);
-    dma_row[i] = r;
-    dma_col[i] = 16 * cb + 8 * ((pos / 16) & 1);
-  }
-  // the sub-chunk's first row is a wave-uniform base; each lane adds its
-  // fixed byte offset, clamped to the last row only in a partial sub-chunk
-  uint32_t dma_off[CF::DMA_PER];
-#pragma unroll
-  for (int i = 0; i < CF::DMA_PER; ++i) dma_off[i] = (uint32_t)((dma_row[i] * D + dma_col[i]) * 2);
-  auto stage = [&](const char* plane, int m, lchar* buf) {
-    const int64_t c0 = s0 + (int64_t)m * kS;
-    const char* base = plane + c0 * D * 2;
-    const uint32_t lds0 = (uint32_t)(uintptr_t)buf + CF::DMA_PER * sw * 1024;
-    if (c0 + kS <= s1) {
-#pragma unroll
-      for (int i = 0; i < CF::DMA_PER; ++i) dma16_s(base, dma_off[i], lds0 + i * 1024);
-    } else {
-      const int last = (int)(s1 - 1 - c0);
-#pragma unroll
-      for (int i = 0; i < CF::DMA_PER; ++i) {
-        const int r = dma_row[i] < last ? dma_row[i] : last;
-        dma16_s(base, (uint32_t)((r * D + dma_col[i]) * 2), lds0 + i * 1024);
-      }
-    }
-  };
 
   // The operands of a state step, read one step ahead: during step n the
   // wave issues the MFMAs of sub-chunk n from registers, then reads
@@ -595,24 +628,11 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
           M[td][cc][r] = st_in[state_base + (size_t)(16 * td + 4 * g + r) * D + 32 * sw + 16 * cc + li];
       }
     }
-  // The initial state has landed before the first DMA is issued: the
-  // compiler does not count the DMAs, so a wait for these loads placed inside
-  // the loop would be vmcnt(0) and stall every step on the DMAs in flight.
-  wait_vm<0>();
-
   // ---- steps -9 .. nsc-1: the state lines of sub-chunk n, then the reads
-  // of sub-chunk n+1's operands.  K(n+4) and V(n+3) are requested here and
-  // waited for at the end of the next step, before the barrier that
-  // publishes them (K(j) is read from step j-2 on, V(j) at step j-1)
+  // of sub-chunk n+1's operands (K and V arrive by the prep waves' DMAs)
   for (int n = -9; n < nsc; ++n) {
-    const bool k_dma = n + 4 >= 0 && n + 4 < nsc, v_dma = n + 3 >= 0 && n + 3 < nsc;
-    if (k_dma) stage(Kplane, n + 4, kbuf(n + 4));
-    if (v_dma) stage(Vplane, n + 3, vbuf(n + 3));
     if (n >= 0) state_step();
     if (n + 1 >= 0 && n + 1 < nsc) load_ops(n + 1);
-    if (k_dma && v_dma) wait_vm<2 * CF::DMA_PER>();
-    else if (k_dma || v_dma) wait_vm<CF::DMA_PER>();
-    else wait_vm<0>();
     lds_barrier();
   }
 
