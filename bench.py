@@ -46,6 +46,9 @@ def log(msg):
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
+PROJ_LAYERS_PER_LAUNCH = 4   # layers of one call that share a fused-projection launch
+
+
 def algorithmic_work(wl, with_q=True):
     """Per-launch algorithmic work of each kernel (flops for the MFMA GEMM,
     HBM bytes for the streaming kernels), from the shapes alone."""
@@ -61,6 +64,9 @@ def algorithmic_work(wl, with_q=True):
     n_layers = len(wl.layers)
     c_q = hk * sh.d_k if with_q else 0
     tail_rows = len(live) * (w - 1)
+    # the fused projection covers PROJ_LAYERS_PER_LAUNCH layers per launch:
+    # its per-launch work is the average over the call's launches
+    proj_layers = n_layers / -(-n_layers // PROJ_LAYERS_PER_LAUNCH)
     return {
         # one launch per layer
         "proj_gemm": ("mfma", 2.0 * T * D * N),
@@ -69,7 +75,7 @@ def algorithmic_work(wl, with_q=True):
         # HBM traffic is anchors + weights in, k_hat | v | G | beta out.  The
         # q part of the conv tail (a GEMM over the live segments' last w-1
         # rows) runs in the same grid.
-        "proj_conv": ("mfma", 2.0 * T * D * N + 2.0 * tail_rows * D * c_q),
+        "proj_conv": ("mfma", proj_layers * (2.0 * T * D * N + 2.0 * tail_rows * D * c_q)),
         # fp32 anchors: the tail's own launch
         "tail": ("hbm", c_q * D * wb + tail_rows * ((c_q + c_kv) * tb + D * es)),
         # one launch per call: 16 bytes of segment info per row

@@ -52,6 +52,7 @@
 #include "sr_device.hpp"
 #include "tail_q.hpp"
 
+#include <cstddef>
 #include <type_traits>
 #include <utility>
 
@@ -194,8 +195,14 @@ __device__ __forceinline__ void store_elem(void* p, int64_t i, float v, bool is_
 }
 
 template <typename TB, int D>
-__global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, int tiles_m, int tiles_n) {
-  if (a.err && *a.err) return;   // the call's table check failed: write nothing
+__global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb, int tiles_m, int tiles_n) {
+  // The batch is the kernel's first argument: a layer's arguments are read
+  // from the argument segment at a block-uniform offset.
+  const char* kargs = (const char*)__builtin_amdgcn_kernarg_segment_ptr();
+  auto layer_args = [&](int l) -> const ProjConvArgs& {
+    return *reinterpret_cast<const ProjConvArgs*>(kargs + offsetof(ProjConvBatch, layer) + l * sizeof(ProjConvArgs));
+  };
+  if (pb.layer[0].err && *pb.layer[0].err) return;   // the call's table check failed: write nothing
   constexpr int BROW = BT<TB>::ROW, BBLK = BT<TB>::BLKS, NS = BT<TB>::NS;
   constexpr int A_BYTES = BM * 64, B_BYTES = BN * BROW, STAGE = A_BYTES + B_BYTES;
   constexpr int LPK = 2 + BBLK;  // DMA instructions per wave per K-step
@@ -204,9 +211,14 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   __shared__ __attribute__((aligned(1024))) char smem_raw[LDS];
   lchar* smem = (lchar*)smem_raw;
   static_assert(LDS >= kTqLds && THREADS == 64 * kTqWaves, "q-tail blocks share the tile's LDS and waves");
-  if ((int)blockIdx.x >= tiles_m * tiles_n) {
-    const int b = (int)blockIdx.x - tiles_m * tiles_n, gx = tail_q_grid_x(a.tq);
-    tail_q_block<TB>(a.tq, b % gx, b / gx, smem_raw);
+  const int n_tiles = pb.n_layers * tiles_m * tiles_n;
+  if ((int)blockIdx.x >= n_tiles) {
+    const int b = (int)blockIdx.x - n_tiles;
+    int l = 0;
+    while (l + 1 < pb.n_layers && b >= pb.tq_off[l + 1]) ++l;
+    const TailArgs& tq = layer_args(l).tq;
+    const int bl = b - pb.tq_off[l], gx = tail_q_grid_x(tq);
+    tail_q_block<TB>(tq, bl % gx, bl / gx, smem_raw);
     return;
   }
 
@@ -214,8 +226,12 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int wm = wid >> 1, wn = wid & 1;                       // 64-row x 128-column sub-tile
   const int hf = lane >> 5, lc = lane & 31;
+  // m-tiles of the layers stacked: the XCD-aware walk runs over all of them
   int mt, nt;
-  tile_of(blockIdx.x, tiles_m, tiles_n, mt, nt);
+  tile_of(blockIdx.x, pb.n_layers * tiles_m, tiles_n, mt, nt);
+  const int layer = mt / tiles_m;
+  mt -= layer * tiles_m;
+  const ProjConvArgs& a = layer_args(layer);
   const int64_t row0 = (int64_t)mt * SM - HALO;  // tile row 0 (negative for the first tile)
   const int n0 = nt * BN;
   const int K = a.K;
@@ -658,17 +674,18 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvArgs a, i
 }
 
 template <typename TB, int D>
-hipError_t run(const ProjConvArgs& a, hipStream_t s) {
+hipError_t run(const ProjConvBatch& b, hipStream_t s) {
+  const ProjConvArgs& a = b.layer[0];
   if (a.K % BK) return hipErrorInvalidValue;
   const int tm = (int)((a.T + SM - 1) / SM), tn = (a.N + BN - 1) / BN;
-  const int blocks = tm * tn + a.tq_blocks;
+  const int blocks = b.n_layers * tm * tn + b.tq_off[b.n_layers];
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((proj_conv_kernel<TB, D>), dim3(blocks), dim3(THREADS), 0, s, a, tm, tn);
+  hipLaunchKernelGGL((proj_conv_kernel<TB, D>), dim3(blocks), dim3(THREADS), 0, s, b, tm, tn);
   return hipGetLastError();
 }
 
 template <typename TB>
-hipError_t by_head(int d, const ProjConvArgs& a, hipStream_t s) {
+hipError_t by_head(int d, const ProjConvBatch& a, hipStream_t s) {
   switch (d) {
     case 32: return run<TB, 32>(a, s);
     case 64: return run<TB, 64>(a, s);
@@ -702,10 +719,22 @@ hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n
   return hipGetLastError();
 }
 
-hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvArgs& a, hipStream_t s) {
-  if (weight_dtype == SR_BF16) return by_head<bf16_t>(d_head, a, s);
-  if (weight_dtype == SR_FP8_E4M3) return by_head<fp8_t>(d_head, a, s);
+hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvBatch& b, hipStream_t s) {
+  if (b.n_layers < 1 || b.n_layers > kProjBatch) return hipErrorInvalidValue;
+  for (int l = 1; l < b.n_layers; ++l)
+    if (b.layer[l].T != b.layer[0].T || b.layer[l].K != b.layer[0].K || b.layer[l].N != b.layer[0].N)
+      return hipErrorInvalidValue;
+  if (weight_dtype == SR_BF16) return by_head<bf16_t>(d_head, b, s);
+  if (weight_dtype == SR_FP8_E4M3) return by_head<fp8_t>(d_head, b, s);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvArgs& a, hipStream_t s) {
+  ProjConvBatch b{};
+  b.layer[0] = a;
+  b.n_layers = 1;
+  b.tq_off[1] = a.tq_blocks;
+  return launch_proj_conv(weight_dtype, d_head, b, s);
 }
 
 }  // namespace sr

@@ -241,6 +241,14 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       return SR_ERR_HIP;
   }
 
+  // fused projections are launched kProjBatch layers at a time
+  sr::ProjConvBatch pb{};
+  auto flush_proj = [&]() {
+    if (pb.n_layers == 0) return hipSuccess;
+    const hipError_t e = timed(SR_KERNEL_PROJ_CONV, s, [&] { return sr::launch_proj_conv(shape->weight_dtype, d, pb, s); });
+    pb.n_layers = 0;
+    return e;
+  };
   for (int l = 0; l < n_layers; ++l) {
     const sr_layer& L = layers[l];
     const int c_q = L.w_q ? c_k : 0;
@@ -299,8 +307,9 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
         f.tq = t;
         f.tq_blocks = sr::tail_q_grid_x(t) * sr::tail_q_grid_y(t);
       }
-      if (timed(SR_KERNEL_PROJ_CONV, s, [&] { return sr::launch_proj_conv(shape->weight_dtype, d, f, s); }) != hipSuccess)
-        return SR_ERR_HIP;
+      pb.layer[pb.n_layers] = f;
+      pb.tq_off[pb.n_layers + 1] = pb.tq_off[pb.n_layers] + f.tq_blocks;
+      if (++pb.n_layers == sr::kProjBatch && flush_proj() != hipSuccess) return SR_ERR_HIP;
     } else if (t_total > 0) {
       sr::GemmArgs g{};
       g.A = L.anchors;
@@ -346,6 +355,8 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
         return SR_ERR_HIP;
     }
   }
+
+  if (flush_proj() != hipSuccess) return SR_ERR_HIP;
 
   for (int l0 = 0; l0 < n_layers; l0 += sr::kScanMaxLayers) {
     const int nl = n_layers - l0 < sr::kScanMaxLayers ? n_layers - l0 : sr::kScanMaxLayers;

@@ -95,8 +95,20 @@ struct ProjConvArgs {
   int32_t tq_blocks;
 };
 
+// The projections of up to kProjBatch layers of one call in one launch: every
+// layer of a call has the same T and N, so the grid holds the tiles of all of
+// them (a small batch leaves CUs idle in a launch of its own), then their
+// q-tail blocks.
+constexpr int kProjBatch = 4;
+struct ProjConvBatch {
+  ProjConvArgs layer[kProjBatch];   // layers 0 .. n_layers-1; T, K and N equal
+  int32_t n_layers;
+  int32_t tq_off[kProjBatch + 1];   // layer i's q-tail blocks: [tq_off[i], tq_off[i+1]) after the tiles
+};
+
 hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, RowInfo* info,
                            const int32_t* err, hipStream_t s);
+hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvBatch& b, hipStream_t s);
 hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvArgs& a, hipStream_t s);
 
 // --------------------------------------------------- conv, activations, gates
