@@ -66,6 +66,12 @@ constexpr int HALO = 3, SM = BM - HALO;           // tile row stride
 constexpr int XB_BYTES = WAVES * 64 * 12 * 4;
 constexpr int INV_BYTES = WAVES * 2 * 4 * 32 * 4;
 constexpr int EPI_BYTES = XB_BYTES + INV_BYTES;
+// Gate columns go through the LDS (below the exchange area) so that one store
+// covers 64 consecutive rows of a head: per wave a 32-column block, column
+// pitch 68 floats (17 x 16 bytes: the 16-byte writes of 16 lanes fall on
+// distinct bank groups).
+constexpr int GATE_PITCH = 68;
+constexpr int GATE_BYTES = WAVES * 32 * GATE_PITCH * 4;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -184,7 +190,10 @@ __device__ __forceinline__ float col_scale(const ProjConvArgs& a, int n) {
 }
 
 __device__ __forceinline__ float fast_sigmoid(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
-__device__ __forceinline__ float softplus(float x) { return fmaxf(x, 0.f) + log1pf(__expf(-fabsf(x))); }
+// max(x, 0) + ln(1 + e^-|x|) on the hardware exp and log: where e^-|x| is
+// below half an ulp of 1 the second term drops out, an absolute error under
+// 6e-8 in a value that then scales a log-decay
+__device__ __forceinline__ float softplus(float x) { return fmaxf(x, 0.f) + __logf(1.f + __expf(-fabsf(x))); }
 
 __device__ __forceinline__ float load_elem(const void* p, int64_t i, bool is_bf16) {
   return is_bf16 ? bf16_bits_to_f32(static_cast<const uint16_t*>(p)[i]) : static_cast<const float*>(p)[i];
@@ -211,6 +220,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
   __shared__ __attribute__((aligned(1024))) char smem_raw[LDS];
   lchar* smem = (lchar*)smem_raw;
   static_assert(LDS >= kTqLds && THREADS == 64 * kTqWaves, "q-tail blocks share the tile's LDS and waves");
+  static_assert(GATE_BYTES <= EPI_OFF, "gate transposes below the epilogue exchange area");
   const int n_tiles = pb.n_layers * tiles_m * tiles_n;
   if ((int)blockIdx.x >= n_tiles) {
     const int b = (int)blockIdx.x - n_tiles;
@@ -650,22 +660,49 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
         });
       }
     } else {
-      // ---- gate columns: G = log2 alpha from a, beta from b (no conv)
+      // ---- gate columns: G = log2 alpha from a, beta from b (no conv).  G
+      // and beta are head-major ([H_v][T]), so a lane's 32 rows of one
+      // column are 32 scattered rows for the wave: each 32-column block is
+      // transposed through the wave's LDS area and stored 64 rows of one
+      // head at a time.  Every row of the tile from HALO on that lies
+      // before T is an output (gates do not depend on the segments).
+      lfloat* tw = (lfloat*)smem_raw + wid * 32 * GATE_PITCH;
+      const int64_t trow = row0 + wm * 64 + lane;   // the row this lane stores
+      const bool st_ok = wm * 64 + lane >= HALO && trow < T;
       static_for<JB>([&](auto jj_c) {
         constexpr int j = hd * JB + decltype(jj_c)::value;
-        const int n = ncol + 32 * j;
-        const float sc = bf16_bits_to_f32(sc_raw[j]);
-        if (n < a.C_z + a.H_v) {
-          const int hv = n - a.C_z;
-          const float al = -__expf(a.a_log[hv]) * kLog2e, db = a.dt_bias[hv];
-          float* g = a.Gbuf + (int64_t)hv * T + t0;
+        const int nb_j = n0 + 128 * wn + 32 * j;   // first column of the block (wave-uniform)
+        if (nb_j < a.N) {
+          const int n = ncol + 32 * j;
+          const float sc = bf16_bits_to_f32(sc_raw[j]);
+          const bool is_a = n < a.C_z + a.H_v;
+          const int hv = is_a ? n - a.C_z : n - a.C_z - a.H_v;
+          float al = 0.f, db = 0.f;
+          if (n < a.N && is_a) {
+            al = -__expf(a.a_log[hv]) * kLog2e;
+            db = a.dt_bias[hv];
+          }
+          lfloat* col = tw + lc * GATE_PITCH + 32 * hf;
 #pragma unroll
-          for (int u = 0; u < 32; ++u) row_store(g + u, al * softplus(XU(j, u) * sc + db), u);
-        } else if (n < a.N) {
-          const int hv = n - a.C_z - a.H_v;
-          float* bp = a.Bbuf + (int64_t)hv * T + t0;
+          for (int u = 0; u < 32; u += 4) {
+            float v[4];
 #pragma unroll
-          for (int u = 0; u < 32; ++u) row_store(bp + u, fast_sigmoid(XU(j, u) * sc), u);
+            for (int e = 0; e < 4; ++e) {
+              const float x = XU(j, u + e) * sc;
+              v[e] = is_a ? al * softplus(x + db) : fast_sigmoid(x);
+            }
+            st_f4(col + u, v[0], v[1], v[2], v[3]);
+          }
+          // LDS operations of one wave complete in order: the reads below
+          // see every lane's writes
+          const int nc = a.N - nb_j < 32 ? a.N - nb_j : 32;
+          for (int c = 0; c < nc; ++c) {
+            const int nn = nb_j + c;
+            const bool ca = nn < a.C_z + a.H_v;
+            float* dst = ca ? a.Gbuf + (int64_t)(nn - a.C_z) * T : a.Bbuf + (int64_t)(nn - a.C_z - a.H_v) * T;
+            const float v = tw[c * GATE_PITCH + lane];
+            if (st_ok) dst[trow] = v;
+          }
         }
       });
     }
