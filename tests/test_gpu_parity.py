@@ -9,7 +9,8 @@ import torch
 
 import oracle
 import workloads as W
-from gpu_harness import TOL_BF16, TOL_F32, check_pairs, layer_tensors, log, rel_frob, run, upload
+import paper_2609_33477_amd as sr
+from gpu_harness import TOL_BF16, TOL_F32, check_pairs, check_slab, layer_tensors, log, rel_frob, run, upload
 
 pytestmark = pytest.mark.gpu
 
@@ -231,3 +232,36 @@ def test_accepted_combinations(name, kw, d, w, with_q):
     check_pairs(dev, _live_pairs(wl), tol, check_tail=w > 1)
     b0 = 3
     assert torch.all(dev.layers[0].state_out[b0] == 0)
+
+
+def test_mixed_layers_share_projection_launches():
+    """The fused projections of up to four layers of a call share a launch;
+    five layers (a launch of four, then one) whose tails differ: layer 1
+    without W_q (a k | v tail), layer 3 without a tail.  Every state and
+    tail matches the oracle, and each layer's state is bit for bit the one a
+    call of that layer alone gives."""
+    shape = W.Shape(256, 2, 4, 128, 128)
+    seg = [70, 1, 200, 33]
+    wl = W.make_workload("mixed_layers", shape, seg, n_layers=5, seed=97)
+    dev = upload(wl)
+    dev.layers[1].w_q = None
+    dev.layers[1].tail_out = torch.full((wl.n_slots, shape.c_kv, shape.conv_width - 1), float("nan"),
+                                        dtype=torch.bfloat16, device="cuda")
+    dev.layers[3].tail_out = None
+    log(f"mixed layers: T={wl.t_total}, 5 layers")
+    run(dev)
+    for li in range(5):
+        for b in range(len(seg)):
+            slot = wl.slot_ids[b]
+            got_state = dev.layers[li].state_out[slot].cpu().numpy()
+            tail = dev.layers[li].tail_out
+            got_tail = tail[slot].float().cpu().numpy() if tail is not None else None
+            check_slab(wl, li, b, got_state, got_tail, TOL_BF16, with_q=(li != 1), check_tail=tail is not None)
+    ws_bytes = sr.replay_workspace_size(shape, 1, wl.t_total)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    for li in range(5):
+        alone = torch.full_like(dev.layers[li].state_out, float("nan"))
+        L = sr.LayerTensors(**{**vars(dev.layers[li]), "state_out": alone, "tail_out": None})
+        sr.replay_state(shape, [L], len(seg), wl.t_total, dev.cu_seqlens, dev.slot_ids, ws, ws_bytes)
+        torch.cuda.synchronize()
+        assert torch.equal(alone, dev.layers[li].state_out), li
