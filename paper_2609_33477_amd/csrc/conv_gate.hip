@@ -43,12 +43,19 @@ __device__ __forceinline__ float silu(float y) { return y / (1.f + expf(-y)); }
 __device__ __forceinline__ float softplus(float x) { return fmaxf(x, 0.f) + log1pf(expf(-fabsf(x))); }
 __device__ __forceinline__ float sigmoid(float x) { return 1.f / (1.f + expf(-x)); }
 
+// One block per (64-row block, head), and one more per row block for the
+// gates.  Rows run in parallel: a wave takes RPW rows of its head at a time
+// (lane = CPL channels of one row), each lane reading the w raw rows its conv
+// needs, so no row waits for the one before it; a key's sum of squares is
+// reduced over the LPH lanes of its row.
 template <typename OUT, typename CW, typename TT, int DH>
 __global__ __launch_bounds__(kConvThreads) void conv_gate_kernel(ConvGateArgs a) {
   if (a.err && *a.err) return;   // the call's table check failed: write nothing
   constexpr int CPL = DH >= 64 ? DH / 64 : 1;   // channels per lane
-  constexpr int LPH = DH / CPL;                   // lanes per head
-  constexpr int HPW = 64 / LPH;                   // heads per wave
+  constexpr int LPH = DH / CPL;                   // lanes per head row
+  constexpr int RPW = 64 / LPH;                   // rows per wave and pass
+  constexpr int WAVES = kConvThreads / 64;
+  constexpr int PASSES = kRowsPerBlock / (WAVES * RPW);
   constexpr int WMAX = 4;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
@@ -56,7 +63,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_gate_kernel(ConvGateArgs a)
   const int n_heads = a.H_k + a.H_v;
   const int C_kv = n_heads * DH;
 
-  if ((int)blockIdx.y == (int)gridDim.y - 1) {
+  if ((int)blockIdx.y == n_heads) {
     // ---- gates: thread -> (head, row), rows fastest: ln alpha and beta per row
     const int rows = (int)(r1 - r0);
     for (int idx = tid; idx < rows * a.H_v; idx += kConvThreads) {
@@ -70,53 +77,45 @@ __global__ __launch_bounds__(kConvThreads) void conv_gate_kernel(ConvGateArgs a)
     return;
   }
 
-  const int head = (blockIdx.y * (kConvThreads / 64) + wid) * HPW + lane / LPH;
-  const bool active = head < n_heads;
+  const int head = blockIdx.y;
   const bool is_k = head < a.H_k;
   const int sub = lane % LPH;
-  const int c0 = (active ? head : 0) * DH + sub * CPL;   // channel of the first value
+  const int c0 = head * DH + sub * CPL;   // channel of the lane's first value
   const int w = a.w;
-
   float taps[CPL][WMAX];
 #pragma unroll
   for (int q = 0; q < CPL; ++q)
 #pragma unroll
     for (int i = 0; i < WMAX; ++i) taps[q][i] = (i < w) ? Elem<CW>::load(a.conv_w, (int64_t)(c0 + q) * w + i) : 0.f;
-
-  // prev[j][q] = raw value at row t-1-j
-  float prev[WMAX - 1][CPL];
-#pragma unroll
-  for (int j = 0; j < WMAX - 1; ++j)
-#pragma unroll
-    for (int q = 0; q < CPL; ++q) {
-      const int64_t t = r0 - 1 - j;
-      prev[j][q] = (j < w - 1 && t >= 0) ? a.P[t * a.ldp + c0 + q] : 0.f;
-    }
-
-  int b = segment_of_row(a.cu, a.n_seg, r0);
-  int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
-  int slot = a.slot_ids ? a.slot_ids[b] : b;
-
   void* dst = is_k ? a.Kbuf : a.Vbuf;
   const int hh = is_k ? head : head - a.H_k;
 
-  for (int64_t t = r0; t < r1; ++t) {
-    while (t >= s1) {
-      ++b;
+#pragma unroll
+  for (int ps = 0; ps < PASSES; ++ps) {
+    const int64_t t = r0 + (ps * WAVES + wid) * RPW + lane / LPH;
+    const bool live = t < r1;
+    int64_t s0 = 0, s1 = 0;
+    int slot = -1;
+    if (live) {
+      const int b = segment_of_row(a.cu, a.n_seg, t);
       s0 = a.cu[b];
       s1 = a.cu[b + 1];
       slot = a.slot_ids ? a.slot_ids[b] : b;
     }
-    float raw[CPL], act[CPL];
+    // raw[d][q]: row t - d (zero before the segment's first row)
+    float raw[WMAX][CPL];
 #pragma unroll
-    for (int q = 0; q < CPL; ++q) raw[q] = a.P[t * a.ldp + c0 + q];
-    float ss = 0.f;
+    for (int d = 0; d < WMAX; ++d)
+#pragma unroll
+      for (int q = 0; q < CPL; ++q)
+        raw[d][q] = (live && d < w && t - d >= s0) ? a.P[(t - d) * a.ldp + c0 + q] : 0.f;
+    float act[CPL], ss = 0.f;
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
-      float y = taps[q][w - 1] * raw[q];
+      float y = 0.f;
 #pragma unroll
-      for (int j = 0; j < WMAX - 1; ++j)
-        if (j < w - 1 && t - 1 - j >= s0) y = fmaf(taps[q][w - 2 - j], prev[j][q], y);
+      for (int d = 0; d < WMAX; ++d)
+        if (d < w) y = fmaf(taps[q][w - 1 - d], raw[d][q], y);
       act[q] = silu(y);
       ss = fmaf(act[q], act[q], ss);
     }
@@ -127,7 +126,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_gate_kernel(ConvGateArgs a)
 #pragma unroll
       for (int q = 0; q < CPL; ++q) act[q] *= inv;
     }
-    if (active) {
+    if (live) {
       const int64_t base = ((int64_t)hh * a.T + t) * DH + sub * CPL;
 #pragma unroll
       for (int q = 0; q < CPL; ++q) Elem<OUT>::store(dst, base + q, act[q]);
@@ -135,27 +134,18 @@ __global__ __launch_bounds__(kConvThreads) void conv_gate_kernel(ConvGateArgs a)
         const int pos = (int)(t - (s1 - (w - 1)));
 #pragma unroll
         for (int q = 0; q < CPL; ++q)
-          Elem<TT>::store(a.tail, ((int64_t)slot * a.c_tail + a.tail_kv_off + c0 + q) * (w - 1) + pos, raw[q]);
+          Elem<TT>::store(a.tail, ((int64_t)slot * a.c_tail + a.tail_kv_off + c0 + q) * (w - 1) + pos, raw[0][q]);
       }
     }
-#pragma unroll
-    for (int j = WMAX - 2; j > 0; --j)
-#pragma unroll
-      for (int q = 0; q < CPL; ++q) prev[j][q] = prev[j - 1][q];
-#pragma unroll
-    for (int q = 0; q < CPL; ++q) prev[0][q] = raw[q];
   }
 }
 
 template <typename OUT, typename CW, typename TT, int DH>
 hipError_t run_conv(const ConvGateArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
-  constexpr int CPL = DH >= 64 ? DH / 64 : 1;
-  constexpr int HPW = 64 / (DH / CPL);
-  const int heads_per_block = (kConvThreads / 64) * HPW;
+  static_assert(kRowsPerBlock % ((kConvThreads / 64) * (64 / (DH / (DH >= 64 ? DH / 64 : 1)))) == 0, "row passes");
   const int n_heads = a.H_k + a.H_v;
-  dim3 grid((unsigned)((a.T + kRowsPerBlock - 1) / kRowsPerBlock),
-            (n_heads + heads_per_block - 1) / heads_per_block + 1);
+  dim3 grid((unsigned)((a.T + kRowsPerBlock - 1) / kRowsPerBlock), (unsigned)(n_heads + 1));
   hipLaunchKernelGGL((conv_gate_kernel<OUT, CW, TT, DH>), grid, dim3(kConvThreads), 0, s, a);
   return hipGetLastError();
 }
@@ -304,7 +294,7 @@ hipError_t conv_by_tail(int tail_dtype, int d, const ConvGateArgs& a, hipStream_
 
 // ------------------------------------------------------------------ tail
 constexpr int kTailThreads = 256;
-constexpr int kTailChannels = 64;
+constexpr int kTailChannels = 4;   // one channel per wave: the channels' loads run in parallel
 
 // 8 consecutive elements starting at element i, as fp32.
 template <typename T>
