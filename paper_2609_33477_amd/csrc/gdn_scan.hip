@@ -16,8 +16,10 @@
 // Only differences G_i - G_j <= 0 are exponentiated, so strong decay
 // underflows to zero instead of overflowing.
 //
-// One workgroup per unit, d/32 waves; wave w owns state columns [32w, 32w+32)
-// as d/32 MFMA accumulator tiles that stay in registers for the whole segment.
+// One workgroup per unit of max(d/32, 4) waves.  State wave w (w < d/32) owns
+// state columns [32w, 32w+32) as d/32 MFMA accumulator tiles that stay in
+// registers for the whole segment; at d < 128 the other waves take the Gram
+// tiles and W = Tw K, so the state waves' chain of products is shorter.
 // Operand precision: K and V arrive rounded once (bf16); beta and the decay
 // factors are folded into T (rounded once) and into Delta (rounded once), so no
 // value is rounded twice.  The state is fp32 throughout.  The two products
@@ -43,7 +45,8 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 template <typename OP, int D>
 struct ScanCfg {
-  static constexpr int NW = D / 32;
+  static constexpr int NSW = D / 32;                   // state waves: wave w owns columns [32w, 32w+32)
+  static constexpr int NW = NSW < 4 ? 4 : NSW;          // waves: the rest share the chunk products
   static constexpr int THREADS = 64 * NW;
   static constexpr int EB = std::is_same<OP, float>::value ? 4 : 2;
   static constexpr int PADE = 16 / EB;
@@ -171,11 +174,11 @@ __device__ __forceinline__ void store_transposed<float>(char* base, int pitch, i
 }
 
 template <typename OP, int D>
-__global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
+__global__ __launch_bounds__(64 * (D / 32 < 4 ? 4 : D / 32)) void gdn_scan_kernel(ScanArgs a) {
   if (a.err && *a.err) return;   // the call's table check failed: write nothing
   using CF = ScanCfg<OP, D>;
   using MF = Mfma<OP>;
-  constexpr int NW = CF::NW, EB = CF::EB, KP = CF::KP, CP = CF::CP;
+  constexpr int NW = CF::NW, NSW = CF::NSW, EB = CF::EB, KP = CF::KP, CP = CF::CP;
   constexpr int NT = D / 32;  // 32-row tiles along d
   __shared__ __attribute__((aligned(16))) char smem[CF::LDS];
   __shared__ int sel;
@@ -197,6 +200,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int fr = lane & 31, h2 = lane >> 5;
   const int fk = h2 * MF::HALF;
+  const bool state_wave = NSW == NW || wid < NSW;   // compile-time true when every wave holds state
 
   const int u = blockIdx.x;
   const int head = u % a.H_v;
@@ -222,12 +226,13 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
   // T's strictly upper 16x16 blocks stay zero for the whole segment.
   for (int i = tid; i < kC * kFP; i += CF::THREADS) Tm[i] = 0.f;
 
-  // State tiles: M[td] covers rows [32 td, 32 td + 32), columns [32 wid, +32).
+  // State tiles (state waves): M[td] covers rows [32 td, 32 td + 32),
+  // columns [32 wid, +32).
   f32x16 M[NT];
   const size_t state_base = ((size_t)slot * a.H_v + head) * D * D;
 #pragma unroll
   for (int td = 0; td < NT; ++td) {
-    if (st_in) {
+    if (st_in && state_wave) {
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         M[td][r] = st_in[state_base + (size_t)(32 * td + acc_row(r, lane)) * D + 32 * wid + fr];
@@ -384,23 +389,30 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
     }
     lds_barrier();
 
-    // ---- 7. U = Tu V (this wave's columns), W = Tw K (tiles q = wid mod NW)
-    f32x16 Uacc[2], Wacc[2];
+    // ---- 7. U = Tu V (state waves, their columns); W = Tw K, 2 NT tiles
+    //         over the waves past the state waves (over all of them when
+    //         every wave holds state)
+    constexpr int WW0 = NW > NSW ? NSW : 0, NWW = NW - WW0;
+    constexpr int WT = (2 * NT + NWW - 1) / NWW;    // W tiles per wave
+    f32x16 Uacc[2], Wacc[WT];
+    if (state_wave) {
 #pragma unroll
-    for (int ti = 0; ti < 2; ++ti) {
-      Uacc[ti] = zero16();
+      for (int ti = 0; ti < 2; ++ti) {
+        Uacc[ti] = zero16();
 #pragma unroll
-      for (int s = 0; s < kC / MF::K; ++s) {
-        const auto fa = frag_std<OP>(Tu, CP, 32 * ti + fr, s * MF::K + fk);
-        const auto fb = frag_std<OP>(Vt, CP, 32 * wid + fr, s * MF::K + fk);
-        MF::mma(Uacc[ti], fa, fb);
+        for (int s = 0; s < kC / MF::K; ++s) {
+          const auto fa = frag_std<OP>(Tu, CP, 32 * ti + fr, s * MF::K + fk);
+          const auto fb = frag_std<OP>(Vt, CP, 32 * wid + fr, s * MF::K + fk);
+          MF::mma(Uacc[ti], fa, fb);
+        }
       }
     }
 #pragma unroll
-    for (int n = 0; n < 2; ++n) {
-      const int q = wid + n * NW;   // 2*NT tiles, exactly 2 per wave
-      const int ti = q / NT, td = q % NT;
+    for (int n = 0; n < WT; ++n) {
+      const int q = wid - WW0 + n * NWW;
       Wacc[n] = zero16();
+      if ((WW0 > 0 && wid < WW0) || q >= 2 * NT) continue;
+      const int ti = q / NT, td = q % NT;
 #pragma unroll
       for (int s = 0; s < kC / MF::K; ++s) {
         const auto fa = frag_std<OP>(Tw, CP, 32 * ti + fr, s * MF::K + fk);
@@ -412,8 +424,9 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
 
     // ---- 8. W to R1, row-major, rounded once
 #pragma unroll
-    for (int n = 0; n < 2; ++n) {
-      const int q = wid + n * NW;
+    for (int n = 0; n < WT; ++n) {
+      const int q = wid - WW0 + n * NWW;
+      if ((WW0 > 0 && wid < WW0) || q >= 2 * NT) continue;
       const int ti = q / NT, td = q % NT;
 #pragma unroll
       for (int r = 0; r < 16; ++r) store_op<OP>(Wr, (32 * ti + acc_row(r, lane)) * KP + 32 * td + fr, Wacc[n][r]);
@@ -421,6 +434,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
     lds_barrier();
 
     // ---- 9. Delta = U - W M0 (state from registers), Delta' = e^{G_C - G} Delta
+    if (state_wave) {
     typename MF::frag dfrag[2][32 / MF::K];
 #pragma unroll
     for (int ti = 0; ti < 2; ++ti) {
@@ -454,9 +468,11 @@ __global__ __launch_bounds__(64 * (D / 32)) void gdn_scan_kernel(ScanArgs a) {
           MF::mma(M[td], fa, dfrag[ti][s]);
         }
     }
+    }
     lds_barrier();
   }
 
+  if (!state_wave) return;
   float* out = st_out + state_base;
 #pragma unroll
   for (int td = 0; td < NT; ++td)
