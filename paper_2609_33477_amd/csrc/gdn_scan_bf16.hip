@@ -20,7 +20,7 @@
 //     Tw = T diag(beta 2^G) (m-3); then W^T = K^T Tw^T, which leaves W
 //     row-major (m-2 for sub-chunk m, m-1 for m+1);
 //   d/32 state waves, wave s owning state columns [32s, 32s+32) as 2 d/16
-//     16x16 fp32 accumulator tiles for the whole segment: at step n they
+//     16x16 fp32 accumulator tiles for the whole unit: at step n they
 //     run the state lines of sub-chunk n from registers, then read the
 //     operands of sub-chunk n+1, so the reads' latency overlaps the MFMAs
 //     and the barrier.
@@ -28,6 +28,14 @@
 // wave whose phase there is Gram or A (the two lightest) and waited for one
 // step later, so the state waves issue nothing but LDS reads and MFMAs.
 // Rings (sub-chunk slots): K 4, V 3, W 2, Tu 4, gate vectors 16.
+//
+// The grid is one workgroup per CU.  A workgroup runs its units (segment,
+// layer, value head) back to back as one stream of sub-chunks: the pipeline
+// does not drain between units, so a unit of a few sub-chunks does not pay
+// the 9 steps of pipeline fill.  Each reference to sub-chunk j of the stream
+// goes through a cursor that caches its unit's rows and planes in scalar
+// registers; the state waves start a unit's state at its first sub-chunk and
+// store it after its last.
 //
 // Every product is v_mfma_f32_16x16x32_bf16.  A 32-wide reduction over
 // sub-chunk rows uses the k-slot order {4g..4g+3, 16+4g..16+4g+3} for lane
@@ -53,6 +61,7 @@ namespace sr {
 namespace {
 
 constexpr int kC = 64;       // rows staged per step
+constexpr int kScanUnits = 64;   // units one workgroup runs at most
 constexpr int kS = 32;       // sub-chunk rows
 constexpr int kAP = 36;      // fp32 pitch of a sub-chunk's A (rows read as float4)
 constexpr int kTP = 48;      // bf16 pitch of the T^T blocks (transposed reads)
@@ -179,7 +188,11 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   using CF = Cfg<D>;
   constexpr int NSW = CF::NSW, NP = CF::NP, NT = CF::NT, WP = CF::WP, NK = CF::NK, NV = CF::NV, QG = CF::QG;
   __shared__ __attribute__((aligned(16))) char smem[CF::LDS];
-  __shared__ int sel;
+  __shared__ int seg_of[kSortMax];                 // rank -> segment, longest first
+  // the block's units, in the order it runs them, and where each one's
+  // sub-chunks start in the block's stream (u_p[k] .. u_p[k+1] - 1)
+  __shared__ int u_s0[kScanUnits], u_s1[kScanUnits], u_lh[kScanUnits], u_slot[kScanUnits];
+  __shared__ int u_p[kScanUnits + 1];
 
   lchar* L = (lchar*)smem;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -191,33 +204,141 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int tr_h = li & 3;
   const int tr_t = ((li >> 2) * kTP + 4 * (li & 3) + 4 * g * kTP) * 2; // transposed reads of T^T, rows 4g + ..
 
-  // Blocks are dealt to the 8 XCDs round-robin; within each full group of
-  // 16 blocks, blocks r and r + 8 (same XCD, dispatched together) take
-  // consecutive units, i.e. value heads 2k and 2k + 1, which share a key
-  // head when H_v = 2 H_k, so its K rows are fetched into one L2.
+  // ---- the block's units.  Unit (rank, layer, value head), ranks longest
+  // first, are dealt in rounds of G (the grid): round k gives block b unit
+  // kG + pi(b) (k even) or kG + G - 1 - pi(b) (k odd), a snake, so a block
+  // with a long unit in one round takes a short one in the next.  Blocks are
+  // dealt to the 8 XCDs round-robin; pi pairs blocks r and r + 8 of each 16
+  // (same XCD, dispatched together) on consecutive units, value heads 2i and
+  // 2i + 1, which share a key head when H_v = 2 H_k, so its K rows are
+  // fetched into one L2.
   const int units = a.n_seg * a.n_layers * a.H_v;
-  int u = blockIdx.x;
-  if ((u | 15) < units) u = (u & ~15) + 2 * (u & 7) + ((u >> 3) & 1);
-  const int head = u % a.H_v;
-  const int layer = (u / a.H_v) % a.n_layers;
-  const int rank = u / (a.H_v * a.n_layers);
-  const int b = segment_of_rank(a, rank, &sel);
-  const int slot = a.slot_ids ? a.slot_ids[b] : b;
-  if (slot < 0) return;
-  const int64_t s0 = a.cu[b], s1 = a.cu[b + 1];
-  const int nsc = (int)((s1 - s0 + kS - 1) / kS);     // sub-chunks
-  const int hk = (head * a.H_k) / a.H_v;
-
-  const char* Kplane = static_cast<const char*>(a.Kbuf) + (layer * a.k_layer_stride + (int64_t)hk * a.T * D) * 2;
-  const char* Vplane = static_cast<const char*>(a.Vbuf) + (layer * a.v_layer_stride + (int64_t)head * a.T * D) * 2;
-  const float* Gp = a.Gbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
-  const float* Bp = a.Bbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
-  // Per-layer state pointers from the kernel-argument segment at a uniform
-  // offset (ScanArgs is the only argument, at offset 0).
+  const int G = gridDim.x, bid = blockIdx.x;
+  const int pi = (G & 15) == 0 ? (bid & ~15) + 2 * (bid & 7) + ((bid >> 3) & 1) : bid;
+  if (a.n_seg <= kSortMax) {
+    for (int sg = tid; sg < a.n_seg; sg += CF::THREADS) {
+      auto len = [&](int q) {
+        const int sl = a.slot_ids ? a.slot_ids[q] : q;
+        return sl < 0 ? -1 : a.cu[q + 1] - a.cu[q];
+      };
+      const int ls = len(sg);
+      int r = 0;
+      for (int s2 = 0; s2 < a.n_seg; ++s2) {
+        const int l2 = len(s2);
+        r += (l2 > ls) || (l2 == ls && s2 < sg);
+      }
+      seg_of[r] = sg;
+    }
+  }
+  __syncthreads();
+  if (tid < kScanUnits) {
+    const int k = tid;
+    const int uk = k * G + ((k & 1) ? G - 1 - pi : pi);
+    int nsc_k = 0, s0k = 0, s1k = 0, lh = 0, sl = -1;
+    if (uk < units) {
+      const int head = uk % a.H_v, layer = (uk / a.H_v) % a.n_layers, rank = uk / (a.H_v * a.n_layers);
+      const int sg = a.n_seg <= kSortMax ? seg_of[rank] : rank;
+      sl = a.slot_ids ? a.slot_ids[sg] : sg;
+      s0k = a.cu[sg];
+      s1k = a.cu[sg + 1];
+      lh = layer * a.H_v + head;
+      if (sl >= 0) nsc_k = (s1k - s0k + kS - 1) / kS;
+    }
+    u_s0[k] = s0k;
+    u_s1[k] = s1k;
+    u_lh[k] = lh;
+    u_slot[k] = sl;
+    u_p[k + 1] = nsc_k;   // prefix summed below
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    u_p[0] = 0;
+    for (int k = 0; k < kScanUnits; ++k) {
+      acc += u_p[k + 1];
+      u_p[k + 1] = acc;
+    }
+  }
+  __syncthreads();
+  // the tables are the same for every lane: their reads go to scalar registers
+  auto uni = [](int v) { return __builtin_amdgcn_readfirstlane(v); };
+  const int NSC = uni(u_p[kScanUnits]);   // sub-chunks of the block's stream
+  // a unit's state pointers (layer l of this launch) from the kernel-argument
+  // segment at a uniform offset (ScanArgs is the only argument, at offset 0)
   const char* kargs = (const char*)__builtin_amdgcn_kernarg_segment_ptr();
-  const float* st_in = *reinterpret_cast<const float* const*>(kargs + offsetof(ScanArgs, state_in) + sizeof(void*) * layer);
-  float* st_out = *reinterpret_cast<float* const*>(kargs + offsetof(ScanArgs, state_out) + sizeof(void*) * layer);
-  const size_t state_base = ((size_t)slot * a.H_v + head) * D * D;
+  auto st_in_of = [&](int layer) {
+    return *reinterpret_cast<const float* const*>(kargs + offsetof(ScanArgs, state_in) + sizeof(void*) * layer);
+  };
+  auto st_out_of = [&](int layer) {
+    return *reinterpret_cast<float* const*>(kargs + offsetof(ScanArgs, state_out) + sizeof(void*) * layer);
+  };
+  // live units without rows: their state is the initial one
+  for (int k = 0; k < kScanUnits; ++k) {
+    if (u_slot[k] < 0 || u_s1[k] != u_s0[k]) continue;
+    const int layer = u_lh[k] / a.H_v, head = u_lh[k] % a.H_v;
+    const float* si = st_in_of(layer);
+    float* so = st_out_of(layer) + ((size_t)u_slot[k] * a.H_v + head) * D * D;
+    const size_t ib = ((size_t)u_slot[k] * a.H_v + head) * D * D;
+    for (int i = tid; i < D * D; i += CF::THREADS) so[i] = si ? si[ib + i] : 0.f;
+  }
+  if (NSC == 0) return;
+
+  // Sub-chunk j of the stream: its unit (a cursor that only moves forward,
+  // with the unit's stream range, rows and planes cached in scalar
+  // registers, so the table is read only when the cursor crosses into the
+  // next unit; j past the stream stays in the last unit with sub-chunks,
+  // past its rows), first row c0, segment end s1 and the K, V, G, beta planes.
+  struct Cursor {
+    int k, beg, end;         // unit, its sub-chunks [beg, end) of the stream
+    int64_t s0, s1;          // its rows
+    const char* kp;
+    const char* vp;
+    const float* gp;
+    const float* bp;
+  };
+  auto cursor_at = [&](Cursor& c, int k) {
+    c.k = k;
+    c.beg = uni(u_p[k]);
+    c.end = uni(u_p[k + 1]);
+    c.s0 = uni(u_s0[k]);
+    c.s1 = uni(u_s1[k]);
+    const int lh = uni(u_lh[k]);
+    const int layer = lh / a.H_v, head = lh % a.H_v;
+    const int hk = (head * a.H_k) / a.H_v;
+    c.kp = static_cast<const char*>(a.Kbuf) + (layer * a.k_layer_stride + (int64_t)hk * a.T * D) * 2;
+    c.vp = static_cast<const char*>(a.Vbuf) + (layer * a.v_layer_stride + (int64_t)head * a.T * D) * 2;
+    c.gp = a.Gbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
+    c.bp = a.Bbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
+  };
+  auto cursor_new = [&]() {
+    Cursor c;
+    int k = 0;
+    while (k + 1 < kScanUnits && uni(u_p[k + 1]) == 0) ++k;   // the first unit with sub-chunks
+    cursor_at(c, k);
+    return c;
+  };
+  struct Sub {
+    const char* kp;
+    const char* vp;
+    const float* gp;
+    const float* bp;
+    int64_t c0, s1;
+  };
+  auto sub = [&](int j, Cursor& c) {
+    if (j >= c.end && c.end < NSC) {
+      int k = c.k + 1;
+      while (k + 1 < kScanUnits && uni(u_p[k + 1]) <= j && uni(u_p[k + 1]) < NSC) ++k;
+      cursor_at(c, k);
+    }
+    Sub r;
+    r.kp = c.kp;
+    r.vp = c.vp;
+    r.gp = c.gp;
+    r.bp = c.bp;
+    r.c0 = c.s0 + (int64_t)(j - c.beg) * kS;
+    r.s1 = c.s1;
+    return r;
+  };
 
   auto kbuf = [&](int m) { return L + CF::OFF_K + (m & (NK - 1)) * CF::SZ_KV; };
   auto vbuf = [&](int m) { return L + CF::OFF_V + (m % NV) * CF::SZ_KV; };
@@ -268,8 +389,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       const int cbp = (pos / 32) ^ ((r / CF::RPL) % CF::NCP);
       dma_off[i] = (uint32_t)((r * D + 16 * cbp + 8 * ((pos / 16) & 1)) * 2);
     }
-    auto stage = [&](const char* plane, int j, lchar* buf) {
-      const int64_t c0 = s0 + (int64_t)j * kS;
+    auto stage = [&](const char* plane, int64_t c0, int64_t s1, lchar* buf) {
       const char* base = plane + c0 * D * 2;
       const uint32_t lds0 = (uint32_t)(uintptr_t)buf;
       if (c0 + kS <= s1) {
@@ -289,14 +409,18 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     auto dma_owner = [](int nn) { return ((nn - (nn & 1)) >> 1) & 3; };
     int n = -9;                      // the step; every prep barrier advances it
     int dma_cur = 0, dma_prev = 0;   // blocks this wave requested in this / the previous step
+    Cursor cur_k = cursor_new(), cur_v = cur_k, cur_l = cur_k;   // of the K and V DMAs and of the Gram loads
+    int64_t pc0[2] = {0, 0}, ps1[2] = {0, 0};   // first row and segment end of the pair being loaded
     auto dma_duty = [&](int nn) {
       if (dma_owner(nn) != p) return;
-      if (nn + 4 >= 0 && nn + 4 < nsc) {
-        stage(Kplane, nn + 4, kbuf(nn + 4));
+      if (nn + 4 >= 0 && nn + 4 < NSC) {
+        const Sub sk = sub(nn + 4, cur_k);
+        stage(sk.kp, sk.c0, sk.s1, kbuf(nn + 4));
         dma_cur += CF::DMA_BLK;
       }
-      if (nn + 3 >= 0 && nn + 3 < nsc) {
-        stage(Vplane, nn + 3, vbuf(nn + 3));
+      if (nn + 3 >= 0 && nn + 3 < NSC) {
+        const Sub sv = sub(nn + 3, cur_v);
+        stage(sv.vp, sv.c0, sv.s1, vbuf(nn + 3));
         dma_cur += CF::DMA_BLK;
       }
     };
@@ -320,25 +444,30 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     // inert: their K rows are read from the segment's last row (any finite
     // values do, they only meet beta = 0), so every load is unconditional.
     auto issue_loads = [&](int m) {
+      const Sub sp[2] = {sub(m, cur_l), sub(m + 1, cur_l)};
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < 2; ++c) {
+        pc0[c] = sp[c].c0;
+        ps1[c] = sp[c].s1;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int64_t t = s0 + (int64_t)(m + c) * kS + 16 * h + li;
-          const char* rp = Kplane + ((t < s1 ? t : s1 - 1) * D + 8 * g) * 2;
+          const int64_t t = sp[c].c0 + 16 * h + li;
+          const char* rp = sp[c].kp + ((t < sp[c].s1 ? t : sp[c].s1 - 1) * D + 8 * g) * 2;
 #pragma unroll
           for (int q = 0; q < QG; ++q) kf[c][q][h] = *reinterpret_cast<const bf16x8*>(rp + 64 * q);
         }
+      }
       // raw values of the row (clamped); zeroed past the end in the Gram
       // phase, where they are first used, so nothing here waits for them
-      const int64_t t = s0 + (int64_t)(m + hc) * kS + col;
-      const int64_t tc = t < s1 ? t : s1 - 1;
-      gv = Gp[tc];
-      bv = Bp[tc];
+      const int64_t t = (hc ? sp[1].c0 : sp[0].c0) + col;
+      const int64_t sh = hc ? sp[1].s1 : sp[0].s1;
+      const int64_t tc = t < sh ? t : sh - 1;
+      gv = (hc ? sp[1].gp : sp[0].gp)[tc];
+      bv = (hc ? sp[1].bp : sp[0].bp)[tc];
     };
     // phase 1: prefix of log2 alpha inside each half, gate vectors, Gram
     auto gram = [&](int m) {
-      if (s0 + (int64_t)(m + hc) * kS + col >= s1) {
+      if ((hc ? pc0[1] : pc0[0]) + col >= (hc ? ps1[1] : ps1[0])) {
         gv = 0.f;
         bv = 0.f;
       }
@@ -505,16 +634,16 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       }
     };
 
-    // steps -9 .. nsc-1, one barrier each: pair m runs phase s at step
+    // steps -9 .. NSC-1, one barrier each: pair m runs phase s at step
     // m - 9 + s, and phase 0 also finishes the previous pair
-    while (n < 2 * p - 9 && n < nsc) {
+    while (n < 2 * p - 9 && n < NSC) {
       dma_duty(n);
       pbar(n);
     }
     int m = 2 * p;
-    if (m < nsc) issue_loads(m);
-    for (; m < nsc; m += 8) {
-      if (m >= 8) make_w(m - 7, 1);            // m - 7 < nsc: the previous pair's second sub-chunk
+    if (m < NSC) issue_loads(m);
+    for (; m < NSC; m += 8) {
+      if (m >= 8) make_w(m - 7, 1);            // m - 7 < NSC: the previous pair's second sub-chunk
       pbar(n);
       gram(m);
       dma_duty(n);                             // after the Gram fragments' loads were waited for
@@ -529,15 +658,15 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       pack(m);
       pbar(n);
       make_w(m, 0);
-      if (m + 8 < nsc) issue_loads(m + 8);     // two steps before its Gram
+      if (m + 8 < NSC) issue_loads(m + 8);     // two steps before its Gram
       pbar(n);
     }
-    if (m >= 8 && m - 7 < nsc) {                 // the last pair's second sub-chunk, at step m - 9
+    if (m >= 8 && m - 7 < NSC) {                 // the last pair's second sub-chunk, at step m - 9
       make_w(m - 7, 1);
       dma_duty(n);
       pbar(n);
     }
-    while (n < nsc) {
+    while (n < NSC) {
       dma_duty(n);
       pbar(n);
     }
@@ -616,40 +745,66 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
       }
   };
 
-  // ---- prologue: the state in registers
+  // ---- steps -9 .. NSC-1: the state lines of sub-chunk n, then the reads
+  // of sub-chunk n+1's operands (K and V arrive by the prep waves' DMAs).
+  // A unit's state starts at its first sub-chunk from zero (or its initial
+  // state) and is stored after its last one.
+  Cursor cs = cursor_new();   // unit of sub-chunk n
+  auto unit_base = [&](const Cursor& c) {
+    return ((size_t)uni(u_slot[c.k]) * a.H_v + uni(u_lh[c.k]) % a.H_v) * D * D + (size_t)(4 * g) * D + 32 * sw + li;
+  };
+  for (int n = -9; n < NSC; ++n) {
+    if (n >= 0) {
+      if (n >= cs.end) (void)sub(n, cs);
+      if (n == cs.beg) {
+        const float* si = st_in_of(uni(u_lh[cs.k]) / a.H_v);
+        const size_t base = unit_base(cs);
 #pragma unroll
-  for (int td = 0; td < NT; ++td)
+        for (int td = 0; td < NT; ++td)
 #pragma unroll
-    for (int cc = 0; cc < 2; ++cc) {
-      M[td][cc] = zero4();
-      if (st_in) {
+          for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          M[td][cc][r] = st_in[state_base + (size_t)(16 * td + 4 * g + r) * D + 32 * sw + 16 * cc + li];
+            for (int r = 0; r < 4; ++r)
+              M[td][cc][r] = si ? si[base + (size_t)(16 * td + r) * D + 16 * cc] : 0.f;
+      }
+      state_step();
+      if (n + 1 == cs.end) {
+        float* out = st_out_of(uni(u_lh[cs.k]) / a.H_v) + unit_base(cs);
+#pragma unroll
+        for (int td = 0; td < NT; ++td)
+#pragma unroll
+          for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) out[(size_t)(16 * td + r) * D + 16 * cc] = M[td][cc][r];
       }
     }
-  // ---- steps -9 .. nsc-1: the state lines of sub-chunk n, then the reads
-  // of sub-chunk n+1's operands (K and V arrive by the prep waves' DMAs)
-  for (int n = -9; n < nsc; ++n) {
-    if (n >= 0) state_step();
-    if (n + 1 >= 0 && n + 1 < nsc) load_ops(n + 1);
+    if (n + 1 >= 0 && n + 1 < NSC) load_ops(n + 1);
     lds_barrier();
   }
+}
 
-  float* out = st_out + state_base;
-#pragma unroll
-  for (int td = 0; td < NT; ++td)
-#pragma unroll
-    for (int cc = 0; cc < 2; ++cc)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) out[(size_t)(16 * td + 4 * g + r) * D + 32 * sw + 16 * cc + li] = M[td][cc][r];
+// Compute units of the current device (one workgroup fits per CU).
+int device_cus() {
+  static int cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
 }
 
 template <int D>
 hipError_t run(const ScanArgs& a, hipStream_t s) {
   const int64_t units = (int64_t)a.n_seg * a.n_layers * a.H_v;
   if (units == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_scan_bf16_kernel<D>), dim3((unsigned)units), dim3(Cfg<D>::THREADS), 0, s, a);
+  // one workgroup per CU, each running its share of the units back to back
+  // (at most kScanUnits)
+  int64_t grid = units < device_cus() ? units : device_cus();
+  if (grid * kScanUnits < units) grid = (units + kScanUnits - 1) / kScanUnits;
+  hipLaunchKernelGGL((gdn_scan_bf16_kernel<D>), dim3((unsigned)grid), dim3(Cfg<D>::THREADS), 0, s, a);
   return hipGetLastError();
 }
 
