@@ -61,7 +61,7 @@ namespace sr {
 namespace {
 
 constexpr int kC = 64;       // rows staged per step
-constexpr int kScanUnits = 64;   // units one workgroup runs at most
+constexpr int kScanUnits = 64;   // units one workgroup runs at most (one wave's lanes: the prefix is a wave scan)
 constexpr int kS = 32;       // sub-chunk rows
 constexpr int kAP = 36;      // fp32 pitch of a sub-chunk's A (rows read as float4)
 constexpr int kTP = 48;      // bf16 pitch of the T^T blocks (transposed reads)
@@ -189,6 +189,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   constexpr int NSW = CF::NSW, NP = CF::NP, NT = CF::NT, WP = CF::WP, NK = CF::NK, NV = CF::NV, QG = CF::QG;
   __shared__ __attribute__((aligned(16))) char smem[CF::LDS];
   __shared__ int seg_of[kSortMax];                 // rank -> segment, longest first
+  __shared__ int seg_len[kSortMax];                // segment lengths (-1: sentinel)
   // the block's units, in the order it runs them, and where each one's
   // sub-chunks start in the block's stream (u_p[k] .. u_p[k+1] - 1)
   __shared__ int u_s0[kScanUnits], u_s1[kScanUnits], u_lh[kScanUnits], u_slot[kScanUnits];
@@ -217,20 +218,22 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   const int pi = (G & 15) == 0 ? (bid & ~15) + 2 * (bid & 7) + ((bid >> 3) & 1) : bid;
   if (a.n_seg <= kSortMax) {
     for (int sg = tid; sg < a.n_seg; sg += CF::THREADS) {
-      auto len = [&](int q) {
-        const int sl = a.slot_ids ? a.slot_ids[q] : q;
-        return sl < 0 ? -1 : a.cu[q + 1] - a.cu[q];
-      };
-      const int ls = len(sg);
+      const int sl = a.slot_ids ? a.slot_ids[sg] : sg;
+      seg_len[sg] = sl < 0 ? -1 : a.cu[sg + 1] - a.cu[sg];
+    }
+    __syncthreads();
+    for (int sg = tid; sg < a.n_seg; sg += CF::THREADS) {
+      const int ls = seg_len[sg];
       int r = 0;
       for (int s2 = 0; s2 < a.n_seg; ++s2) {
-        const int l2 = len(s2);
+        const int l2 = seg_len[s2];
         r += (l2 > ls) || (l2 == ls && s2 < sg);
       }
       seg_of[r] = sg;
     }
   }
   __syncthreads();
+  const int n_rounds = (units + G - 1) / G;   // units this block may hold (<= kScanUnits)
   if (tid < kScanUnits) {
     const int k = tid;
     const int uk = k * G + ((k & 1) ? G - 1 - pi : pi);
@@ -251,13 +254,15 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     u_p[k + 1] = nsc_k;   // prefix summed below
   }
   __syncthreads();
-  if (tid == 0) {
-    int acc = 0;
-    u_p[0] = 0;
-    for (int k = 0; k < kScanUnits; ++k) {
-      acc += u_p[k + 1];
-      u_p[k + 1] = acc;
+  if (tid < 64) {   // inclusive prefix over the 64 entries, one per lane of wave 0
+    int v = u_p[tid + 1];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(v, off);
+      if (tid >= off) v += y;
     }
+    u_p[tid + 1] = v;
+    if (tid == 0) u_p[0] = 0;
   }
   __syncthreads();
   // the tables are the same for every lane: their reads go to scalar registers
@@ -273,7 +278,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     return *reinterpret_cast<float* const*>(kargs + offsetof(ScanArgs, state_out) + sizeof(void*) * layer);
   };
   // live units without rows: their state is the initial one
-  for (int k = 0; k < kScanUnits; ++k) {
+  for (int k = 0; k < n_rounds; ++k) {
     if (u_slot[k] < 0 || u_s1[k] != u_s0[k]) continue;
     const int layer = u_lh[k] / a.H_v, head = u_lh[k] % a.H_v;
     const float* si = st_in_of(layer);
