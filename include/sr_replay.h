@@ -249,7 +249,8 @@ typedef enum sr_kernel_kind {
   SR_KERNEL_TAIL = 2,        /* q part of the conv tail + zero fill           */
   SR_KERNEL_GDN_SCAN = 3,    /* chunked state accumulation                    */
   SR_KERNEL_PROJ_CONV = 4,   /* projection fused with conv, SiLU, key norm,
-                                gates and the k|v tail (bf16 / fp8 path)      */
+                                gates and the k|v tail (bf16 / fp8 path); one
+                                launch covers up to 4 layers of a call        */
   SR_KERNEL_ROW_INFO = 5,    /* per-row segment position and slot (bf16 path) */
   SR_KERNEL_ANCHOR_COMPACT = 6,  /* sidecar: prefill compaction (sr_sidecar.h)  */
   SR_KERNEL_ANCHOR_WRITE = 7,    /* sidecar: indexed copy into the blocks       */

@@ -46,9 +46,16 @@
 // variants decided per row for the whole wave.  The segment info and conv
 // taps the epilogue needs are loaded before the main loop.
 //
-// Blocks past the tiles compute the q part of the conv tail and the tail's
-// leading zeros (tail_q.hpp): they need nothing the tiles write, so they run
-// in the grid's last, partial round or on CUs the tiles leave idle.
+// Gate columns (no conv) leave through a per-wave LDS transpose, so their
+// head-major G and beta planes get stores of 64 consecutive rows of a head.
+//
+// One launch covers up to kProjBatch layers of a call (same T and N): the
+// grid holds the tiles of all of them, their m-tiles stacked for the walk
+// above, and each block reads its layer's arguments from the kernel
+// argument segment.  Blocks past the tiles compute the q part of the conv
+// tail and the tail's leading zeros (tail_q.hpp): they need nothing the
+// tiles write, so they run in the grid's last, partial round or on CUs the
+// tiles leave idle.
 #include "sr_device.hpp"
 #include "tail_q.hpp"
 
