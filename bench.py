@@ -78,10 +78,10 @@ def algorithmic_work(wl, with_q=True):
         "proj_conv": ("mfma", proj_layers * (2.0 * T * D * N + 2.0 * tail_rows * D * c_q)),
         # fp32 anchors: the tail's own launch
         "tail": ("hbm", c_q * D * wb + tail_rows * ((c_q + c_kv) * tb + D * es)),
-        # one launch per call: 16 bytes of segment info per row
-        "row_info": ("hbm", T * 16),
-        # one launch per call: the varlen tables in, one flag word out
-        "validate": ("hbm", (2 * len(wl.seg_lens) + 1) * 4 + 4),
+        # one launch per call: the varlen tables in, one flag word out, and on
+        # the fused path the rows' segment info (16 bytes per row) out
+        "validate": ("hbm", (2 * len(wl.seg_lens) + 1) * 4 + 4
+                     + (T * 16 if sh.anchor_dtype != "f32" and sh.d_k == sh.d_v else 0)),
         # one launch covers all layers (up to 32)
         "gdn_scan": ("hbm", min(n_layers, 32) * (T * (c_kv * es + hv * 8) + len(live) * hv * sh.d_k * sh.d_v * 4)),
         # the per-head-decay state reads the same operands and writes the same states
@@ -455,8 +455,8 @@ def group_work(gw):
         # input norm of every layer, post-mixer norm of every layer but the last
         "rmsnorm": ("hbm", T * D * ((2 + 2 + 4) + (n - 1) * (4 + 2) + (n - 1) * (4 + 2))),
         "gdn_scan": ("hbm", T * ((hk + hv) * d * 2 + hv * 8) + len(live) * hv * d * d * 4),
-        "row_info": ("hbm", T * 16),
-        "validate": ("hbm", (2 * len(gw.seg_lens) + 1) * 4 + 4),
+        # the table check, with the rows' segment info in the same launch
+        "validate": ("hbm", (2 * len(gw.seg_lens) + 1) * 4 + 4 + T * 16),
     }
 
 

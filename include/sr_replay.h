@@ -251,7 +251,9 @@ typedef enum sr_kernel_kind {
   SR_KERNEL_PROJ_CONV = 4,   /* projection fused with conv, SiLU, key norm,
                                 gates and the k|v tail (bf16 / fp8 path); one
                                 launch covers up to 4 layers of a call        */
-  SR_KERNEL_ROW_INFO = 5,    /* per-row segment position and slot (bf16 path) */
+  SR_KERNEL_ROW_INFO = 5,    /* per-row segment position and slot; runs in
+                                the table check's launch (SR_KERNEL_VALIDATE)
+                                and is never launched on its own            */
   SR_KERNEL_ANCHOR_COMPACT = 6,  /* sidecar: prefill compaction (sr_sidecar.h)  */
   SR_KERNEL_ANCHOR_WRITE = 7,    /* sidecar: indexed copy into the blocks       */
   SR_KERNEL_ANCHOR_SEQLENS = 8,  /* sidecar: segment offsets of a gather        */

@@ -738,30 +738,7 @@ hipError_t by_head(int d, const ProjConvBatch& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-// One block per segment: position in the segment, rows left, slot.
-__global__ void row_info_kernel(const int32_t* cu, const int32_t* slot_ids, RowInfo* info, const int32_t* err) {
-  if (err && *err) return;   // the call's table check failed: write nothing
-  const int b = blockIdx.x;
-  const int32_t s0 = cu[b], s1 = cu[b + 1];
-  const int32_t slot = slot_ids ? slot_ids[b] : b;
-  for (int32_t t = s0 + (int32_t)threadIdx.x; t < s1; t += (int32_t)blockDim.x) {
-    RowInfo v;
-    v.pos = t - s0;
-    v.rem = s1 - t;
-    v.slot = slot;
-    v.seg = b;
-    info[t] = v;
-  }
-}
-
 }  // namespace
-
-hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, RowInfo* info,
-                           const int32_t* err, hipStream_t s) {
-  if (n_seg == 0) return hipSuccess;
-  hipLaunchKernelGGL(row_info_kernel, dim3(n_seg), dim3(256), 0, s, cu, slot_ids, info, err);
-  return hipGetLastError();
-}
 
 hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvBatch& b, hipStream_t s) {
   if (b.n_layers < 1 || b.n_layers > kProjBatch) return hipErrorInvalidValue;

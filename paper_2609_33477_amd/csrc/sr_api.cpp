@@ -1,20 +1,21 @@
 // C ABI of the replay library: argument validation, workspace plan and the
 // launch sequence per call.
 //
-// Every call first runs validate (one workgroup) on the device tables; every
-// later kernel exits without writing if that check failed.
-// bf16 / fp8 path (stream-ordered):
-//   row_info       once per call: position in segment, rows left, slot per row
-//   per layer:
-//     proj_conv    anchors x [W_k; W_v; W_a; W_b]^T fused with conv, SiLU, key
-//                  norm and gates -> k_hat, v (bf16, head-major), log2 alpha,
-//                  beta, and the k | v part of the conv tail
-//     tail         q part of the conv tail (+ zeros before a segment's start)
-// fp32 path, per layer:
+// Every call first checks the device tables (one workgroup); every later
+// kernel exits without writing if that check failed.
+// bf16 / fp8 path, d_k = d_v (stream-ordered):
+//   check          once per call, in the same launch the rows' position in
+//                  their segment, rows left and slot (one block per segment)
+//   proj_conv      per launch up to 4 layers: anchors x [W_k; W_v; W_a;
+//                  W_b]^T fused with conv, SiLU, key norm and gates -> k_hat,
+//                  v (bf16, head-major), log2 alpha, beta, the k | v part of
+//                  the conv tail; blocks past the tiles compute its q part
+// fp32 path, and bf16 heads with d_k != d_v, per layer:
 //     proj_gemm    anchors x [W_k; W_v; W_a; W_b]^T -> P (fp32 workspace)
-//     conv_gate    P -> k_hat, v, ln alpha, beta, k | v tail
-//     tail
-// then one chunked-scan launch per group of <= 32 layers writes the states.
+//     conv_gate    P -> k_hat, v, log alpha, beta, k | v tail
+//     tail         q part of the conv tail (+ zeros before a segment's start)
+// then one state launch per group of <= 32 layers writes the states (the
+// pipelined bf16 scan, the fp32 scan, or the chunked kernel for d_k != d_v).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -229,17 +230,17 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
   float* Bb = reinterpret_cast<float*>(ws + plan.off_b);
 
   int32_t* flag = reinterpret_cast<int32_t*>(ws + plan.off_flag);
-  if (timed(SR_KERNEL_VALIDATE, s, [&] {
-        return sr::launch_validate(cu_seqlens, slot_ids, n_segments, t_total, n_slots, flag, varlen_status, s);
-      }) != hipSuccess)
-    return SR_ERR_HIP;
-
   const bool fused = plan.fused;
   sr::RowInfo* info = reinterpret_cast<sr::RowInfo*>(ws + plan.off_info);
-  if (fused && t_total > 0) {
-    if (timed(SR_KERNEL_ROW_INFO, s, [&] { return sr::launch_row_info(cu_seqlens, slot_ids, n_segments, info, flag, s); }) != hipSuccess)
-      return SR_ERR_HIP;
-  }
+  // the table check, with the rows' segment info in the same launch when the
+  // fused projection needs it
+  if (timed(SR_KERNEL_VALIDATE, s, [&] {
+        return fused && t_total > 0
+                   ? sr::launch_validate_rows(cu_seqlens, slot_ids, n_segments, t_total, n_slots, flag,
+                                              varlen_status, info, s)
+                   : sr::launch_validate(cu_seqlens, slot_ids, n_segments, t_total, n_slots, flag, varlen_status, s);
+      }) != hipSuccess)
+    return SR_ERR_HIP;
 
   // fused projections are launched kProjBatch layers at a time
   sr::ProjConvBatch pb{};

@@ -2,7 +2,7 @@
 // workspace plan and the launch sequence.
 //
 // Per call (stream-ordered):
-//   validate, row_info                  once
+//   validate (with the row info)        once
 //   rmsnorm(anchors) -> x (bf16), h (fp32 residual stream)
 //   per layer j < n - 1:
 //     proj_conv   x -> q, k, v, z (bf16, head-major), log2 alpha, beta, conv tail
@@ -140,8 +140,12 @@ sr_status sr_replay_group(const sr_shape* shape, int32_t d_ff, float norm_eps, i
   void* Mh = ws + plan.off_m;
   auto fail = [&](hipError_t e) { return e == hipSuccess ? SR_OK : SR_ERR_HIP; };
 
+  // the table check, with the rows' segment info for the fused projection
+  // in the same launch when there are rows
   if (fail(sr::timed_call(SR_KERNEL_VALIDATE, s, [&] {
-        return sr::launch_validate(cu_seqlens, slot_ids, n_segments, t_total, n_slots, flag, varlen_status, s);
+        return T > 0 ? sr::launch_validate_rows(cu_seqlens, slot_ids, n_segments, t_total, n_slots, flag,
+                                                varlen_status, info, s)
+                     : sr::launch_validate(cu_seqlens, slot_ids, n_segments, t_total, n_slots, flag, varlen_status, s);
       })) != SR_OK)
     return SR_ERR_HIP;
   if (T == 0) {
@@ -159,10 +163,6 @@ sr_status sr_replay_group(const sr_shape* shape, int32_t d_ff, float norm_eps, i
     }
     return SR_OK;
   }
-  if (fail(sr::timed_call(SR_KERNEL_ROW_INFO, s, [&] {
-        return sr::launch_row_info(cu_seqlens, slot_ids, n_segments, info, flag, s);
-      })) != SR_OK)
-    return SR_ERR_HIP;
 
   auto rmsnorm = [&](const void* x, bool in_bf16, const void* wgt, void* out, float* copy) {
     sr::RmsNormArgs r{};

@@ -106,8 +106,6 @@ struct ProjConvBatch {
   int32_t tq_off[kProjBatch + 1];   // layer i's q-tail blocks: [tq_off[i], tq_off[i+1]) after the tiles
 };
 
-hipError_t launch_row_info(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, RowInfo* info,
-                           const int32_t* err, hipStream_t s);
 hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvBatch& b, hipStream_t s);
 hipError_t launch_proj_conv(int weight_dtype, int d_head, const ProjConvArgs& a, hipStream_t s);
 
@@ -236,6 +234,9 @@ hipError_t launch_chunk_state(int d_k, int d_v, const ScanArgs& a, hipStream_t s
 // *status (either may be null).
 hipError_t launch_validate(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, int64_t T, int32_t n_slots,
                            int32_t* flag, int32_t* status, hipStream_t s);
+// the check and the rows' segment info for the fused projection, one launch
+hipError_t launch_validate_rows(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, int64_t T,
+                                int32_t n_slots, int32_t* flag, int32_t* status, RowInfo* info, hipStream_t s);
 
 // ----------------------------------------------------------- launch timing
 // Runs launch(ctx) on stream s under the library's per-kind timing and

@@ -31,10 +31,9 @@ __host__ __device__ inline int32_t segment_mask(int32_t b, int32_t B, int32_t c0
   return m;
 }
 
-__global__ __launch_bounds__(kThreads) void validate_varlen_kernel(const int32_t* __restrict__ cu,
-                                                                  const int32_t* __restrict__ slot_ids, int32_t B,
-                                                                  int64_t T, int32_t n_slots, int32_t* flag,
-                                                                  int32_t* status) {
+// The check itself, by one workgroup of kThreads.
+__device__ __forceinline__ void check_tables(const int32_t* __restrict__ cu, const int32_t* __restrict__ slot_ids,
+                                             int32_t B, int64_t T, int32_t n_slots, int32_t* flag, int32_t* status) {
   __shared__ uint32_t seen[kWords];
   __shared__ int32_t bad;
   const int words = (n_slots + 31) >> 5;
@@ -56,6 +55,46 @@ __global__ __launch_bounds__(kThreads) void validate_varlen_kernel(const int32_t
     if (flag) *flag = bad;
     if (status) *status = bad;
   }
+}
+
+__global__ __launch_bounds__(kThreads) void validate_varlen_kernel(const int32_t* __restrict__ cu,
+                                                                  const int32_t* __restrict__ slot_ids, int32_t B,
+                                                                  int64_t T, int32_t n_slots, int32_t* flag,
+                                                                  int32_t* status) {
+  check_tables(cu, slot_ids, B, T, n_slots, flag, status);
+}
+
+// The check (block B) in one launch with the per-row segment info the fused
+// projection reads (block b < B: segment b's rows).  The info is scratch in
+// the call's workspace: it is written whatever the check finds, its rows
+// clamped to [0, T), and nothing that reads it runs unless the check passed.
+__global__ __launch_bounds__(kThreads) void validate_rows_kernel(const int32_t* __restrict__ cu,
+                                                                 const int32_t* __restrict__ slot_ids, int32_t B,
+                                                                 int64_t T, int32_t n_slots, int32_t* flag,
+                                                                 int32_t* status, RowInfo* __restrict__ info) {
+  if ((int)blockIdx.x == B) {
+    check_tables(cu, slot_ids, B, T, n_slots, flag, status);
+    return;
+  }
+  const int b = blockIdx.x;
+  const int32_t s0 = cu[b], s1 = cu[b + 1];
+  const int32_t slot = slot_ids ? slot_ids[b] : b;
+  const int64_t lo = s0 < 0 ? 0 : s0, hi = (int64_t)s1 < T ? s1 : T;
+  for (int64_t t = lo + threadIdx.x; t < hi; t += kThreads) {
+    RowInfo v;
+    v.pos = (int32_t)(t - s0);
+    v.rem = (int32_t)(s1 - t);
+    v.slot = slot;
+    v.seg = b;
+    info[t] = v;
+  }
+}
+
+hipError_t launch_validate_rows(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, int64_t T,
+                                int32_t n_slots, int32_t* flag, int32_t* status, RowInfo* info, hipStream_t s) {
+  hipLaunchKernelGGL(validate_rows_kernel, dim3(n_seg + 1), dim3(kThreads), 0, s, cu, slot_ids, n_seg, T, n_slots,
+                     flag, status, info);
+  return hipGetLastError();
 }
 
 hipError_t launch_validate(const int32_t* cu, const int32_t* slot_ids, int32_t n_seg, int64_t T, int32_t n_slots,
