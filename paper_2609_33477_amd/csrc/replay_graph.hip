@@ -10,15 +10,13 @@
 // (several objects replayed in order on one stream can share one).
 //
 // Every bucket of B rows is captured at creation, so the hit path never
-// captures.  A bucket's graph
-//   1. pads the live table (n segments, t_total rows) to max_segments + 1
-//      segments covering exactly B rows: live segments as given, then one
-//      sentinel segment (slot -1) over rows t_total .. B - 1, then empty
-//      sentinels;
-//   2. runs sr_replay_state over B rows and max_segments + 1 segments.
-// A run writes the caller's table pointers and live segment count into a
-// device parameter block (one one-thread kernel) and launches the smallest
-// bucket holding t_total.  A batch no bucket holds (too many rows or
+// captures.  A bucket's graph runs sr_replay_state over B rows and
+// max_segments + 1 segments of the object's padded table.  A run picks the
+// smallest bucket holding t_total, pads the caller's live table (n segments,
+// t_total rows) into the object's table with one small kernel on the stream
+// -- live segments as given, then one sentinel segment (slot -1) over rows
+// t_total .. B - 1, then empty sentinels -- and launches that bucket's
+// graph.  A batch no bucket holds (too many rows or
 // segments) runs eagerly: on the object's buffers and workspace when they are
 // large enough, otherwise on anchors and a workspace the caller passes.
 // Padding rows are projected like any other row (their anchors are whatever
@@ -45,30 +43,16 @@ namespace {
 
 constexpr int kPadThreads = 256;
 
-// The batch a graph launch replays: the caller's table and its live segment
-// count, written by a one-thread kernel before each launch.
-struct PadParams {
-  const int32_t* cu;     // [n + 1], cu[n] = live rows
-  const int32_t* slot;   // [n] or null (identity)
-  int32_t n;
-};
-
-__global__ void set_params_kernel(PadParams* p, const int32_t* cu, const int32_t* slot, int32_t n) {
-  p->cu = cu;
-  p->slot = slot;
-  p->n = n;
-}
-
-// Pads the live table to max_seg + 1 segments over `rows` rows: live
-// segments as given, then the sentinel over the rest of the rows, then empty
-// sentinels.
-__global__ __launch_bounds__(kPadThreads) void pad_table_kernel(const PadParams* __restrict__ p,
+// Pads the caller's live table (cu [n + 1], slot [n] or null for identity)
+// to max_seg + 1 segments over `rows` rows: live segments as given, then the
+// sentinel over the rest of the rows, then empty sentinels.  It runs on the
+// stream just before the bucket's graph, which reads the padded table from
+// the object's own buffers.
+__global__ __launch_bounds__(kPadThreads) void pad_table_kernel(const int32_t* __restrict__ cu,
+                                                               const int32_t* __restrict__ slot, int32_t n,
                                                                int32_t* __restrict__ cu_pad,
                                                                int32_t* __restrict__ slot_pad, int32_t max_seg,
                                                                int32_t rows) {
-  const int n = p->n;
-  const int32_t* cu = p->cu;
-  const int32_t* slot = p->slot;
   for (int s = threadIdx.x; s <= max_seg + 1; s += kPadThreads) {
     cu_pad[s] = s == 0 ? 0 : (s <= n ? cu[s] : rows);
     if (s <= max_seg) slot_pad[s] = s < n ? (slot ? slot[s] : s) : -1;
@@ -85,7 +69,6 @@ struct sr_replay_graph {
   size_t row_bytes = 0;
   std::vector<sr_layer> layers;          // anchors replaced by the owned buffers
   std::vector<void*> anchor_buf;
-  PadParams* params = nullptr;
   int32_t* cu_pad = nullptr;             // [max_seg + 2]
   int32_t* slot_pad = nullptr;           // [max_seg + 1]
   void* ws = nullptr;                    // shared by every bucket
@@ -115,7 +98,7 @@ void release(sr_replay_graph* g) {
     if (b.exec) (void)hipGraphExecDestroy(b.exec);
   for (void* p : g->anchor_buf)
     if (p) (void)hipFree(p);
-  for (void* p : {(void*)g->params, (void*)g->cu_pad, (void*)g->slot_pad})
+  for (void* p : {(void*)g->cu_pad, (void*)g->slot_pad})
     if (p) (void)hipFree(p);
   if (g->own_ws && g->ws) (void)hipFree(g->ws);
   if (g->ready) (void)hipEventDestroy(g->ready);
@@ -126,21 +109,13 @@ void release(sr_replay_graph* g) {
 
 int elem_bytes(int dt) { return dt == SR_F32 ? 4 : (dt == SR_BF16 ? 2 : 1); }
 
-// Captures bucket b: the padding kernel and the replay over b.rows rows.
+// Captures bucket b: the replay over b.rows rows of the padded table.
 sr_status capture(sr_replay_graph* g, sr_replay_graph::Bucket& b) {
   hipStream_t s = g->capture_stream;
   hipError_t e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
   if (e != hipSuccess) return hip_fail(e);
-  (void)hipGetLastError();
-  hipLaunchKernelGGL(pad_table_kernel, dim3(1), dim3(kPadThreads), 0, s, g->params, g->cu_pad, g->slot_pad,
-                     g->max_seg, (int32_t)b.rows);
-  const hipError_t le = hipGetLastError();
-  const sr_status st = le == hipSuccess
-                           ? sr_replay_state(&g->shape, g->n_layers, g->layers.data(), g->max_seg + 1, b.rows,
-                                             g->cu_pad, g->slot_pad, g->n_slots, g->varlen_status, g->ws,
-                                             g->ws_bytes, s)
-                           : SR_ERR_HIP;
-  if (le != hipSuccess) sr::note_error(SR_KERNEL_GRAPH, le);
+  const sr_status st = sr_replay_state(&g->shape, g->n_layers, g->layers.data(), g->max_seg + 1, b.rows, g->cu_pad,
+                                       g->slot_pad, g->n_slots, g->varlen_status, g->ws, g->ws_bytes, s);
   hipGraph_t graph = nullptr;
   const hipError_t ee = hipStreamEndCapture(s, &graph);
   if (st != SR_OK || ee != hipSuccess || !graph) {
@@ -194,7 +169,6 @@ sr_status sr_replay_graph_create(const sr_shape* shape, int32_t n_layers, const 
     if (e == hipSuccess) e = hipMemset(g->anchor_buf[l], 0, (size_t)g->t_max * g->row_bytes);
     g->layers[l].anchors = g->anchor_buf[l];
   }
-  if (e == hipSuccess) e = hipMalloc((void**)&g->params, sizeof(PadParams));
   if (e == hipSuccess) e = hipMalloc((void**)&g->cu_pad, (max_segments + 2) * sizeof(int32_t));
   if (e == hipSuccess) e = hipMalloc((void**)&g->slot_pad, (max_segments + 1) * sizeof(int32_t));
   if (e == hipSuccess) {
@@ -223,6 +197,9 @@ sr_status sr_replay_graph_create(const sr_shape* shape, int32_t n_layers, const 
       return st;
     }
   }
+  // the capture stream is not used again: give its hardware queue back
+  (void)hipStreamDestroy(g->capture_stream);
+  g->capture_stream = nullptr;
   *out = g;
   return SR_OK;
 }
@@ -298,7 +275,8 @@ sr_status sr_replay_graph_run(sr_replay_graph* g, int32_t n_segments, int64_t t_
     size_t bi = 0;
     while (g->buckets[bi].rows < t_total) ++bi;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(set_params_kernel, dim3(1), dim3(1), 0, s, g->params, cu_seqlens, slot_ids, n_segments);
+    hipLaunchKernelGGL(pad_table_kernel, dim3(1), dim3(kPadThreads), 0, s, cu_seqlens, slot_ids, n_segments, g->cu_pad,
+                       g->slot_pad, g->max_seg, (int32_t)g->buckets[bi].rows);
     e = hipGetLastError();
     if (e == hipSuccess) e = hipGraphLaunch(g->buckets[bi].exec, s);
     if (e != hipSuccess) return hip_fail(e);
