@@ -46,6 +46,30 @@ def log(msg):
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
+WARMUP_MIN_S = 0.15   # wall time of untimed steps before any timing
+
+
+def warm_up(step, n):
+    """Runs at least n untimed steps, and keeps going (8 at a time, waiting
+    for each group) until WARMUP_MIN_S has passed.  From idle the shader
+    clock takes ~50-100 ms of this load to settle: timed right after 5
+    warmup steps, varlen16 ran 1.43 ms per step, against 1.35-1.37 ms after
+    50.  Returns the number of steps run (reported as warmup_run)."""
+    import torch
+    t0 = time.perf_counter()
+    done = 0
+    while done < n:
+        step()
+        done += 1
+    torch.cuda.synchronize()
+    while time.perf_counter() - t0 < WARMUP_MIN_S:
+        for _ in range(8):
+            step()
+        done += 8
+        torch.cuda.synchronize()
+    return done
+
+
 PROJ_LAYERS_PER_LAUNCH = 4   # layers of one call that share a fused-projection launch
 
 
@@ -282,9 +306,7 @@ def bench_sidecar(args):
     else:
         raise SystemExit(f"unknown sidecar workload {args.workload}")
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_run = warm_up(step, args.warmup)
     sr.kernel_timing_enable(True)
     sr.kernel_timing_read()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -314,7 +336,7 @@ def bench_sidecar(args):
     log(f"{ms_per_step:.4f} ms/step, {value / 1e6:.2f} M rows/s; {dom} {dk['achieved']:.0f} GB/s")
     cpu = None if args.no_cpu_baseline else cpu_leg(min(args.cpu_budget_s, 15.0))
     out = {"metric": f"anchor rows x layers/sec ({args.workload.replace('_', ' ')})", "value": round(value, 1),
-           "unit": "rows/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "unit": "rows/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "warmup_run": warm_run,
            "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "bf16", "data": "synthetic", "config": config, "latency_ms": round(ms_per_step, 5),
            "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu}
@@ -325,7 +347,7 @@ GRAPH_SEGMENTS = [128] * 8          # a small batch of hits: 8 requests x 128 re
 GRAPH_LAYERS = 24                   # every linear-attention layer of Qwen3.5-4B (Appendix A)
 GRAPH_GROUPS = 8                    # its 8 groups of 3 linear layers (G = 8 full-attention layers)
 GRAPH_BUCKETS = [256, 1024, 4096]   # total-length buckets, up to the paper's T_max = 4096
-GRAPH_MIN_WARMUP = 100              # untimed batches per mode before timing
+GRAPH_MIN_WARMUP = 100              # untimed batches per mode before timing (at least)
 
 
 def bench_graph(args):
@@ -374,14 +396,14 @@ def bench_graph(args):
             g.fetch(r, copy_stream)
             g.run(n, wl.t_total, dev.cu_seqlens, dev.slot_ids, stream)
 
+    warm_runs = []
+
     def timed(fn):
         # The first ~60 pipelined batches of a process run ~25% slower: the
         # runtime blocks the host inside the copy submissions until it has
         # warmed up, and the copy stream idles between copies.  Warm every
         # mode past that point.
-        for _ in range(max(args.warmup, GRAPH_MIN_WARMUP)):
-            fn()
-        torch.cuda.synchronize()
+        warm_runs.append(warm_up(fn, max(args.warmup, GRAPH_MIN_WARMUP)))
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
         a.record(stream)
@@ -414,7 +436,7 @@ def bench_graph(args):
         f"({fetched / ms_fetch / 1e6:.1f} GB/s), replay {ms_replay:.4f} ms, sum {ms_fetch + ms_replay:.4f} ms, "
         f"eager replay {ms_eager:.4f} ms")
     out = {"metric": METRIC + " (graph-bucketed small batch, anchors fetched from host)", "value": round(value, 1),
-           "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "warmup_run": warm_runs[0],
            "ms_per_step": round(ms_pipe, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "bf16", "data": "synthetic",
            "config": {"workload": "graph_small", "requests": n, "anchors_per_request": GRAPH_SEGMENTS[0],
@@ -488,9 +510,7 @@ def bench_group(args):
                         dg.slot_ids, ws, ws_bytes, stream)
 
     log(f"group: T={gw.t_total} rows x {len(blocks)} layers, d_ff {gw.d_ff}, workspace {ws_bytes / 2**20:.1f} MiB")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_run = warm_up(step, args.warmup)
     sr.kernel_timing_enable(True)
     sr.kernel_timing_read()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -539,7 +559,8 @@ def bench_group(args):
                "cores": int(os.cpu_count() or 1),
                "sample": f"{rows} anchor rows of {n_seg} segments through {len(blocks)} layers, fp64, {el:.1f} s"}
     out = {"metric": METRIC + " (group replay chaining)", "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
-           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "steps": args.steps, "warmup": args.warmup, "warmup_run": warm_run, "ms_per_step": round(ms, 4),
+           "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
            "config": {"workload": gw.name, "requests": n_seg, "anchors_per_request": GROUP_SEGMENTS[0],
                       "layers": len(blocks), "t_total": gw.t_total, "d_model": shape.d_model,
@@ -555,8 +576,8 @@ def bench_group(args):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    # the clock needs ~50 steps (~80 ms of this load) to settle; the default
-    # warmup covers that so the timed steps measure the steady state
+    # the clock needs ~50 steps (~80 ms of this load) to settle: warm_up
+    # runs at least --warmup steps and at least WARMUP_MIN_S of them
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="varlen16")
@@ -602,9 +623,8 @@ def main():
         sr.replay_state(wl.shape, layers, n_seg, wl.t_total, dev.cu_seqlens, dev.slot_ids, ws, ws_bytes, stream)
 
     log(f"T={wl.t_total} rows x {len(wl.layers)} layers, workspace {ws_bytes / 2**20:.1f} MiB; warmup {args.warmup}")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_run = warm_up(step, args.warmup)
+    log(f"{warm_run} warmup steps run")
 
     sr.kernel_timing_enable(True)
     sr.kernel_timing_read()                       # drop anything recorded before
@@ -655,7 +675,8 @@ def main():
     sh = wl.shape
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "warmup": args.warmup, "warmup_run": warm_run, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32" if sh.anchor_dtype == "f32" else "bf16",
         "data": "synthetic",
         "config": {"workload": wl.name, "requests": n_seg, "layers": len(wl.layers), "t_total": wl.t_total,
