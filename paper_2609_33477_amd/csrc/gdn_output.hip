@@ -167,6 +167,7 @@ __global__ __launch_bounds__(64 * (DV / 32)) void gdn_chunk_kernel(A a) {
   const int hk = (head * a.H_k) / a.H_v;
   const uint16_t* Kp;
   const uint16_t* Vp;
+  int kpitch = DK;                                      // elements per K row
   const uint16_t* Qp = nullptr;
   const uint16_t* Zp = nullptr;
   const float* Gp;
@@ -182,7 +183,8 @@ __global__ __launch_bounds__(64 * (DV / 32)) void gdn_chunk_kernel(A a) {
     Bp = a.Bbuf + (int64_t)head * a.T;
     st_out = a.state_out;
   } else {
-    Kp = static_cast<const uint16_t*>(a.Kbuf) + layer * a.k_layer_stride + (int64_t)hk * a.T * DK;
+    if (a.k_pitch > 0) kpitch = a.k_pitch;
+    Kp = static_cast<const uint16_t*>(a.Kbuf) + layer * a.k_layer_stride + (int64_t)hk * a.T * kpitch;
     Vp = static_cast<const uint16_t*>(a.Vbuf) + layer * a.v_layer_stride + (int64_t)head * a.T * DV;
     Gp = a.Gbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
     Bp = a.Bbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
@@ -249,9 +251,8 @@ __global__ __launch_bounds__(64 * (DV / 32)) void gdn_chunk_kernel(A a) {
       const int row = p / (DK / 8), cc = p % (DK / 8);
       uint4 kv = make_uint4(0, 0, 0, 0), qv = kv;
       if (row < n) {
-        const int64_t off = (c0 + row) * DK + cc * 8;
-        kv = *reinterpret_cast<const uint4*>(Kp + off);
-        if constexpr (OUT) qv = *reinterpret_cast<const uint4*>(Qp + off);
+        kv = *reinterpret_cast<const uint4*>(Kp + (c0 + row) * kpitch + cc * 8);
+        if constexpr (OUT) qv = *reinterpret_cast<const uint4*>(Qp + (c0 + row) * DK + cc * 8);
       }
       const int lo = (row * KP + cc * 8) * 2;
       *reinterpret_cast<uint4*>(smem + CF::OFF_K + lo) = kv;

@@ -33,6 +33,15 @@
 // narrow last N-tile (the 2 H_v gate columns) waves skip the MFMAs and
 // fragment reads of columns past N.
 //
+// Rectangular heads (RECT: OLMo-Hybrid's 96-wide keys and 192-wide values,
+// Appendix A): each key head takes 128 output columns, its last 32 computed
+// from a repeated weight row and zeroed before the conv, so the per-wave key
+// norm is unchanged; keys stay in that padded layout, values are stored in
+// 192-wide heads, and every channel index into the caller's weights,
+// scales, conv taps and tail goes through real_col.  The pad costs a tenth
+// more MFMA work at OLMo's shape, against an unfused projection whose fp32
+// rows went through HBM.
+//
 // Conv epilogue, in registers: M-tiles overlap by 3 rows (stride 253), so
 // every output row's w-1 predecessors are in the tile.  Lane l of wave w
 // holds rows 64 (w / 2) + 32 (l / 32) + 0..31 of 4 columns; the conv runs
@@ -189,6 +198,19 @@ __device__ __forceinline__ const uint16_t* col_scale_ptr(const ProjConvArgs& a, 
     if (s < a.n_wseg && n >= a.seg[s].n0 && n < a.seg[s].n1) p = static_cast<const uint16_t*>(a.seg[s].scale) + (n - a.seg[s].n0);
   return p;
 }
+// Output column n -> the caller's channel order (weight rows, fp8 scales,
+// conv taps, tail channels).  Square heads: n itself.  RECT: key head h's
+// output columns h D + j map to channel h k_real + j (the pad columns
+// j >= k_real to the head's last channel: their products are discarded),
+// and the value and gate columns shift down by the keys' padding.
+template <bool RECT, int D>
+__device__ __forceinline__ int real_col(const ProjConvArgs& a, int n) {
+  if constexpr (!RECT) return n;
+  const int pad = (a.C_k / D) * (D - a.k_real);
+  if (n >= a.C_k) return n - pad;
+  const int h = n / D, j = n - h * D;
+  return h * a.k_real + (j < a.k_real ? j : a.k_real - 1);
+}
 // per-output-column scale of fp8 weights (1 for bf16 weights)
 template <typename TB>
 __device__ __forceinline__ float col_scale(const ProjConvArgs& a, int n) {
@@ -210,7 +232,7 @@ __device__ __forceinline__ void store_elem(void* p, int64_t i, float v, bool is_
   else static_cast<float*>(p)[i] = v;
 }
 
-template <typename TB, int D>
+template <typename TB, int D, bool RECT>
 __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb, int tiles_m, int tiles_n) {
   // The batch is the kernel's first argument: a layer's arguments are read
   // from the argument segment at a block-uniform offset.
@@ -276,14 +298,15 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
   uint32_t tr[4][4], sc_raw[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int n = ncol + 32 * j;
+    const int n_out = ncol + 32 * j;
+    const int n = real_col<RECT, D>(a, n_out);
     sc_raw[j] = 0x3f80u;   // bf16 bits of 1
 #pragma unroll
     for (int d = 0; d < 4; ++d) tr[j][d] = 0u;
-    if (n < a.N) {
+    if (n_out < a.N) {
       if constexpr (std::is_same<TB, fp8_t>::value) sc_raw[j] = *col_scale_ptr(a, n);
     }
-    if (n < a.C_kv) {
+    if (n_out < a.C_kv) {
       if (tap_mode == 1) {
         const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.conv_w) + (int64_t)n * 4);
         tr[j][0] = v.x;
@@ -329,7 +352,7 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
       row = wid * 32 + (lane >> 1);
       coff = (lane & 1) * 16;
     }
-    const int n = (n0 + row < a.N) ? n0 + row : a.N - 1;
+    const int n = real_col<RECT, D>(a, (n0 + row < a.N) ? n0 + row : a.N - 1);
     const char* p = static_cast<const char*>(a.seg[0].ptr);
 #pragma unroll
     for (int s = 0; s < 6; ++s)
@@ -467,6 +490,19 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
   // rows before rbase come from another lane (lane l ^ 32 of this wave for
   // hf = 1, of the wave above for hf = 0), through the LDS.
 #define XU(j, u) acc[(u) >> 4][j][(u) & 15]
+  // RECT: a key head's pad columns (its 32-column blocks from k_real on)
+  // hold products of a repeated weight row; they enter neither the conv
+  // halo, the tail, nor the key's norm
+  const bool rect_k = RECT && n0 + 128 * wn < a.C_k;
+  if constexpr (RECT) {
+    if (rect_k) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (32 * j >= a.k_real)
+#pragma unroll
+          for (int u = 0; u < 32; ++u) XU(j, u) = 0.f;
+    }
+  }
   lfloat* XB = (lfloat*)(smem_raw + EPI_OFF);
   lfloat* INV = (lfloat*)(smem_raw + EPI_OFF + XB_BYTES);
   {
@@ -569,12 +605,14 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
         static_for<JB>([&](auto jj_c) {
           constexpr int j = hd * JB + decltype(jj_c)::value;
           const float sc = bf16_bits_to_f32(sc_raw[j]);
+          const bool pad = rect_k && 32 * j >= a.k_real;
+          const int ch = real_col<RECT, D>(a, ncol + 32 * j);
 #pragma unroll
           for (int u = 0; u < 32; ++u) {
             if ((tailm >> u) & 1u) {
               const RowInfo r = a.info[t0 + u];
-              if (r.slot >= 0)
-                store_elem(a.tail, ((int64_t)r.slot * a.c_tail + a.tail_kv_off + ncol + 32 * j) * w1 + (w1 - r.rem),
+              if (r.slot >= 0 && !pad)
+                store_elem(a.tail, ((int64_t)r.slot * a.c_tail + a.tail_kv_off + ch) * w1 + (w1 - r.rem),
                            XU(j, u) * sc, tail_bf16);
             }
           }
@@ -626,6 +664,20 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
       // scale (1/|k| for keys), round to bf16, store two rows per pack
       const int hh = is_q ? nb / D : (is_k ? (nb - a.C_q) / D : (nb - a.C_k) / D);
       uint16_t* dst = static_cast<uint16_t*>(is_q ? a.Qbuf : (is_k ? a.Kbuf : a.Vbuf)) + ((int64_t)hh * T + t0) * D + lc;
+      // RECT values: block jj of these 128 columns lies in value head
+      // vh = c / v_head at column c % v_head, rows v_head apart
+      uint16_t* vdst[JB];
+      int vpitch = D;
+      if constexpr (RECT) {
+        if (!is_k) {
+          vpitch = a.v_head;
+#pragma unroll
+          for (int jj = 0; jj < JB; ++jj) {
+            const int c = nb - a.C_k + 32 * jj, vh = c / a.v_head;
+            vdst[jj] = static_cast<uint16_t*>(a.Vbuf) + ((int64_t)vh * T + t0) * a.v_head + (c - vh * a.v_head) + lc;
+          }
+        }
+      }
       const lfloat* ivp = INV + ((wid * 2 + hf) * NH + hd) * 32;
       // SIMPLE: every lane outputs rows 3..31, so only rows 0-2 need a
       // per-lane predicate
@@ -645,8 +697,13 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
             for (int v = 0; v < 4; v += 2) {
               const int u = 4 * q + v;
               const uint32_t p = pack_bf16x2(XU(j, u) * iv[v], XU(j, u + 1) * iv[v + 1]);
-              st(dst + (int64_t)u * D + 32 * jj, (uint16_t)(p & 0xffffu), u);
-              st(dst + (int64_t)(u + 1) * D + 32 * jj, (uint16_t)(p >> 16), u + 1);
+              if (RECT && !is_k) {
+                st(vdst[jj] + (int64_t)u * vpitch, (uint16_t)(p & 0xffffu), u);
+                st(vdst[jj] + (int64_t)(u + 1) * vpitch, (uint16_t)(p >> 16), u + 1);
+              } else {
+                st(dst + (int64_t)u * D + 32 * jj, (uint16_t)(p & 0xffffu), u);
+                st(dst + (int64_t)(u + 1) * D + 32 * jj, (uint16_t)(p >> 16), u + 1);
+              }
             }
           });
         }
@@ -717,19 +774,29 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
 #undef XU
 }
 
-template <typename TB, int D>
+template <typename TB, int D, bool RECT = false>
 hipError_t run(const ProjConvBatch& b, hipStream_t s) {
   const ProjConvArgs& a = b.layer[0];
   if (a.K % BK) return hipErrorInvalidValue;
   const int tm = (int)((a.T + SM - 1) / SM), tn = (a.N + BN - 1) / BN;
   const int blocks = b.n_layers * tm * tn + b.tq_off[b.n_layers];
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((proj_conv_kernel<TB, D>), dim3(blocks), dim3(THREADS), 0, s, b, tm, tn);
+  hipLaunchKernelGGL((proj_conv_kernel<TB, D, RECT>), dim3(blocks), dim3(THREADS), 0, s, b, tm, tn);
   return hipGetLastError();
 }
 
 template <typename TB>
 hipError_t by_head(int d, const ProjConvBatch& a, hipStream_t s) {
+  if (a.layer[0].k_real > 0) {
+    // rectangular heads: key heads padded to 128 columns, no q or z columns
+    for (int l = 0; l < a.n_layers; ++l) {
+      const ProjConvArgs& x = a.layer[l];
+      if (x.k_real != a.layer[0].k_real || x.v_head != a.layer[0].v_head || x.k_real % 32 || x.k_real > 128 ||
+          x.v_head % 32 || x.v_head <= 0 || x.C_q != 0 || x.C_z != x.C_kv || x.C_k % 128 || (x.C_kv - x.C_k) % 128)
+        return hipErrorInvalidValue;
+    }
+    return d == 128 ? run<TB, 128, true>(a, s) : hipErrorInvalidValue;
+  }
   switch (d) {
     case 32: return run<TB, 32>(a, s);
     case 64: return run<TB, 64>(a, s);

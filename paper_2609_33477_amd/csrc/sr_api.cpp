@@ -3,14 +3,17 @@
 //
 // Every call first checks the device tables (one workgroup); every later
 // kernel exits without writing if that check failed.
-// bf16 / fp8 path, d_k = d_v (stream-ordered):
+// bf16 / fp8 path, d_k = d_v, or d_k = 96, d_v = 192 with an even number of
+// value heads (stream-ordered):
 //   check          once per call, in the same launch the rows' position in
 //                  their segment, rows left and slot (one block per segment)
 //   proj_conv      per launch up to 4 layers: anchors x [W_k; W_v; W_a;
 //                  W_b]^T fused with conv, SiLU, key norm and gates -> k_hat,
 //                  v (bf16, head-major), log2 alpha, beta, the k | v part of
-//                  the conv tail; blocks past the tiles compute its q part
-// fp32 path, and bf16 heads with d_k != d_v, per layer:
+//                  the conv tail; blocks past the tiles compute its q part.
+//                  96-wide key heads take 128 output columns each (zero
+//                  pads) and land in a padded [H_k][T][128] key buffer
+// fp32 path, and 96 x 192 heads with an odd number of value heads, per layer:
 //     proj_gemm    anchors x [W_k; W_v; W_a; W_b]^T -> P (fp32 workspace)
 //     conv_gate    P -> k_hat, v, log alpha, beta, k | v tail
 //     tail         q part of the conv tail (+ zeros before a segment's start)
@@ -69,8 +72,18 @@ struct Plan {
   int64_t off_flag, off_p, off_info, off_k, off_v, off_g, off_b, total;
   int64_t k_stride, v_stride, g_stride;   // per-layer strides (elements)
   int op_dtype, op_bytes;
-  bool fused;                        // bf16 square heads: projection fused with the conv epilogue
+  bool fused;                        // bf16 anchors: projection fused with the conv epilogue
+  bool rect;                         // fused rectangular heads: keys padded to 128 columns
+  int k_pitch;                       // elements per K row
 };
+
+// Rectangular heads take the fused projection when their value columns fill
+// whole 128-column wave blocks (the epilogue treats each block as one kind
+// of column): an even number of 192-wide value heads.
+bool rect_fused(const sr_shape* s) {
+  return s->d_k == 96 && s->d_v == 192 && s->anchor_dtype == SR_BF16 &&
+         ((int64_t)s->n_v_heads * s->d_v) % 128 == 0;
+}
 
 Plan make_plan(const sr_shape* s, int32_t n_layers, int64_t T) {
   Plan p{};
@@ -79,8 +92,10 @@ Plan make_plan(const sr_shape* s, int32_t n_layers, int64_t T) {
   p.ldp = align_up(N, 4);
   p.op_dtype = s->anchor_dtype == SR_F32 ? SR_F32 : SR_BF16;
   p.op_bytes = dtype_bytes(p.op_dtype);
-  p.fused = p.op_dtype == SR_BF16 && s->d_k == s->d_v;
-  p.k_stride = hk * T * s->d_k;
+  p.rect = rect_fused(s);
+  p.fused = p.op_dtype == SR_BF16 && (s->d_k == s->d_v || p.rect);
+  p.k_pitch = p.rect ? 128 : s->d_k;
+  p.k_stride = hk * T * p.k_pitch;
   p.v_stride = hv * T * s->d_v;
   p.g_stride = hv * T;
   int64_t off = 0;
@@ -223,6 +238,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
   char* ws = static_cast<char*>(workspace);
   const int hk = shape->n_k_heads, hv = shape->n_v_heads, d = shape->d_k, w = shape->conv_width;
   const int c_k = hk * shape->d_k, c_v = hv * shape->d_v;
+  const int c_kp = plan.rect ? hk * plan.k_pitch : c_k;   // key columns of the fused projection
   float* P = reinterpret_cast<float*>(ws + plan.off_p);
   char* Kb = ws + plan.off_k;
   char* Vb = ws + plan.off_v;
@@ -246,7 +262,9 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
   sr::ProjConvBatch pb{};
   auto flush_proj = [&]() {
     if (pb.n_layers == 0) return hipSuccess;
-    const hipError_t e = timed(SR_KERNEL_PROJ_CONV, s, [&] { return sr::launch_proj_conv(shape->weight_dtype, d, pb, s); });
+    const hipError_t e = timed(SR_KERNEL_PROJ_CONV, s, [&] {
+      return sr::launch_proj_conv(shape->weight_dtype, plan.rect ? plan.k_pitch : d, pb, s);
+    });
     pb.n_layers = 0;
     return e;
   };
@@ -279,7 +297,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       f.A = L.anchors;
       f.T = t_total;
       f.K = shape->d_model;
-      f.N = c_k + c_v + 2 * hv;
+      f.N = c_kp + c_v + 2 * hv;
       f.n_wseg = 4;
       for (int i = 0; i < 4; ++i) f.seg[i] = wseg[i];
       f.info = info;
@@ -289,9 +307,11 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       f.a_log = L.a_log;
       f.dt_bias = L.dt_bias;
       f.C_q = 0;
-      f.C_k = c_k;
-      f.C_kv = c_k + c_v;
-      f.C_z = c_k + c_v;
+      f.C_k = c_kp;
+      f.C_kv = c_kp + c_v;
+      f.C_z = c_kp + c_v;
+      f.k_real = plan.rect ? shape->d_k : 0;
+      f.v_head = plan.rect ? shape->d_v : 0;
       f.q_scale = 1.f;
       f.H_v = hv;
       f.eps = shape->l2_eps;
@@ -377,6 +397,7 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
     a.H_v = hv;
     a.n_layers = nl;
     a.err = flag;
+    a.k_pitch = plan.k_pitch;
     for (int i = 0; i < nl; ++i) {
       a.state_in[i] = layers[l0 + i].state_in;
       a.state_out[i] = layers[l0 + i].state_out;

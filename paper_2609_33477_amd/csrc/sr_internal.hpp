@@ -93,6 +93,13 @@ struct ProjConvArgs {
   // blocks appended to the projection's grid; tq_blocks = 0: none
   TailArgs tq;
   int32_t tq_blocks;
+  // Heads whose key width k_real is below the kernel's head width D (the
+  // rectangular-head variant; no q or z columns): each key head takes D
+  // output columns, its last D - k_real zero, and Kbuf keeps that padded
+  // [H_k][T][D] layout; value heads are v_head columns wide ([H_v][T][v_head]).
+  // Weight segments, fp8 scales, conv taps and the tail are in the caller's
+  // unpadded channel order.  0, 0 for square heads.
+  int32_t k_real, v_head;
 };
 
 // The projections of up to kProjBatch layers of one call in one launch: every
@@ -163,6 +170,7 @@ struct ScanArgs {
   const int32_t* err;   // the call's table-check flag: non-zero = write nothing
   const float* state_in[kScanMaxLayers];
   float* state_out[kScanMaxLayers];
+  int32_t k_pitch;      // elements per K row (0: d_k); rectangular heads: 128 (padded keys)
 };
 
 hipError_t launch_scan(int op_dtype, int d_head, const ScanArgs& a, hipStream_t s);

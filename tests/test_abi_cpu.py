@@ -264,9 +264,13 @@ def test_rect_heads_host_checks():
     rect = Shape(3840, 30, 30, 96, 192)
     T = 1000
     ws = sr.replay_workspace_size(rect, 1, T)
-    # unfused: the fp32 projection rows, bf16 k | v, fp32 gates
-    n = 30 * 96 + 30 * 192 + 60
-    assert ws >= T * n * 4 + T * 30 * (96 + 192) * 2 + 2 * T * 30 * 4
+    # an even number of value heads takes the fused projection: row info,
+    # bf16 keys padded to 128 columns, bf16 values, fp32 gates
+    assert ws >= T * 16 + T * 30 * (128 + 192) * 2 + 2 * T * 30 * 4
+    # an odd number takes the unfused path: fp32 projection rows, bf16 k | v
+    odd = Shape(256, 1, 3, 96, 192)
+    n = 96 + 3 * 192 + 6
+    assert sr.replay_workspace_size(odd, 1, T) >= T * n * 4 + T * (96 + 3 * 192) * 2 + 2 * T * 3 * 4
     for bad in (Shape(256, 2, 2, 96, 96), Shape(256, 2, 2, 64, 192), Shape(256, 2, 2, 192, 96),
                 Shape(256, 2, 2, 96, 128)):
         with pytest.raises(sr.SrError) as e:

@@ -1,9 +1,11 @@
 """GPU parity of heads whose key and value widths differ (Appendix A:
-OLMo-Hybrid-7B, d_k = 96, d_v = 192) against the fp64 oracle: the unfused
-bf16 path (projection GEMM, one-head-per-wave conv/gates, the q-tail blocks
-on their own) and the state-only chunk kernel.  Ragged and empty segments,
-sentinel slots, fp8 weights, a short conv, fp32 conv taps and tail, an
-initial state, bitwise determinism, and the model's full shape."""
+OLMo-Hybrid-7B, d_k = 96, d_v = 192) against the fp64 oracle: the fused
+projection with key heads padded to 128 columns (an even number of value
+heads), the unfused bf16 path (projection GEMM, one-head-per-wave
+conv/gates, the q-tail blocks on their own; an odd number), and the
+state-only chunk kernel.  Ragged and empty segments, sentinel slots, fp8
+weights, a short conv, fp32 conv taps and tail, an initial state, bitwise
+determinism, and the model's full shape."""
 import numpy as np
 import pytest
 import torch
@@ -33,6 +35,19 @@ def test_rect_heads_ragged_two_layers():
     for li in range(2):
         assert torch.all(dev.layers[li].state_out[b0] == 0)
         assert torch.all(dev.layers[li].tail_out[b0] == 0)
+
+
+def test_rect_heads_odd_value_heads_unfused():
+    # 3 value heads of 192 columns do not fill whole 128-column blocks: the
+    # unfused path, with GQA (one key head)
+    shape = W.Shape(256, 1, 3, 96, 192)
+    seg = [40, 0, 131, 7]
+    wl = W.make_workload("rect_odd", shape, seg, seed=309)
+    log(f"rect heads, 3 value heads (unfused): T={wl.t_total}")
+    dev = upload(wl)
+    run(dev)
+    check_pairs(dev, _live_pairs(wl), TOL_BF16)
+    assert torch.all(dev.layers[0].state_out[1] == 0)
 
 
 def test_rect_heads_fp8_gqa_sentinels_short_conv():
