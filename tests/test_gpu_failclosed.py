@@ -1,7 +1,8 @@
 """Fail-closed replay on the GPU (Section 5.2: a bad input becomes a cache
 miss, never a corrupt write).  Each bad varlen table below is rejected by the
 device check that runs first in the call: every state and tail stays as it
-was (NaN fill), and the reported mask equals the host twin's.  Every table
+was (NaN fill), and the reported mask equals the host twin's.  So is the
+table of a gather that ran out of output rows.  Every table
 here stays inside the allocated buffers even where the check would not stop
 it (slot ids below the allocated slot count, row offsets below the allocated
 rows), so a broken check shows up as a written output, never as a fault.
@@ -99,3 +100,43 @@ def test_graph_run_with_a_bad_table_writes_nothing():
         assert int(status.item()) == want, (cu, slots)
         assert torch.all(torch.isnan(dev.layers[0].state_out))
     g.close()
+
+
+def _to_dev(a):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).cuda()
+
+
+def test_short_gather_is_refused_by_the_replay():
+    """The read path end to end: a gather whose outputs hold fewer rows than
+    the requests' anchors stops at their capacity but reports the full
+    prefix sums; replaying that many rows with its table is refused on the
+    device (the table's total is not the row count), so a short gather ends
+    as a miss, not as states built from missing rows.  The workspace is
+    sized for every row the table names, so nothing could be read outside it
+    even without the check."""
+    import paper_2609_33477_amd as sr
+    from workloads import sidecar as wsc
+    _, wl, dev, ws, ws_bytes = _setup()
+    cap = 150
+    g = wsc.gather_case(11, SEG, 1, SHAPE.d_model, 2)          # 200 anchors of SHAPE's rows
+    sc = sr.make_sidecar(_to_dev(g.pool), g.n_layers, wsc.PER_PAGE, SHAPE.d_model)
+    rows = torch.zeros((cap, SHAPE.d_model), dtype=torch.int16, device="cuda")
+    cu = torch.full((len(SEG) + 1,), -7, dtype=torch.int32, device="cuda")
+    log(f"short gather: {sum(SEG)} anchors into {cap} rows, then replay of {cap} rows")
+    sr.anchor_gather(sc, _to_dev(g.block_table), _to_dev(g.block_cu), _to_dev(g.anchor_first),
+                     _to_dev(g.n_anchors), [0], [rows], cu)
+    torch.cuda.synchronize()
+    assert cu.cpu().tolist() == [0, 40, 105, 112, 200]
+    layers = layer_tensors(dev)
+    layers[0] = sr.LayerTensors(**{**vars(dev.layers[0]), "anchors": rows.view(torch.bfloat16)})
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    sr.replay_state(SHAPE, layers, len(SEG), cap, cu, dev.slot_ids[:len(SEG)].contiguous(), ws, ws_bytes,
+                    n_slots=ALLOC_SLOTS, varlen_status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == sr.validate_varlen_host(cu.cpu().tolist(), list(range(len(SEG))), cap, ALLOC_SLOTS)
+    assert int(status.item()) == 4                               # the total does not match
+    assert torch.all(torch.isnan(dev.layers[0].state_out))
+    assert torch.all(torch.isnan(dev.layers[0].tail_out.float()))
