@@ -53,6 +53,13 @@
 // W rows hold their columns in the state's k order (32q + 4g .. + 3, then
 // 32q + 16 + 4g .. + 3, at 32q + 8g) so each fragment is one 16-byte read,
 // with the row pitch 8 mod 64 dwords measured conflict free for those.
+//
+// Rectangular heads (SPLIT, d = 128): OLMo-Hybrid's 192-wide value heads
+// arrive as two 96-column halves and its 96-wide keys as 128-column rows,
+// all padded with zeros.  Each half runs as a unit of its own with the head's
+// G, beta and key head; zero key columns leave Gram, T and W those of the
+// real keys, zero value columns stay zero in the state, and the unit reads
+// and writes only its 96 x 96 block of the head's [96][192] state.
 #include "sr_device.hpp"
 
 #include <cstddef>
@@ -182,7 +189,9 @@ __device__ __forceinline__ int kv_off(int r, int cb, int h) {
   return r * 2 * D + 32 * (cb ^ ((r / RPL) % NCP)) + 8 * h;
 }
 
-template <int D>
+// SPLIT: value heads run as several units (the v_split fields of ScanArgs);
+// the square-head kernels are built without it.
+template <int D, bool SPLIT>
 __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(ScanArgs a) {
   if (a.err && *a.err) return;   // the call's table check failed: write nothing
   using CF = Cfg<D>;
@@ -277,14 +286,26 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   auto st_out_of = [&](int layer) {
     return *reinterpret_cast<float* const*>(kargs + offsetof(ScanArgs, state_out) + sizeof(void*) * layer);
   };
+  // Where a unit's state lives: value heads of v_split units each, the
+  // unit's rows < st_rows and columns < st_cols at [row][col] of pitch
+  // st_pitch (D, D, D and one unit per head for square heads)
+  const int vsp = SPLIT ? a.v_split : 1;
+  const int srows = SPLIT ? a.st_rows : D, scols = SPLIT ? a.st_cols : D;
+  const int spitch = SPLIT ? a.st_pitch : D;
+  auto state_base = [&](int slot, int head) {
+    return ((size_t)slot * (a.H_v / vsp) + head / vsp) * srows * spitch + (size_t)(head % vsp) * scols;
+  };
   // live units without rows: their state is the initial one
   for (int k = 0; k < n_rounds; ++k) {
     if (u_slot[k] < 0 || u_s1[k] != u_s0[k]) continue;
     const int layer = u_lh[k] / a.H_v, head = u_lh[k] % a.H_v;
     const float* si = st_in_of(layer);
-    float* so = st_out_of(layer) + ((size_t)u_slot[k] * a.H_v + head) * D * D;
-    const size_t ib = ((size_t)u_slot[k] * a.H_v + head) * D * D;
-    for (int i = tid; i < D * D; i += CF::THREADS) so[i] = si ? si[ib + i] : 0.f;
+    const size_t ib = state_base(u_slot[k], head);
+    float* so = st_out_of(layer) + ib;
+    for (int i = tid; i < srows * scols; i += CF::THREADS) {
+      const size_t o = (size_t)(i / scols) * spitch + i % scols;
+      so[o] = si ? si[ib + o] : 0.f;
+    }
   }
   if (NSC == 0) return;
 
@@ -312,8 +333,8 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     const int hk = (head * a.H_k) / a.H_v;
     c.kp = static_cast<const char*>(a.Kbuf) + (layer * a.k_layer_stride + (int64_t)hk * a.T * D) * 2;
     c.vp = static_cast<const char*>(a.Vbuf) + (layer * a.v_layer_stride + (int64_t)head * a.T * D) * 2;
-    c.gp = a.Gbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
-    c.bp = a.Bbuf + layer * a.g_layer_stride + (int64_t)head * a.T;
+    c.gp = a.Gbuf + layer * a.g_layer_stride + (int64_t)(head / vsp) * a.T;
+    c.bp = a.Bbuf + layer * a.g_layer_stride + (int64_t)(head / vsp) * a.T;
   };
   auto cursor_new = [&]() {
     Cursor c;
@@ -756,8 +777,11 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
   // state) and is stored after its last one.
   Cursor cs = cursor_new();   // unit of sub-chunk n
   auto unit_base = [&](const Cursor& c) {
-    return ((size_t)uni(u_slot[c.k]) * a.H_v + uni(u_lh[c.k]) % a.H_v) * D * D + (size_t)(4 * g) * D + 32 * sw + li;
+    return state_base(uni(u_slot[c.k]), uni(u_lh[c.k]) % a.H_v) + (size_t)(4 * g) * spitch + 32 * sw + li;
   };
+  // this lane's state element (16 td + r, 16 cc) of the wave's columns lies
+  // inside the unit's rows and columns
+  auto in_state = [&](int td, int cc, int r) { return 4 * g + 16 * td + r < srows && 32 * sw + li + 16 * cc < scols; };
   for (int n = -9; n < NSC; ++n) {
     if (n >= 0) {
       if (n >= cs.end) (void)sub(n, cs);
@@ -770,7 +794,7 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
           for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-              M[td][cc][r] = si ? si[base + (size_t)(16 * td + r) * D + 16 * cc] : 0.f;
+              M[td][cc][r] = si && in_state(td, cc, r) ? si[base + (size_t)(16 * td + r) * spitch + 16 * cc] : 0.f;
       }
       state_step();
       if (n + 1 == cs.end) {
@@ -780,7 +804,8 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
 #pragma unroll
           for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) out[(size_t)(16 * td + r) * D + 16 * cc] = M[td][cc][r];
+            for (int r = 0; r < 4; ++r)
+              if (in_state(td, cc, r)) out[(size_t)(16 * td + r) * spitch + 16 * cc] = M[td][cc][r];
       }
     }
     if (n + 1 >= 0 && n + 1 < NSC) load_ops(n + 1);
@@ -801,7 +826,7 @@ int device_cus() {
   return cache[dev];
 }
 
-template <int D>
+template <int D, bool SPLIT = false>
 hipError_t run(const ScanArgs& a, hipStream_t s) {
   const int64_t units = (int64_t)a.n_seg * a.n_layers * a.H_v;
   if (units == 0) return hipSuccess;
@@ -809,13 +834,20 @@ hipError_t run(const ScanArgs& a, hipStream_t s) {
   // (at most kScanUnits)
   int64_t grid = units < device_cus() ? units : device_cus();
   if (grid * kScanUnits < units) grid = (units + kScanUnits - 1) / kScanUnits;
-  hipLaunchKernelGGL((gdn_scan_bf16_kernel<D>), dim3((unsigned)grid), dim3(Cfg<D>::THREADS), 0, s, a);
+  hipLaunchKernelGGL((gdn_scan_bf16_kernel<D, SPLIT>), dim3((unsigned)grid), dim3(Cfg<D>::THREADS), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_scan_bf16(int d_head, const ScanArgs& a, hipStream_t s) {
+  if (a.v_split > 1) {
+    // value heads split into units of 128 state columns (rectangular heads)
+    if (d_head != 128 || a.H_v % a.v_split || a.st_rows <= 0 || a.st_rows > 128 || a.st_cols <= 0 ||
+        a.st_cols > 128 || a.st_pitch < a.v_split * a.st_cols)
+      return hipErrorInvalidValue;
+    return run<128, true>(a, s);
+  }
   switch (d_head) {
     case 32: return run<32>(a, s);
     case 64: return run<64>(a, s);

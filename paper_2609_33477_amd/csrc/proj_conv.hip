@@ -36,9 +36,10 @@
 // Rectangular heads (RECT: OLMo-Hybrid's 96-wide keys and 192-wide values,
 // Appendix A): each key head takes 128 output columns, its last 32 computed
 // from a repeated weight row and zeroed before the conv, so the per-wave key
-// norm is unchanged; keys stay in that padded layout, values are stored in
-// 192-wide heads, and every channel index into the caller's weights,
-// scales, conv taps and tail goes through real_col.  The pad costs a tenth
+// norm is unchanged; keys stay in that padded layout, each value head is
+// stored as two 96-column halves padded the same way (the scan runs them as
+// two square units of 128), and every channel index into the caller's
+// weights, scales, conv taps and tail goes through real_col.  The pad costs a tenth
 // more MFMA work at OLMo's shape, against an unfused projection whose fp32
 // rows went through HBM.
 //
@@ -664,17 +665,21 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
       // scale (1/|k| for keys), round to bf16, store two rows per pack
       const int hh = is_q ? nb / D : (is_k ? (nb - a.C_q) / D : (nb - a.C_k) / D);
       uint16_t* dst = static_cast<uint16_t*>(is_q ? a.Qbuf : (is_k ? a.Kbuf : a.Vbuf)) + ((int64_t)hh * T + t0) * D + lc;
-      // RECT values: block jj of these 128 columns lies in value head
-      // vh = c / v_head at column c % v_head, rows v_head apart
+      // RECT values: value head h (v_head = 2 k_real columns) is stored as
+      // two halves h 2 + e of k_real columns, each padded to D like a key
+      // head ([2 H_v][T][D]).  Block jj of these 128 columns is columns
+      // col .. col + 31 of half vh; the block ending a half also writes the
+      // half's pad columns (zeros).
       uint16_t* vdst[JB];
-      int vpitch = D;
+      bool vpad[JB];
       if constexpr (RECT) {
         if (!is_k) {
-          vpitch = a.v_head;
 #pragma unroll
           for (int jj = 0; jj < JB; ++jj) {
-            const int c = nb - a.C_k + 32 * jj, vh = c / a.v_head;
-            vdst[jj] = static_cast<uint16_t*>(a.Vbuf) + ((int64_t)vh * T + t0) * a.v_head + (c - vh * a.v_head) + lc;
+            const int c = nb - a.C_k + 32 * jj, h = c / a.v_head, j0 = c - h * a.v_head;
+            const int e = j0 / a.k_real, col = j0 - e * a.k_real;
+            vdst[jj] = static_cast<uint16_t*>(a.Vbuf) + ((int64_t)(2 * h + e) * T + t0) * D + col + lc;
+            vpad[jj] = col + 32 == a.k_real;
           }
         }
       }
@@ -698,8 +703,12 @@ __global__ __launch_bounds__(THREADS, 1) void proj_conv_kernel(ProjConvBatch pb,
               const int u = 4 * q + v;
               const uint32_t p = pack_bf16x2(XU(j, u) * iv[v], XU(j, u + 1) * iv[v + 1]);
               if (RECT && !is_k) {
-                st(vdst[jj] + (int64_t)u * vpitch, (uint16_t)(p & 0xffffu), u);
-                st(vdst[jj] + (int64_t)(u + 1) * vpitch, (uint16_t)(p >> 16), u + 1);
+                st(vdst[jj] + (int64_t)u * D, (uint16_t)(p & 0xffffu), u);
+                st(vdst[jj] + (int64_t)(u + 1) * D, (uint16_t)(p >> 16), u + 1);
+                if (vpad[jj]) {
+                  st(vdst[jj] + (int64_t)u * D + 32, (uint16_t)0, u);
+                  st(vdst[jj] + (int64_t)(u + 1) * D + 32, (uint16_t)0, u + 1);
+                }
               } else {
                 st(dst + (int64_t)u * D + 32 * jj, (uint16_t)(p & 0xffffu), u);
                 st(dst + (int64_t)(u + 1) * D + 32 * jj, (uint16_t)(p >> 16), u + 1);
@@ -791,8 +800,9 @@ hipError_t by_head(int d, const ProjConvBatch& a, hipStream_t s) {
     // rectangular heads: key heads padded to 128 columns, no q or z columns
     for (int l = 0; l < a.n_layers; ++l) {
       const ProjConvArgs& x = a.layer[l];
-      if (x.k_real != a.layer[0].k_real || x.v_head != a.layer[0].v_head || x.k_real % 32 || x.k_real > 128 ||
-          x.v_head % 32 || x.v_head <= 0 || x.C_q != 0 || x.C_z != x.C_kv || x.C_k % 128 || (x.C_kv - x.C_k) % 128)
+      if (x.k_real != a.layer[0].k_real || x.v_head != a.layer[0].v_head || x.k_real % 32 || x.k_real >= 128 ||
+          x.k_real + 32 != 128 || x.v_head != 2 * x.k_real || x.C_q != 0 || x.C_z != x.C_kv || x.C_k % 128 ||
+          (x.C_kv - x.C_k) % 128)
         return hipErrorInvalidValue;
     }
     return d == 128 ? run<TB, 128, true>(a, s) : hipErrorInvalidValue;

@@ -12,13 +12,16 @@
 //                  v (bf16, head-major), log2 alpha, beta, the k | v part of
 //                  the conv tail; blocks past the tiles compute its q part.
 //                  96-wide key heads take 128 output columns each (zero
-//                  pads) and land in a padded [H_k][T][128] key buffer
+//                  pads) and land in a padded [H_k][T][128] key buffer; a
+//                  192-wide value head lands as two padded halves, which
+//                  the bf16 scan runs as two units of 128
 // fp32 path, and 96 x 192 heads with an odd number of value heads, per layer:
 //     proj_gemm    anchors x [W_k; W_v; W_a; W_b]^T -> P (fp32 workspace)
 //     conv_gate    P -> k_hat, v, log alpha, beta, k | v tail
 //     tail         q part of the conv tail (+ zeros before a segment's start)
 // then one state launch per group of <= 32 layers writes the states (the
-// pipelined bf16 scan, the fp32 scan, or the chunked kernel for d_k != d_v).
+// pipelined bf16 scan, the fp32 scan, or the chunked kernel for the unfused
+// 96 x 192 heads).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -73,7 +76,7 @@ struct Plan {
   int64_t k_stride, v_stride, g_stride;   // per-layer strides (elements)
   int op_dtype, op_bytes;
   bool fused;                        // bf16 anchors: projection fused with the conv epilogue
-  bool rect;                         // fused rectangular heads: keys padded to 128 columns
+  bool rect;                         // fused rectangular heads: keys and value halves padded to 128 columns
   int k_pitch;                       // elements per K row
 };
 
@@ -96,7 +99,7 @@ Plan make_plan(const sr_shape* s, int32_t n_layers, int64_t T) {
   p.fused = p.op_dtype == SR_BF16 && (s->d_k == s->d_v || p.rect);
   p.k_pitch = p.rect ? 128 : s->d_k;
   p.k_stride = hk * T * p.k_pitch;
-  p.v_stride = hv * T * s->d_v;
+  p.v_stride = p.rect ? 2 * hv * T * p.k_pitch : hv * T * s->d_v;
   p.g_stride = hv * T;
   int64_t off = 0;
   p.off_flag = off; off = align_up(off + 4, kAlign);   // the table check's result word
@@ -402,8 +405,19 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
       a.state_in[i] = layers[l0 + i].state_in;
       a.state_out[i] = layers[l0 + i].state_out;
     }
+    if (plan.rect) {
+      // each value head as two square units of 128 (96 live rows and columns)
+      a.H_v = 2 * hv;
+      a.v_split = 2;
+      a.st_rows = shape->d_k;
+      a.st_cols = shape->d_v / 2;
+      a.st_pitch = shape->d_v;
+    }
     if (shape->recurrence == SR_RECURRENCE_DECAY) {
       if (timed(SR_KERNEL_DECAY_STATE, s, [&] { return sr::launch_decay_state(d, a, s); }) != hipSuccess)
+        return SR_ERR_HIP;
+    } else if (plan.rect) {
+      if (timed(SR_KERNEL_GDN_SCAN, s, [&] { return sr::launch_scan(plan.op_dtype, plan.k_pitch, a, s); }) != hipSuccess)
         return SR_ERR_HIP;
     } else if (shape->d_k != shape->d_v) {
       if (timed(SR_KERNEL_GDN_SCAN, s, [&] { return sr::launch_chunk_state(shape->d_k, shape->d_v, a, s); }) != hipSuccess)

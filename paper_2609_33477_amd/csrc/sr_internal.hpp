@@ -96,7 +96,8 @@ struct ProjConvArgs {
   // Heads whose key width k_real is below the kernel's head width D (the
   // rectangular-head variant; no q or z columns): each key head takes D
   // output columns, its last D - k_real zero, and Kbuf keeps that padded
-  // [H_k][T][D] layout; value heads are v_head columns wide ([H_v][T][v_head]).
+  // [H_k][T][D] layout; value heads are v_head = 2 k_real columns wide and
+  // stored as two halves padded the same way ([2 H_v][T][D], pads zero).
   // Weight segments, fp8 scales, conv taps and the tail are in the caller's
   // unpadded channel order.  0, 0 for square heads.
   int32_t k_real, v_head;
@@ -171,6 +172,12 @@ struct ScanArgs {
   const float* state_in[kScanMaxLayers];
   float* state_out[kScanMaxLayers];
   int32_t k_pitch;      // elements per K row (0: d_k); rectangular heads: 128 (padded keys)
+  // bf16 scan only: each value head runs as v_split units of D state
+  // columns (0 or 1: one unit per head).  H_v and the V planes then count
+  // units; G and beta stay per value head (unit / v_split), and the state of
+  // value head h is [st_rows][st_pitch] fp32 of which unit h v_split + e
+  // holds rows < st_rows, columns [e st_cols, (e + 1) st_cols).  0: D each.
+  int32_t v_split, st_rows, st_cols, st_pitch;
 };
 
 hipError_t launch_scan(int op_dtype, int d_head, const ScanArgs& a, hipStream_t s);

@@ -1,9 +1,10 @@
 """GPU parity of heads whose key and value widths differ (Appendix A:
 OLMo-Hybrid-7B, d_k = 96, d_v = 192) against the fp64 oracle: the fused
-projection with key heads padded to 128 columns (an even number of value
-heads), the unfused bf16 path (projection GEMM, one-head-per-wave
-conv/gates, the q-tail blocks on their own; an odd number), and the
-state-only chunk kernel.  Ragged and empty segments, sentinel slots, fp8
+projection with key heads and value halves padded to 128 columns and the
+pipelined bf16 scan running each value head as two units (an even number
+of value heads), and the unfused bf16 path (projection GEMM,
+one-head-per-wave conv/gates, the q-tail blocks on their own, the
+state-only chunk kernel; an odd number).  Ragged and empty segments, sentinel slots, fp8
 weights, a short conv, fp32 conv taps and tail, an initial state, bitwise
 determinism, and the model's full shape."""
 import numpy as np
