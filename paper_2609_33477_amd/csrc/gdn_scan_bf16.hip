@@ -21,13 +21,14 @@
 //     row-major (m-2 for sub-chunk m, m-1 for m+1);
 //   d/32 state waves, wave s owning state columns [32s, 32s+32) as 2 d/16
 //     16x16 fp32 accumulator tiles for the whole unit: at step n they
-//     run the state lines of sub-chunk n from registers, then read the
-//     operands of sub-chunk n+1, so the reads' latency overlaps the MFMAs
-//     and the barrier.
-// K(n+4) and V(n+3) go global -> LDS by DMA, requested at step n by the prep
-// wave whose phase there is Gram or A (the two lightest) and waited for one
-// step later, so the state waves issue nothing but LDS reads and MFMAs.
-// Rings (sub-chunk slots): K 4, V 3, W 2, Tu 4, gate vectors 16.
+//     run the state lines of sub-chunk n from registers (in phases that
+//     pair MFMA groups with the VALU work they do not wait on), then read
+//     the operands of sub-chunk n+1, so the reads' latency overlaps the
+//     MFMAs and the barrier.
+// K(n+5) and V(n+4) go global -> LDS by DMA, requested at step n by the prep
+// wave whose phase there is Gram or A (the two lightest) and waited for two
+// steps later, so the state waves issue nothing but LDS reads and MFMAs.
+// Rings (sub-chunk slots): K 5, V 4, W 2, Tu 4, gate vectors 16.
 //
 // The grid is one workgroup per CU.  A workgroup runs its units (segment,
 // layer, value head) back to back as one stream of sub-chunks: the pipeline
@@ -46,9 +47,9 @@
 // 16-lane group rows kbase..kbase+3 of column n0 + i when lane j of the group
 // addresses row kbase + j/4, columns n0 + 4 (j%4) .. +3.
 //
-// LDS (d = 128): K and V rings 56 KB, W ring 18 KB, Tu ring 24 KB, gate
+// LDS (d = 128): K and V rings 72 KB, W ring 18 KB, Tu ring 24 KB, gate
 // vectors 4 KB, per prep wave A^T of a pair (reused for Tw^T) and gate
-// scratch 38 KB: ~141 KB, one workgroup (8 waves) per CU.  K and V rows are
+// scratch 38 KB: ~159 KB, one workgroup (8 waves) per CU.  K and V rows are
 // unpadded and XOR-swizzled (kv_off) so the DMA writes whole 1 KB blocks;
 // W rows hold their columns in the state's k order (32q + 4g .. + 3, then
 // 32q + 16 + 4g .. + 3, at 32q + 8g) so each fragment is one 16-byte read,
@@ -151,8 +152,8 @@ struct Cfg {
   static constexpr int DMA_ROWS = 512 / D;            // rows per 1 KB DMA block
   static constexpr int DMA_BLK = kS * 2 * D / 1024;         // 1 KB DMA blocks of one K or V sub-chunk
   static constexpr int WP = D + 16;                   // W row pitch (bf16): 16-byte row reads
-  static constexpr int NK = 4;                        // K ring: K(n) DMA issued at step n-4
-  static constexpr int NV = 3;                        // V ring: V(n) DMA issued at step n-3
+  static constexpr int NK = 5;                        // K ring: K(n) DMA issued at step n-5
+  static constexpr int NV = 4;                        // V ring: V(n) DMA issued at step n-4
   static constexpr int NTU = 4;                       // Tu ring: a pair is packed two steps ahead
   static constexpr int NVEC = 16;                     // gate-vector ring: written nine steps ahead
   static constexpr int SZ_KV = kS * D * 2;            // one sub-chunk of K or V
@@ -366,8 +367,8 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     return r;
   };
 
-  auto kbuf = [&](int m) { return L + CF::OFF_K + (m & (NK - 1)) * CF::SZ_KV; };
-  auto vbuf = [&](int m) { return L + CF::OFF_V + (m % NV) * CF::SZ_KV; };
+  auto kbuf = [&](int m) { return L + CF::OFF_K + (m % NK) * CF::SZ_KV; };
+  auto vbuf = [&](int m) { return L + CF::OFF_V + (m & (NV - 1)) * CF::SZ_KV; };
   auto wbuf = [&](int m) { return L + CF::OFF_W + (m & 1) * CF::SZ_W; };
   auto tubuf = [&](int m) { return L + CF::OFF_TU + (m & (CF::NTU - 1)) * 2 * CF::SZ_TT; };   // Tu_hi^T, then Tu_lo^T
   auto vecbuf = [&](int m) { return (SR_LDS float*)(L + CF::OFF_VEC + (m & (CF::NVEC - 1)) * CF::SZ_VEC); };
@@ -399,10 +400,12 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     float x[kS];           // column `col` of T, carried over the solve phases
 
     // DMA staging of K and V, global -> LDS: at step n the prep wave in its
-    // Gram or A phase (the two lightest) requests K(n + 4) and V(n + 3), all
+    // Gram or A phase (the two lightest) requests K(n + 5) and V(n + 4), all
     // DMA_BLK 1 KB blocks of each, and waits for them at the end of step
-    // n + 1, before the barrier that publishes them (K(j) is read from step
-    // j - 2 on, V(j) at step j - 1).  Lane l carries the 16 bytes at byte
+    // n + 2, before the barrier that publishes them (K(j) is read from step
+    // j - 2 on, V(j) at step j - 1): a DMA has the rest of its step and two
+    // more to land, which covers its latency under load (one step did not:
+    // the A-phase requests then stalled the next phase by ~2K cycles).  Lane l carries the 16 bytes at byte
     // 16 l of a block: dma_off is their byte offset from the sub-chunk's first
     // row in the swizzled layout.  Rows past the segment end are read from
     // its last row: their beta and log decay are 0, so T has unit rows and
@@ -434,32 +437,37 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     // or its A (odd n)
     auto dma_owner = [](int nn) { return ((nn - (nn & 1)) >> 1) & 3; };
     int n = -9;                      // the step; every prep barrier advances it
-    int dma_cur = 0, dma_prev = 0;   // blocks this wave requested in this / the previous step
+    int dma_cur = 0, dma_prev = 0, dma_prev2 = 0;   // blocks this wave requested in this / the previous / the step before
     Cursor cur_k = cursor_new(), cur_v = cur_k, cur_l = cur_k;   // of the K and V DMAs and of the Gram loads
     int64_t pc0[2] = {0, 0}, ps1[2] = {0, 0};   // first row and segment end of the pair being loaded
     auto dma_duty = [&](int nn) {
       if (dma_owner(nn) != p) return;
-      if (nn + 4 >= 0 && nn + 4 < NSC) {
-        const Sub sk = sub(nn + 4, cur_k);
-        stage(sk.kp, sk.c0, sk.s1, kbuf(nn + 4));
+      if (nn + 5 >= 0 && nn + 5 < NSC) {
+        const Sub sk = sub(nn + 5, cur_k);
+        stage(sk.kp, sk.c0, sk.s1, kbuf(nn + 5));
         dma_cur += CF::DMA_BLK;
       }
-      if (nn + 3 >= 0 && nn + 3 < NSC) {
-        const Sub sv = sub(nn + 3, cur_v);
-        stage(sv.vp, sv.c0, sv.s1, vbuf(nn + 3));
+      if (nn + 4 >= 0 && nn + 4 < NSC) {
+        const Sub sv = sub(nn + 4, cur_v);
+        stage(sv.vp, sv.c0, sv.s1, vbuf(nn + 4));
         dma_cur += CF::DMA_BLK;
       }
     };
-    // the barrier that ends step nn: the previous step's requests have
-    // landed (this step's may still be in flight)
+    // the barrier that ends step nn: the requests of step nn - 2 have
+    // landed (those of this step and the previous one may still be in
+    // flight; a wave requests on two consecutive steps, then not for six)
     auto pbar = [&](int& nn) {
-      if (dma_prev) {
-        if (dma_cur == 0) wait_vm<0>();
-        else if (dma_cur == CF::DMA_BLK) wait_vm<CF::DMA_BLK>();
-        else wait_vm<2 * CF::DMA_BLK>();
+      if (dma_prev2) {
+        const int newer = dma_cur + dma_prev;
+        if (newer == 0) wait_vm<0>();
+        else if (newer == CF::DMA_BLK) wait_vm<CF::DMA_BLK>();
+        else if (newer == 2 * CF::DMA_BLK) wait_vm<2 * CF::DMA_BLK>();
+        else if (newer == 3 * CF::DMA_BLK) wait_vm<3 * CF::DMA_BLK>();
+        else wait_vm<4 * CF::DMA_BLK>();
       }
       lds_barrier();
       ++nn;
+      dma_prev2 = dma_prev;
       dma_prev = dma_cur;
       dma_cur = 0;
     };
@@ -734,41 +742,78 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
 #pragma unroll
     for (int td = 0; td < NT; ++td) kt[td] = tr_kv(Kc, td);
   };
-  // the state lines of a sub-chunk for this wave's 32 columns
+  // The state lines of a sub-chunk for this wave's 32 columns, in six phases
+  // that pair each group of MFMAs with VALU work it does not wait on: the
+  // two column tiles cc run one after the other, so the bf16 copies of the
+  // state, its decay and the scaled Delta of one tile are formed under the
+  // other tile's products.  Each accumulator sees its products in the same
+  // order as a plain loop would give them, so the results do not depend on
+  // this schedule.
   auto state_step = [&]() {
-    // U = Tu V for row halves bi and column tiles cc; Delta = U + (-W) M0
     f32x4 dl[2][2];
-#pragma unroll
-    for (int cc = 0; cc < 2; ++cc) {
+    bf16x8 mb[NT / 2], dfr[2];
+    // U = Tu V for row halves bi of column tile cc (the bf16 copy of M0's
+    // tile cc made under those products)
+    auto u_and_copy = [&](int cc) {
       dl[0][cc] = mma_k32(mma_k32(zero4(), t0l, vf[cc]), t0, vf[cc]);
       dl[1][cc] = mma_k32(mma_k32(zero4(), t1l, vf[cc]), t1, vf[cc]);
-    }
 #pragma unroll
-    for (int q = 0; q < NT / 2; ++q) {
-      const bf16x8 m0 = acc_pair(M[2 * q][0], M[2 * q + 1][0]);
-      const bf16x8 m1 = acc_pair(M[2 * q][1], M[2 * q + 1][1]);
+      for (int q = 0; q < NT / 2; ++q) mb[q] = acc_pair(M[2 * q][cc], M[2 * q + 1][cc]);
 #pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-        dl[bi][0] = mma_k32(dl[bi][0], wf[q][bi], m0);
-        dl[bi][1] = mma_k32(dl[bi][1], wf[q][bi], m1);
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, NT / 2, 0);
       }
-    }
-    // scale the rows by 2^{G_31 - G_i}; decay the state; M += K^T Delta
-    bf16x8 dfr[2];
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    // Delta = U + (-W) M0 for column tile cc
+    auto wm = [&](int cc) {
 #pragma unroll
-    for (int cc = 0; cc < 2; ++cc)
+      for (int q = 0; q < NT / 2; ++q)
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi) dl[bi][cc] = mma_k32(dl[bi][cc], wf[q][bi], mb[q]);
+    };
+    // M's tile cc decays once its bf16 copy is made
+    auto decay_tile = [&](int cc, int td0, int td1) {
+#pragma unroll
+      for (int td = td0; td < td1; ++td)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) M[td][cc][r] *= decay;
+    };
+    // rows scaled by 2^{G_31 - G_i}, as the bf16 operand of M += K^T Delta
+    auto scale_delta = [&](int cc) {
       dfr[cc] = as_bf16x8(make_uint4(pack_bf16x2(dl[0][cc][0] * e0.x, dl[0][cc][1] * e0.y),
                                      pack_bf16x2(dl[0][cc][2] * e0.z, dl[0][cc][3] * e0.w),
                                      pack_bf16x2(dl[1][cc][0] * e1.x, dl[1][cc][1] * e1.y),
                                      pack_bf16x2(dl[1][cc][2] * e1.z, dl[1][cc][3] * e1.w)));
+    };
+    auto update = [&](int cc) {
 #pragma unroll
-    for (int td = 0; td < NT; ++td)
+      for (int td = 0; td < NT; ++td) M[td][cc] = mma_k32(M[td][cc], kt[td], dfr[cc]);
+    };
+    // NT MFMAs, each followed by up to 4 VALU instructions
+    auto pair_groups = [&]() {
 #pragma unroll
-      for (int cc = 0; cc < 2; ++cc) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) M[td][cc][r] *= decay;
-        M[td][cc] = mma_k32(M[td][cc], kt[td], dfr[cc]);
+      for (int i = 0; i < NT; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    u_and_copy(0);                       // 1: U of tile 0 | bf16 copy of M0's tile 0
+    wm(0);                               // 2: (-W) M0 into tile 0 | decay of M's tile 0
+    decay_tile(0, 0, NT);
+    pair_groups();
+    u_and_copy(1);                       // 3: U of tile 1 | bf16 copy of M0's tile 1
+    wm(1);                               // 4: (-W) M0 into tile 1 | scaled Delta of tile 0, half the decay of tile 1
+    scale_delta(0);
+    decay_tile(1, 0, NT / 2);
+    pair_groups();
+    update(0);                           // 5: M += K^T Delta for tile 0 | the rest, scaled Delta of tile 1
+    decay_tile(1, NT / 2, NT);
+    scale_delta(1);
+    pair_groups();
+    update(1);                           // 6: M += K^T Delta for tile 1
   };
 
   // ---- steps -9 .. NSC-1: the state lines of sub-chunk n, then the reads
