@@ -405,9 +405,9 @@ __global__ __launch_bounds__(64 * (D / 32 + 4), 1) void gdn_scan_bf16_kernel(Sca
     // n + 2, before the barrier that publishes them (K(j) is read from step
     // j - 2 on, V(j) at step j - 1): a DMA has the rest of its step and two
     // more to land, which covers its latency under load (one step did not:
-    // the A-phase requests then stalled the next phase by ~2K cycles).  Lane l carries the 16 bytes at byte
-    // 16 l of a block: dma_off is their byte offset from the sub-chunk's first
-    // row in the swizzled layout.  Rows past the segment end are read from
+    // the A-phase requests then stalled the next phase by ~2K cycles).
+    // Lane l carries the 16 bytes at byte 16 l of a block: dma_off is their
+    // byte offset from the sub-chunk's first row in the swizzled layout.  Rows past the segment end are read from
     // its last row: their beta and log decay are 0, so T has unit rows and
     // zero columns there and any finite values are multiplied by exact zeros.
     uint32_t dma_off[CF::DMA_BLK];
