@@ -102,3 +102,40 @@ def test_olmo_hybrid_shape():
     dev = upload(wl)
     run(dev)
     check_pairs(dev, _live_pairs(wl), TOL_BF16)
+
+
+def test_rect_heads_graph_and_noalloc_match_eager():
+    """The graph-bucketed replay and the allocation-free entry point take the
+    rectangular-head path through the same sr_replay_state: each must write
+    what the eager call writes, bit for bit (graph: twice, into NaN)."""
+    import paper_2609_33477_amd as sr
+    shape = W.Shape(256, 2, 2, 96, 192)
+    seg = [70, 0, 129]
+    wl = W.make_workload("rect_graph", shape, seg, seed=311, n_slots=4)
+    log(f"rect heads through a graph and the no-alloc entry: T={wl.t_total}")
+    dev = upload(wl)
+    run(dev)
+    L0 = dev.layers[0]
+    ref_s, ref_t = L0.state_out.clone(), L0.tail_out.clone()
+    live = [s for s in wl.slot_ids if s >= 0]
+    layers = [sr.LayerTensors(**vars(ns)) for ns in dev.layers]
+    g = sr.ReplayGraph(shape, layers, max_segments=4, bucket_rows=[256, 512])
+    g.anchors(0)[:wl.t_total].copy_(L0.anchors.view(torch.int16))
+    for rep in range(2):
+        L0.state_out.fill_(float("nan"))
+        L0.tail_out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        used = g.run(len(seg), wl.t_total, dev.cu_seqlens, dev.slot_ids)
+        torch.cuda.synchronize()
+        assert used == 0
+        for s in live:
+            assert torch.equal(L0.state_out[s], ref_s[s]), (rep, s)
+            assert torch.equal(L0.tail_out[s], ref_t[s]), (rep, s)
+    g.close()
+    L0.state_out.fill_(float("nan"))
+    L0.tail_out.fill_(float("nan"))
+    sr.replay_state_noalloc(shape, layers, len(seg), wl.t_total, dev.cu_seqlens, dev.slot_ids)
+    torch.cuda.synchronize()
+    for s in live:
+        assert torch.equal(L0.state_out[s], ref_s[s]), s
+        assert torch.equal(L0.tail_out[s], ref_t[s]), s
