@@ -47,6 +47,7 @@ def log(msg):
 
 
 WARMUP_MIN_S = 0.15   # wall time of untimed steps before any timing
+BREAKDOWN_STEPS = 20  # untimed steps whose every kernel launch is bracketed by events
 
 
 def warm_up(step, n):
@@ -626,8 +627,18 @@ def main():
     warm_run = warm_up(step, args.warmup)
     log(f"{warm_run} warmup steps run")
 
+    # Per-kernel breakdown: a short pass with HIP events around every launch.
+    # The timed steps then bracket only the dominant kernel (its live
+    # duration gives the roofline), so the other kernels run without the
+    # events' overhead (~20 us per step with all of them).
+    sr.kernel_timing_kinds(None)
     sr.kernel_timing_enable(True)
     sr.kernel_timing_read()                       # drop anything recorded before
+    for _ in range(BREAKDOWN_STEPS):
+        step()
+    kt_all = sr.kernel_timing_read()
+    dom = max((k for k, (_, n) in kt_all.items() if n), key=lambda k: kt_all[k][0])
+    sr.kernel_timing_kinds([dom])
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
@@ -638,8 +649,9 @@ def main():
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall) * 1e3
     ms_total = start.elapsed_time(stop)
-    kt = sr.kernel_timing_read()
+    kt_dom = sr.kernel_timing_read()[dom]
     sr.kernel_timing_enable(False)
+    sr.kernel_timing_kinds(None)
     ms_per_step = ms_total / args.steps
     tokens = wl.replayed_tokens
     value = tokens / (ms_per_step / 1e3)
@@ -647,21 +659,24 @@ def main():
 
     work = algorithmic_work(wl, with_q=dev.with_q)
     kernels = {}
-    for k, (tot, n) in kt.items():
+    total_all = max(sum(v[0] for v in kt_all.values()), 1e-12)
+    for k, (tot, n) in kt_all.items():
         if n == 0:
             continue
         bound, amount = work[k]
+        launches = n / BREAKDOWN_STEPS
+        if k == dom:                               # the timed steps' own events
+            tot, n = kt_dom
         avg_ms = tot / n
         if bound == "mfma":
             dt = "f32" if wl.shape.anchor_dtype == "f32" else "bf16"
             ach, peak, unit = amount / (avg_ms * 1e-3) / 1e12, PEAK_TFLOPS[dt], "TFLOP/s"
         else:
             ach, peak, unit = amount / (avg_ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
-        kernels[k] = {"avg_ms": round(avg_ms, 5), "launches_per_step": n / args.steps,
-                      "share": round(tot / max(sum(v[0] for v in kt.values()), 1e-12), 4),
+        kernels[k] = {"avg_ms": round(avg_ms, 5), "launches_per_step": launches,
+                      "share": round(kt_all[k][0] / total_all, 4),
                       "bound": bound, "achieved": round(ach, 2), "peak": peak, "unit": unit,
                       "frac": round(ach / peak, 4)}
-    dom = max(kernels, key=lambda k: kernels[k]["share"])
     d = kernels[dom]
     traffic = measured_traffic(wl.name, dom)
     roofline = {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
@@ -686,6 +701,8 @@ def main():
         "latency_ms": round(ms_per_step, 4),
         "roofline": roofline,
         "kernels": kernels,
+        "kernels_timing": f"{dom}: HIP events around each of its launches in the timed steps; the others: "
+                          f"{BREAKDOWN_STEPS} untimed steps just before, every launch bracketed",
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

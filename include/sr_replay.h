@@ -279,6 +279,10 @@ typedef enum sr_kernel_kind {
  * Not thread-safe; not for use under graph capture. */
 sr_status sr_kernel_timing_enable(int32_t enable);
 sr_status sr_kernel_timing_read(double* ms, int64_t* launches);
+/* The kinds recorded while timing is enabled: bit k of `mask` for kind k
+ * (default: every kind).  Launches of other kinds run without events, so a
+ * benchmark can time one kernel live without bracketing the others. */
+sr_status sr_kernel_timing_kinds(uint32_t mask);
 
 /* Diagnostics for SR_ERR_HIP: the HIP error code (hipError_t) and the
  * sr_kernel_kind of the calling thread's most recent failed launch inside a

@@ -10,7 +10,7 @@ import importlib
 
 _BINDING_NAMES = {
     "LIB_PATH", "SR_BF16", "SR_F32", "SR_FP8_E4M3", "KERNEL_KINDS", "LayerTensors", "SrError",
-    "conv_tail_bytes", "kernel_timing_enable", "kernel_timing_read", "replay_state",
+    "conv_tail_bytes", "kernel_timing_enable", "kernel_timing_read", "kernel_timing_kinds", "replay_state",
     "replay_workspace_size", "state_bytes", "status_str", "SrSidecar", "make_sidecar", "anchor_dest_table",
     "anchor_compact", "anchor_write", "anchor_gather", "ReplayGraph", "SrHostRange", "replay_state_noalloc",
     "NOALLOC_SCRATCH_BYTES", "validate_varlen", "validate_varlen_host", "VARLEN_BAD_START", "VARLEN_NOT_MONOTONE", "VARLEN_BAD_TOTAL",

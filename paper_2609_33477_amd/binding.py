@@ -121,6 +121,8 @@ def _load() -> ctypes.CDLL:
     lib.sr_kernel_timing_enable.restype = ctypes.c_int
     lib.sr_kernel_timing_read.argtypes = [P(ctypes.c_double), P(ctypes.c_int64)]
     lib.sr_kernel_timing_read.restype = ctypes.c_int
+    lib.sr_kernel_timing_kinds.argtypes = [ctypes.c_uint32]
+    lib.sr_kernel_timing_kinds.restype = ctypes.c_int
     lib.sr_last_hip_error.argtypes = [P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_char_p)]
     lib.sr_last_hip_error.restype = ctypes.c_int
     lib.sr_status_str.argtypes = [ctypes.c_int]
@@ -163,7 +165,8 @@ LIB = _load()
 
 EXPORTED_SYMBOLS = ("sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
                     "sr_replay_state", "sr_replay_state_noalloc", "sr_validate_varlen",
-                    "sr_validate_varlen_host", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_last_hip_error",
+                    "sr_validate_varlen_host", "sr_kernel_timing_enable", "sr_kernel_timing_read", "sr_kernel_timing_kinds",
+                    "sr_last_hip_error",
                     "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact", "sr_anchor_write",
                     "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
                     "sr_replay_graph_max_rows", "sr_replay_graph_fetch", "sr_replay_graph_run",
@@ -265,6 +268,13 @@ def make_layer_array(layers: Sequence[LayerTensors]):
 
 def kernel_timing_enable(enable: bool = True):
     _check(LIB.sr_kernel_timing_enable(int(bool(enable))))
+
+
+def kernel_timing_kinds(kinds=None):
+    """Record only these kernel kinds (names of KERNEL_KINDS) while timing is
+    enabled; None: every kind."""
+    mask = 0xFFFFFFFF if kinds is None else sum(1 << KERNEL_KINDS.index(k) for k in kinds)
+    _check(LIB.sr_kernel_timing_kinds(mask))
 
 
 def kernel_timing_read():

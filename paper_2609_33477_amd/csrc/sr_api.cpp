@@ -122,6 +122,7 @@ struct TimedLaunch {
   hipEvent_t start, stop;
 };
 bool g_timing = false;
+uint32_t g_timing_kinds = ~0u;   // kinds bracketed by events while timing is on
 std::vector<TimedLaunch> g_records;
 std::vector<hipEvent_t> g_free_events;
 
@@ -154,7 +155,7 @@ hipError_t note(int kind, hipError_t e) {
 template <typename F>
 hipError_t timed(int kind, hipStream_t s, F&& launch) {
   (void)hipGetLastError();
-  if (!g_timing) return note(kind, launch());
+  if (!g_timing || kind < 0 || kind >= 32 || !((g_timing_kinds >> kind) & 1u)) return note(kind, launch());
   TimedLaunch t{kind, take_event(), take_event()};
   if (!t.start || !t.stop) return note(kind, hipErrorOutOfMemory);
   hipError_t e = hipEventRecord(t.start, s);
@@ -430,6 +431,11 @@ sr_status sr_replay_state(const sr_shape* shape, int32_t n_layers, const sr_laye
 
 sr_status sr_kernel_timing_enable(int32_t enable) {
   g_timing = enable != 0;
+  return SR_OK;
+}
+
+sr_status sr_kernel_timing_kinds(uint32_t mask) {
+  g_timing_kinds = mask;
   return SR_OK;
 }
 

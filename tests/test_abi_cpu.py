@@ -29,7 +29,7 @@ def test_header_declares_and_library_exports_every_function():
     assert set(names) == {"sr_state_bytes", "sr_conv_tail_bytes", "sr_replay_workspace_size",
                           "sr_replay_state", "sr_replay_state_noalloc", "sr_validate_varlen",
                           "sr_validate_varlen_host", "sr_kernel_timing_enable", "sr_kernel_timing_read",
-                          "sr_last_hip_error", "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact",
+                          "sr_kernel_timing_kinds", "sr_last_hip_error", "sr_status_str", "sr_anchor_dest_table", "sr_anchor_compact",
                           "sr_anchor_write", "sr_anchor_gather", "sr_replay_graph_create", "sr_replay_graph_anchors",
                           "sr_replay_graph_max_rows", "sr_replay_graph_fetch", "sr_replay_graph_run",
                           "sr_replay_graph_wait", "sr_replay_graph_destroy", "sr_group_workspace_size",
