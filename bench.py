@@ -71,6 +71,47 @@ def warm_up(step, n):
     return done
 
 
+def timed_steps(step, steps, stream):
+    """Times `steps` calls of step() between two events on `stream`, with the
+    library's HIP events around every launch of the dominant kernel only
+    (its live duration is the roofline's); the dominant kernel and the
+    others' durations come from BREAKDOWN_STEPS untimed steps just before,
+    every launch bracketed.  Events around every kernel inside the timed
+    steps would add their own overhead (~20 us per varlen16 step).
+    Returns (ms per step, wall ms per step, {kind: (ms, launches)} of the
+    breakdown steps with the dominant kind's entry from the timed steps
+    scaled to BREAKDOWN_STEPS, dominant kind)."""
+    import torch
+    import paper_2609_33477_amd as sr
+    sr.kernel_timing_kinds(None)
+    sr.kernel_timing_enable(True)
+    sr.kernel_timing_read()                       # drop anything recorded before
+    for _ in range(BREAKDOWN_STEPS):
+        step()
+    kt = sr.kernel_timing_read()
+    dom = max((k for k, (_, n) in kt.items() if n), key=lambda k: kt[k][0])
+    sr.kernel_timing_kinds([dom])
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for _ in range(steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t_wall) * 1e3 / steps
+    tot, n = sr.kernel_timing_read()[dom]
+    sr.kernel_timing_enable(False)
+    sr.kernel_timing_kinds(None)
+    kt[dom] = (tot * BREAKDOWN_STEPS / steps, n * BREAKDOWN_STEPS // steps)
+    return start.elapsed_time(stop) / steps, wall, kt, dom
+
+
+def kernels_timing_note(dom):
+    return (f"{dom}: HIP events around each of its launches in the timed steps; the others: "
+            f"{BREAKDOWN_STEPS} untimed steps just before, every launch bracketed")
+
+
 PROJ_LAYERS_PER_LAUNCH = 4   # layers of one call that share a fused-projection launch
 
 
@@ -308,28 +349,17 @@ def bench_sidecar(args):
         raise SystemExit(f"unknown sidecar workload {args.workload}")
 
     warm_run = warm_up(step, args.warmup)
-    sr.kernel_timing_enable(True)
-    sr.kernel_timing_read()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(args.steps):
-        step()
-    stop.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = start.elapsed_time(stop) / args.steps
-    kt = sr.kernel_timing_read()
-    sr.kernel_timing_enable(False)
+    ms_per_step, _, kt, dom = timed_steps(step, args.steps, stream)
     kernels = {}
     for k, (tot, cnt) in kt.items():
         if cnt == 0:
             continue
         avg_ms = tot / cnt
         ach = bytes_of[k] / (avg_ms * 1e-3) / 1e9
-        kernels[k] = {"avg_ms": round(avg_ms, 5), "launches_per_step": cnt / args.steps,
+        kernels[k] = {"avg_ms": round(avg_ms, 5), "launches_per_step": cnt / BREAKDOWN_STEPS,
                       "share": round(tot / max(sum(v[0] for v in kt.values()), 1e-12), 4), "bound": "hbm",
                       "bytes": bytes_of[k], "achieved": round(ach, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                       "frac": round(ach / PEAK_HBM_GBS, 4)}
-    dom = max(kernels, key=lambda k: kernels[k]["share"])
     dk = kernels[dom]
     roofline = {"bound": "hbm", "achieved": dk["achieved"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": dk["frac"], "traffic": measured_traffic(args.workload, dom), "kernel": dom}
@@ -340,7 +370,7 @@ def bench_sidecar(args):
            "unit": "rows/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "warmup_run": warm_run,
            "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "bf16", "data": "synthetic", "config": config, "latency_ms": round(ms_per_step, 5),
-           "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu}
+           "roofline": roofline, "kernels": kernels, "kernels_timing": kernels_timing_note(dom), "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
 
 
@@ -512,18 +542,7 @@ def bench_group(args):
 
     log(f"group: T={gw.t_total} rows x {len(blocks)} layers, d_ff {gw.d_ff}, workspace {ws_bytes / 2**20:.1f} MiB")
     warm_run = warm_up(step, args.warmup)
-    sr.kernel_timing_enable(True)
-    sr.kernel_timing_read()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for _ in range(args.steps):
-        step()
-    stop.record(stream)
-    torch.cuda.synchronize()
-    kt = sr.kernel_timing_read()
-    sr.kernel_timing_enable(False)
-    ms = start.elapsed_time(stop) / args.steps
+    ms, _, kt, dom = timed_steps(step, args.steps, stream)
     value = gw.replayed_tokens / (ms / 1e3)
     log(f"{ms:.3f} ms/step, {value / 1e6:.2f} M tokens/s (rows x layers)")
     work = group_work(gw)
@@ -532,16 +551,15 @@ def bench_group(args):
         if cnt == 0:
             continue
         bound, amount = work[k]
-        step_ms = tot / args.steps                           # all launches of the kind in one step
+        step_ms = tot / BREAKDOWN_STEPS                      # all launches of the kind in one step
         if bound == "mfma":
             ach, peak, unit = amount / (step_ms * 1e-3) / 1e12, PEAK_TFLOPS["bf16"], "TFLOP/s"
         else:
             ach, peak, unit = amount / (step_ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
-        kernels[k] = {"ms_per_step": round(step_ms, 5), "launches_per_step": cnt / args.steps,
+        kernels[k] = {"ms_per_step": round(step_ms, 5), "launches_per_step": cnt / BREAKDOWN_STEPS,
                       "share": round(tot / max(sum(v[0] for v in kt.values()), 1e-12), 4),
                       "bound": "mfma" if bound.startswith("mfma") else bound, "achieved": round(ach, 2),
                       "peak": peak, "unit": unit, "frac": round(ach / peak, 4)}
-    dom = max(kernels, key=lambda k: kernels[k]["share"])
     dk = kernels[dom]
     cpu = None
     if not args.no_cpu_baseline:
@@ -570,7 +588,7 @@ def bench_group(args):
            "latency_ms": round(ms, 4),
            "roofline": {"bound": dk["bound"], "achieved": dk["achieved"], "peak": dk["peak"], "unit": dk["unit"],
                         "frac": dk["frac"], "traffic": None, "kernel": dom},
-           "kernels": kernels, "cpu_baseline": cpu}
+           "kernels": kernels, "kernels_timing": kernels_timing_note(dom), "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
 
 
@@ -627,35 +645,11 @@ def main():
     warm_run = warm_up(step, args.warmup)
     log(f"{warm_run} warmup steps run")
 
-    # Per-kernel breakdown: a short pass with HIP events around every launch.
-    # The timed steps then bracket only the dominant kernel (its live
-    # duration gives the roofline), so the other kernels run without the
-    # events' overhead (~20 us per step with all of them).
-    sr.kernel_timing_kinds(None)
-    sr.kernel_timing_enable(True)
-    sr.kernel_timing_read()                       # drop anything recorded before
-    for _ in range(BREAKDOWN_STEPS):
-        step()
-    kt_all = sr.kernel_timing_read()
-    dom = max((k for k, (_, n) in kt_all.items() if n), key=lambda k: kt_all[k][0])
-    sr.kernel_timing_kinds([dom])
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    start.record(stream)
-    for _ in range(args.steps):
-        step()
-    stop.record(stream)
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - t_wall) * 1e3
-    ms_total = start.elapsed_time(stop)
-    kt_dom = sr.kernel_timing_read()[dom]
-    sr.kernel_timing_enable(False)
-    sr.kernel_timing_kinds(None)
-    ms_per_step = ms_total / args.steps
+    ms_per_step, wall_ms, kt_all, dom = timed_steps(step, args.steps, stream)
+
     tokens = wl.replayed_tokens
     value = tokens / (ms_per_step / 1e3)
-    log(f"{ms_per_step:.3f} ms/step (wall {wall_ms / args.steps:.3f}), {value / 1e6:.2f} M tokens/s")
+    log(f"{ms_per_step:.3f} ms/step (wall {wall_ms:.3f}), {value / 1e6:.2f} M tokens/s")
 
     work = algorithmic_work(wl, with_q=dev.with_q)
     kernels = {}
@@ -665,8 +659,6 @@ def main():
             continue
         bound, amount = work[k]
         launches = n / BREAKDOWN_STEPS
-        if k == dom:                               # the timed steps' own events
-            tot, n = kt_dom
         avg_ms = tot / n
         if bound == "mfma":
             dt = "f32" if wl.shape.anchor_dtype == "f32" else "bf16"
@@ -701,8 +693,7 @@ def main():
         "latency_ms": round(ms_per_step, 4),
         "roofline": roofline,
         "kernels": kernels,
-        "kernels_timing": f"{dom}: HIP events around each of its launches in the timed steps; the others: "
-                          f"{BREAKDOWN_STEPS} untimed steps just before, every launch bracketed",
+        "kernels_timing": kernels_timing_note(dom),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
